@@ -1,0 +1,228 @@
+"""Seeded synthetic inputs for the layerwise prefix-KV path.
+
+This module only draws random numbers and random structure.  It is the one
+piece of code that both the CPU oracle and the GPU path consume, so it holds
+none of the method's arithmetic: no KV layout decoding, no paging, no
+attention.  Everything it returns is an input.
+
+Random streams are Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel
+random numbers: as easy as 1, 2, 3", SC'11) as shipped by numpy.  Each stream
+is keyed by (seed, tensor kind, request, layer) through Philox's 128-bit key,
+so any tensor of any layer of any request can be regenerated on its own.
+Normal variates are numpy's float32 standard normal, rounded to bfloat16 with
+round-to-nearest-even.  bfloat16 values are carried as uint16 bit patterns.
+
+The five workload presets carry the shapes the paper evaluates: a Llama 3.1 8B
+shape (32 layers, 32 query / 8 KV heads, head dim 128) at 4K and 64K cached
+prefixes, a concurrent batch of that shape, a 70B shape, and a tiny case.
+"""
+from __future__ import annotations
+
+import math
+import threading
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+# tensor kinds, folded into the Philox key
+KIND_KV = 1        # chunk-object bytes (the cached prefix)
+KIND_Q = 2         # suffix queries
+KIND_KNEW = 3      # suffix keys
+KIND_VNEW = 4      # suffix values
+KIND_TABLE = 5     # block-table permutation
+KIND_LENGTHS = 6   # batch prefix lengths
+
+
+def _philox(seed: int, kind: int, req: int = 0, layer: int = 0) -> np.random.Generator:
+    if not (0 <= req < (1 << 24) and 0 <= layer < (1 << 24) and 0 <= kind < (1 << 16)):
+        raise ValueError("stream coordinates out of range")
+    k1 = (kind << 48) | (req << 24) | layer
+    return np.random.Generator(np.random.Philox(key=[seed & ((1 << 64) - 1), k1]))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bfloat16 (round to nearest, ties to even); NaN stays NaN."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).copy()
+    nan = (u & 0x7FFFFFFF) > 0x7F800000
+    u += ((u >> 16) & 1) + np.uint32(0x7FFF)
+    out = (u >> 16).astype(np.uint16)
+    if nan.any():
+        out[nan] = 0x7FC0
+    return out
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def normal_bf16(seed: int, kind: int, req: int, layer: int, n: int) -> np.ndarray:
+    """n i.i.d. N(0,1) values rounded to bfloat16, from stream (seed, kind, req, layer)."""
+    g = _philox(seed, kind, req, layer)
+    return f32_to_bf16_bits(g.standard_normal(n, dtype=np.float32))
+
+
+# ---------------------------------------------------------------------------
+# cached-prefix bytes
+# ---------------------------------------------------------------------------
+
+def chunk_layer_slices(seed: int, req: int, layer: int, n_chunks: int, slice_elems: int) -> np.ndarray:
+    """Random bfloat16 contents of the layer-`layer` slice of every chunk object.
+
+    Returns uint16 [n_chunks, slice_elems]; row j is the slice that chunk object
+    j stores for that layer.  The values are i.i.d.; this function does not
+    interpret them.
+    """
+    return normal_bf16(seed, KIND_KV, req, layer, n_chunks * slice_elems).reshape(n_chunks, slice_elems)
+
+
+def chunk_objects(seed: int, req: int, num_layers: int, n_chunks: int, slice_elems: int,
+                  threads: int = 8) -> np.ndarray:
+    """The immutable chunk objects of one cached prefix, as an object store holds them.
+
+    Returns uint16 [n_chunks, num_layers, slice_elems]: object j is row j, its
+    num_layers slices stored back to back.  Layers are drawn in parallel threads
+    (numpy releases the GIL while filling).
+    """
+    out = np.empty((n_chunks, num_layers, slice_elems), dtype=np.uint16)
+
+    def work(layers):
+        for l in layers:
+            out[:, l, :] = chunk_layer_slices(seed, req, l, n_chunks, slice_elems)
+
+    threads = max(1, min(threads, num_layers))
+    parts = [list(range(num_layers))[i::threads] for i in range(threads)]
+    ts = [threading.Thread(target=work, args=(p,)) for p in parts]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    return out
+
+
+def suffix_tensor(seed: int, kind: int, req: int, layer: int, shape: Sequence[int]) -> np.ndarray:
+    """Random bfloat16 suffix tensor (queries, new keys or new values) of a layer."""
+    n = int(np.prod(shape))
+    return normal_bf16(seed, kind, req, layer, n).reshape(tuple(shape))
+
+
+# ---------------------------------------------------------------------------
+# random structure: block tables and batch lengths
+# ---------------------------------------------------------------------------
+
+def fisher_yates(seed: int, req: int, n: int) -> np.ndarray:
+    """Uniform random permutation of range(n) by the Fisher-Yates shuffle.
+
+    Uses bounded integer draws from the keyed Philox stream, one per step,
+    so the permutation depends only on (seed, req, n).
+    """
+    g = _philox(seed, KIND_TABLE, req, 0)
+    perm = np.arange(n, dtype=np.int64)
+    if n > 1:
+        # j_i uniform in [0, i] for i = n-1 .. 1
+        highs = np.arange(n - 1, 0, -1, dtype=np.int64)
+        js = g.integers(0, highs + 1)
+        for i, j in zip(highs.tolist(), js.tolist()):
+            perm[i], perm[j] = perm[j], perm[i]
+    return perm
+
+
+def block_tables(seed: int, pages_needed: Sequence[int], pool_pages: int) -> List[np.ndarray]:
+    """Distinct random pool pages for each request.
+
+    A seeded permutation of the pool is dealt round-robin to the requests (one
+    page per request per round, skipping requests that already hold what they
+    need), so requests sharing a pool get interleaved pages.
+    """
+    total = int(sum(pages_needed))
+    if total > pool_pages:
+        raise ValueError("pool too small for the requested pages")
+    perm = fisher_yates(seed, 0, pool_pages)
+    tables = [[] for _ in pages_needed]
+    pos = 0
+    while pos < total:
+        for r, need in enumerate(pages_needed):
+            if len(tables[r]) < need:
+                tables[r].append(int(perm[pos]))
+                pos += 1
+    return [np.asarray(t, dtype=np.int32) for t in tables]
+
+
+def batch_prefix_lengths(seed: int, n_req: int, lo: int, hi: int, quantum: int) -> List[int]:
+    """Log-uniform prefix lengths in [lo, hi], rounded down to whole chunks."""
+    g = _philox(seed, KIND_LENGTHS, 0, 0)
+    u = g.random(n_req)
+    raw = np.exp(math.log(lo) + u * (math.log(hi) - math.log(lo)))
+    return [max(quantum, int(quantum * math.floor(x / quantum))) for x in raw]
+
+
+# ---------------------------------------------------------------------------
+# workload presets
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Workload:
+    name: str
+    num_layers: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    chunk_tokens: int
+    prefix_tokens: List[int]          # per request
+    suffix_tokens: List[int]          # per request
+    pool_pages: int
+    seed: int
+    rate_bytes_per_s: float = 12.5e9  # 100 Gbps producer cap
+    description: str = ""
+
+    @property
+    def n_requests(self) -> int:
+        return len(self.prefix_tokens)
+
+    def pages_needed(self, r: int) -> int:
+        return -(-self.prefix_tokens[r] // self.page_size)
+
+    def n_chunks(self, r: int) -> int:
+        return self.prefix_tokens[r] // self.chunk_tokens
+
+    @property
+    def slice_elems(self) -> int:
+        # elements of one chunk object's layer slice: K and V rows of G tokens
+        return 2 * self.chunk_tokens * self.num_kv_heads * self.head_dim
+
+
+def _single(name, seed, L, nq, nkv, d, tp, ts, pool_mult=4, pool_pages=None, desc=""):
+    need = -(-tp // 16)
+    return Workload(name=name, num_layers=L, num_q_heads=nq, num_kv_heads=nkv, head_dim=d,
+                    page_size=16, chunk_tokens=16, prefix_tokens=[tp], suffix_tokens=[ts],
+                    pool_pages=pool_pages if pool_pages is not None else pool_mult * need,
+                    seed=seed, description=desc)
+
+
+def workload(name: str, seed: Optional[int] = None) -> Workload:
+    """Preset workloads (all G = page size = 16 tokens, bfloat16)."""
+    if name == "tiny":
+        return _single("tiny", seed or 1, 2, 4, 2, 64, 256, 32, pool_pages=64,
+                       desc="2 layers, 4q/2kv, d64, 256-token prefix + 32-token suffix, 64-page pool")
+    if name == "8b-4k":
+        return _single("8b-4k", seed or 2, 32, 32, 8, 128, 4096, 128,
+                       desc="Llama-3-8B shape, 4096-token prefix + 128-token suffix")
+    if name == "8b-64k":
+        return _single("8b-64k", seed or 3, 32, 32, 8, 128, 65536, 512,
+                       desc="Llama-3-8B shape, 65536-token prefix + 512-token suffix")
+    if name == "batch8":
+        s = seed or 4
+        tps = batch_prefix_lengths(s, 8, 4096, 32768, 16)
+        need = sum(-(-t // 16) for t in tps)
+        return Workload(name="batch8", num_layers=32, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                        page_size=16, chunk_tokens=16, prefix_tokens=tps, suffix_tokens=[256] * 8,
+                        pool_pages=4 * need, seed=s,
+                        description="8 requests, Llama-3-8B shape, log-uniform prefixes in [4096, 32768] + 256")
+    if name == "70b-32k":
+        return _single("70b-32k", seed or 5, 80, 64, 8, 128, 32768, 512,
+                       desc="70B shape (80 layers, 64q/8kv, d128), 32768-token prefix + 512-token suffix")
+    raise KeyError(name)
+
+
+WORKLOADS = ["tiny", "8b-4k", "8b-64k", "batch8", "70b-32k"]

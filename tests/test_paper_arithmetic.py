@@ -1,0 +1,102 @@
+"""Paper arithmetic: eq. (1) sizes, the element counts of the aggregation
+table, eq. (3) and the overlap requirement of Section 5.3 against the numbers
+the paper prints."""
+import pytest
+
+import kvgen
+from oracle import model
+from tests.conftest import golden_rows
+
+KiB, MiB, GiB = 1 << 10, 1 << 20, 1 << 30
+L8B, NKV, D = 32, 8, 128
+
+
+def test_eq1_sizes_match_the_paper():
+    want = {r[0]: (float(r[1]), r[2]) for r in golden_rows("kv_sizes.txt")}
+    unit = {"B": 1, "KiB": KiB, "MiB": MiB, "GiB": GiB}
+    b = model.kv_bytes_per_token(L8B, NKV, D) // L8B
+    assert b == want["bytes_per_token_per_layer"][0] * unit[want["bytes_per_token_per_layer"][1]]
+    for key, G in (("layer_slice_16_token_chunk", 16), ("layer_slice_256_token_chunk", 256)):
+        v, u = want[key]
+        assert model.layer_chunk_bytes(G, NKV, D) == v * unit[u]
+    for key, ctx in (("payload_4k_hit_0.875", 4096), ("payload_64k_hit_0.875", 65536)):
+        v, u = want[key]
+        assert int(ctx * 0.875) * L8B * b == v * unit[u]
+
+
+def test_layer_ranges_tile_the_object():
+    S = model.layer_chunk_bytes(16, NKV, D)
+    spans = [model.layer_range(l, S) for l in range(L8B)]
+    assert spans[0][0] == 0 and spans[-1][1] == L8B * S
+    assert all(a[1] == b[0] for a, b in zip(spans, spans[1:]))
+
+
+def test_aggregation_element_counts():
+    for r in golden_rows("lw_opcount.txt"):
+        ctx, G, chunks, elems, agg_mib, per_agg, after, red = map(int, r)
+        n = int(ctx * 0.875) // G
+        assert n == chunks
+        assert n * L8B == elems
+        S = model.layer_chunk_bytes(G, NKV, D)
+        assert agg_mib * MiB // S == per_agg
+        assert elems // per_agg == after and per_agg == red
+
+
+def test_canonical_cells_required_bandwidth():
+    b = model.kv_bytes_per_token(L8B, NKV, D) // L8B
+    for r in golden_rows("canonical_cells.txt"):
+        ctx, hit, cached, t_total, t_layer, req = int(r[0]), float(r[1]), int(r[2]), float(r[3]), float(r[4]), float(r[5])
+        assert int(ctx * hit) == cached
+        assert round(t_total / L8B, 2) == pytest.approx(t_layer, abs=0.006)
+        # Section 5.3: per-layer bytes over the printed per-layer compute time
+        breq = model.required_bandwidth(ctx, hit, NKV, D, t_layer / 1e3)
+        assert breq / 1e9 == pytest.approx(req, abs=0.005)
+        # equivalently total cached bytes over total compute (table caption);
+        # the 4K/87.5% row was evidently computed from the rounded 1.98 ms, so
+        # the total form agrees only to the table's rounding of the time
+        assert cached * L8B * b / (t_total / 1e3) / 1e9 == pytest.approx(req, abs=0.011)
+
+
+def test_eq3_limits():
+    L = 5
+    # transfer-bound: every layer waits for its transfer, then the last compute
+    assert model.layerwise_ttft([4.0] * L, [1.0] * L) == pytest.approx(L * 4.0 + 1.0)
+    # compute-bound: first transfer then back-to-back compute
+    assert model.layerwise_ttft([1.0] * L, [4.0] * L) == pytest.approx(1.0 + L * 4.0)
+    # a single layer is transfer then compute
+    assert model.layerwise_ttft([2.0], [3.0]) == 5.0
+    # never below either the total transfer or the total compute
+    X, C = [3, 1, 4, 1, 5], [2, 7, 1, 8, 2]
+    t = model.layerwise_ttft(X, C)
+    assert t >= sum(X) and t >= sum(C)
+
+
+def test_eq2_mode_dispatch():
+    S = model.layer_chunk_bytes(16, NKV, D)
+    theta = 512 * 1e6
+    # Section 3.4: with theta about 512 MB the 4K configurations stay chunkwise
+    # and the 16K/64K ones go layerwise
+    assert model.mode_dispatch(int(4096 * 0.875) // 16, L8B, S, theta) == "chunkwise"
+    assert model.mode_dispatch(int(16384 * 0.5) // 16, L8B, S, theta) == "layerwise"
+    assert model.mode_dispatch(int(65536 * 0.875) // 16, L8B, S, theta) == "layerwise"
+
+
+def test_stall_and_zero_stall_rate():
+    s, c = 10.0, 2.0
+    r = model.zero_stall_rate(s, c)
+    assert model.per_layer_stall(s, r, c) == 0.0
+    assert model.per_layer_stall(s, r / 2, c) == pytest.approx(c)
+    assert model.per_layer_stall(s, 2 * r, c) == 0.0
+
+
+def test_workload_presets_sizes():
+    w = kvgen.workload("8b-64k")
+    assert w.slice_elems * 2 == 64 * KiB
+    assert w.n_chunks(0) * w.slice_elems * 2 == 256 * MiB           # one layer payload
+    assert w.num_layers * w.n_chunks(0) * w.slice_elems * 2 == 8 * GiB
+    w70 = kvgen.workload("70b-32k")
+    assert model.kv_bytes_per_token(80, 8, 128) == 320 * KiB
+    assert w70.num_layers * w70.n_chunks(0) * w70.slice_elems * 2 == 10 * GiB
+    wb = kvgen.workload("batch8")
+    assert all(4096 <= t <= 32768 and t % 16 == 0 for t in wb.prefix_tokens)
+    assert len(set(wb.prefix_tokens)) > 1

@@ -1,0 +1,224 @@
+/*
+ * objectcache.h -- C ABI of the MI355X layerwise prefix-KV library.
+ *
+ * A reused prefix KV cache arrives one layer at a time as a single contiguous,
+ * layer-major payload (the storage server's per-layer aggregation of all
+ * matched chunk objects, Section 3.3 of the ObjectCache paper).  This library
+ * unpacks each layer payload into a paged KV pool through a block table and
+ * runs the suffix-prefill GQA attention of that layer over the cached prefix
+ * plus the new suffix tokens, while the next layer is still landing
+ * (layerwise prefetch, Section 3.5, eq. (3)).
+ *
+ * Conventions for every entry point:
+ *   - Element type is bfloat16 (2 bytes) for K, V, Q and outputs; the paper's
+ *     eq. (1) uses p = 2 bytes per element.
+ *   - Device pointers are HIP device memory owned by the caller; they must
+ *     stay valid until the stream the call was enqueued on is synchronised.
+ *     Host pointers are read during the call only, except where stated.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Single-layer calls are asynchronous on that stream.
+ *   - Return value: OC_OK (0) or a negative oc_status.  Arguments are fully
+ *     validated before anything is launched; on error nothing is enqueued and
+ *     oc_last_error() returns a message (thread-local, valid until the next
+ *     call on the same thread).  No C++ exception crosses this boundary.
+ *   - The library never allocates device memory inside the single-layer
+ *     calls; scratch space is the caller's `workspace`.
+ */
+#ifndef OBJECTCACHE_H
+#define OBJECTCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OC_ABI_VERSION 1
+
+typedef enum {
+    OC_OK = 0,
+    OC_EINVAL = -1,    /* null pointer, bad enum, negative size            */
+    OC_ESHAPE = -2,    /* shapes disagree (S != 2*G*n_kv*d*2, n_q % n_kv)  */
+    OC_EALIGN = -3,    /* pointer not 16-byte aligned                      */
+    OC_ERANGE = -4,    /* layer or page index out of range, table too short */
+    OC_EHIP = -5,      /* the HIP runtime reported an error                */
+    OC_ETIMEOUT = -6,  /* a layer did not arrive within the timeout        */
+    OC_ENOMEM = -7,    /* host/pinned/device allocation failed (contexts)  */
+    OC_EABORT = -8     /* the producer stopped before delivering a layer   */
+} oc_status;
+
+/* Model and paging layout (Section 2.1, eq. (1); Table "ObjectCache request
+ * descriptor" fields num_layers L and chunk_tokens G).  The per-layer chunk
+ * slice is S = 2 * G * n_kv * d * 2 bytes. */
+typedef struct {
+    int32_t num_layers;     /* L                                              */
+    int32_t num_q_heads;    /* n_q, a multiple of n_kv (GQA)                  */
+    int32_t num_kv_heads;   /* n_kv                                           */
+    int32_t head_dim;       /* d, 64 or 128                                   */
+    int32_t page_size;      /* tokens per pool page, a multiple of 8          */
+    int32_t chunk_tokens;   /* G, tokens per stored chunk                     */
+    int64_t num_pages;      /* P, pages in the pool                           */
+} oc_layout;
+
+/* Paged KV pool, device memory of L*2*P*n_kv*page_size*d bfloat16 values laid
+ * out [L][2][P][n_kv][block].  The block of (layer, K, page, head) is
+ * [slot][dim]; the block of (layer, V, page, head) is [dim][slot] (values
+ * transposed inside the page so the attention reads keys contiguously).
+ * 16-byte aligned. */
+typedef struct {
+    void *base;
+    oc_layout layout;
+} oc_kv_pool;
+
+/* Block table of one request: device int32 page ids.  Logical prefix token T
+ * lives in page pages[T / page_size] at slot T % page_size.  num_tokens is the
+ * cached prefix length; num_entries >= ceil(num_tokens / page_size).  Page ids
+ * must be distinct and in [0, P); the kernels trust them (validate with
+ * oc_block_table_check when the table is not trusted). */
+typedef struct {
+    const int32_t *pages;
+    int64_t num_entries;
+    int64_t num_tokens;
+} oc_block_table;
+
+/* One layer's staging payload in device memory (the "client buffer" of the
+ * layerwise GET): the concatenation, in prefix order, of the layer slice of
+ * each of num_chunks chunk objects.  Each slice is KV_L2TD (Section 3.3):
+ * the K matrix then the V matrix, each [G tokens][n_kv heads][d].
+ * per_layer_chunk_bytes is S. */
+typedef struct {
+    const void *data;
+    int64_t num_chunks;
+    int64_t per_layer_chunk_bytes;
+} oc_staging;
+
+/* Library version (OC_ABI_VERSION) */
+int oc_abi_version(void);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char *oc_last_error(void);
+
+/* Host-side check of a block table held in HOST memory: every entry needed
+ * for num_tokens tokens is in [0, P) and no page repeats.  Returns OC_OK or
+ * OC_ERANGE. */
+int oc_block_table_check(const int32_t *host_pages, int64_t num_entries, int64_t num_tokens,
+                         int64_t num_pages, int32_t page_size);
+
+/* Layer ingest (unpack + scatter): copy every K and V row of the staging
+ * payload of `layer` into the pool pages named by the block table.
+ * Requirements: S == 2*G*n_kv*d*2, num_chunks*G == block_table->num_tokens,
+ * 0 <= layer < L, data/base 16-byte aligned.  Bytes are copied exactly (NaN
+ * and denormal patterns included); pool slots past the prefix are not
+ * written.  Asynchronous on `stream`. */
+int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_table,
+                       oc_kv_pool *kv_pool, int32_t layer, void *stream);
+
+/* Inverse of the ingest: read the prefix of `layer` out of the pool into a
+ * staging-layout device buffer (the layout a chunk object's layer slice has;
+ * the write-back direction).  Same requirements as oc_kv_layer_ingest. */
+int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool,
+                       int32_t layer, void *staging_out, int64_t num_chunks,
+                       int64_t per_layer_chunk_bytes, void *stream);
+
+/* Bytes of device workspace oc_suffix_prefill_layer needs for these lengths. */
+size_t oc_attention_workspace_bytes(const oc_layout *layout, int64_t prefix_tokens,
+                                    int64_t suffix_tokens);
+
+/* Suffix-prefill GQA attention of one layer (the compute the miss tokens
+ * expose per layer, Section 3.5):
+ *   out[i][h][:] = sum_j softmax_j(q[i][h].k_j[g] / sqrt(d)) v_j[g],
+ *   g = h / (n_q / n_kv), j over the prefix tokens 0..T_p-1 read from the pool
+ *   through the block table (T_p = block_table->num_tokens), then the suffix
+ *   tokens 0..i from k_new/v_new (causal within the suffix).
+ * q, out: device [suffix_tokens][n_q][d]; k_new, v_new: device
+ * [suffix_tokens][n_kv][d]; bfloat16, 16-byte aligned.  Scores and
+ * accumulation are fp32; out is rounded to bfloat16 (nearest even).
+ * workspace: device, at least oc_attention_workspace_bytes(), 256-byte
+ * aligned.  suffix_tokens >= 1.  Asynchronous on `stream`. */
+int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
+                            int64_t suffix_tokens, const oc_kv_pool *kv_pool,
+                            const oc_block_table *block_table, int32_t layer, void *out,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Layerwise pipeline (Section 3.5, eq. (3)): for every layer, the payload
+ * lands (host producer -> pinned slot -> DMA into an HBM slot), is ingested
+ * into the pool, and the layer's attention runs on a second stream as soon
+ * as that layer is in; layer l+1 lands and is ingested while layer l
+ * computes.  The producer stands in for the storage server's layerwise GET:
+ * it assembles each layer payload from the chunk objects in prefix order
+ * (appendix pseudocode "layerwise GET"), paced to a byte rate, and signals
+ * layer-ready.  With several requests, layers are delivered layer-major,
+ * request-minor (round-robin), all requests sharing one rate.
+ * ------------------------------------------------------------------------- */
+
+typedef enum {
+    OC_MODE_HBM_RESIDENT = 0,  /* pool already holds the prefix: attention only          */
+    OC_MODE_DEVICE_STAGED = 1, /* payloads already in HBM: ingest + attention, 2 streams  */
+    OC_MODE_PRODUCER = 2       /* host producer -> pinned -> HBM -> ingest -> attention   */
+} oc_mode;
+
+typedef enum {
+    OC_FAULT_NONE = 0,
+    OC_FAULT_STALL = 1,        /* producer stops delivering at fault_layer (tests timeouts) */
+    OC_FAULT_ABORT = 2         /* producer gives up at fault_layer (tests error paths)      */
+} oc_fault;
+
+typedef struct {
+    int32_t mode;              /* oc_mode                                                  */
+    double rate_bytes_per_s;   /* producer pacing; 0 = as fast as memcpy goes              */
+    int64_t piece_bytes;       /* pacing/copy granularity (default 1 MiB when 0)           */
+    int32_t slots;             /* pinned and HBM staging slots (>= 2; default 3 when 0)    */
+    int32_t producer_threads;  /* memcpy threads (default 4 when 0)                        */
+    int32_t timeout_ms;        /* wait limit per layer (default 60000 when 0)              */
+    int32_t fault;             /* oc_fault, test injection                                 */
+    int32_t fault_layer;       /* layer at which the fault triggers                        */
+} oc_pipeline_opts;
+
+/* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */
+typedef struct {
+    int64_t prefix_tokens;                /* T_p = num_chunks * G                          */
+    int64_t suffix_tokens;                /* T_s >= 1                                      */
+    const oc_block_table *block_table;    /* device table covering T_p                     */
+    const void *const *chunk_objects;     /* PRODUCER: host, num_chunks objects, each L*S
+                                             bytes (KV_L2TD, all layers); read during run   */
+    const void *device_payload;           /* DEVICE_STAGED: device, L payloads of T_p*b
+                                             bytes back to back (b = 2*n_kv*d*2)           */
+    const void *q;                        /* device [L][T_s][n_q][d]                       */
+    const void *k_new;                    /* device [L][T_s][n_kv][d]                      */
+    const void *v_new;                    /* device [L][T_s][n_kv][d]                      */
+    void *out;                            /* device [L][T_s][n_q][d]                       */
+} oc_request;
+
+/* Per-request timings (milliseconds from the start of the run, all on one
+ * clock).  Arrays, when non-NULL, are caller-owned with num_layers entries. */
+typedef struct {
+    double ttft_ms;            /* start -> this request's last layer done          */
+    double *produced_ms;       /* host: layer payload fully in its pinned slot     */
+    double *landed_ms;         /* device: payload in HBM (layer-ready)             */
+    double *ingested_ms;       /* device: ingest kernel finished                   */
+    double *done_ms;           /* device: attention finished                       */
+} oc_request_stats;
+
+/* Create a context on `device` for one pool.  Allocates the streams, events,
+ * pinned and HBM staging rings (slots * max_layer_bytes each) and the
+ * attention workspace for up to max_prefix_tokens / max_suffix_tokens, and
+ * keeps them until oc_context_destroy.  The pool stays caller-owned. */
+int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_opts *opts,
+                      int64_t max_prefix_tokens, int64_t max_suffix_tokens, void **ctx);
+
+/* Run the pipeline over n_reqs requests for all L layers; synchronous.
+ * stats (optional) has n_reqs entries.  On OC_ETIMEOUT / OC_EABORT the run is
+ * stopped, all enqueued GPU work is drained and the context stays usable. */
+int oc_pipeline_run(void *ctx, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats);
+
+/* Time of the whole last run (ms, start -> last layer of the last request). */
+double oc_pipeline_last_ms(void *ctx);
+
+void oc_context_destroy(void *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OBJECTCACHE_H */

@@ -1,0 +1,203 @@
+"""ctypes binding of ``libobjectcache.so`` -- argument marshalling only.
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of the method: it turns torch tensors (device memory owned by the
+caller) and Python ints into the C structs of ``include/objectcache.h`` and
+raises ``OcError`` on a non-zero status.  The library must have been built
+(``python -m paper_2605_22850_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_double, c_int, c_int32, c_int64, c_size_t, c_void_p
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libobjectcache.so")
+
+OC_OK, OC_EINVAL, OC_ESHAPE, OC_EALIGN, OC_ERANGE, OC_EHIP, OC_ETIMEOUT, OC_ENOMEM, OC_EABORT = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8
+OC_MODE_HBM_RESIDENT, OC_MODE_DEVICE_STAGED, OC_MODE_PRODUCER = 0, 1, 2
+OC_FAULT_NONE, OC_FAULT_STALL, OC_FAULT_ABORT = 0, 1, 2
+
+EXPORTS = [
+    "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather",
+    "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
+    "oc_pipeline_last_ms", "oc_context_destroy",
+]
+
+
+class OcError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"objectcache status {status}: {msg}")
+        self.status = status
+
+
+class c_layout(ctypes.Structure):
+    _fields_ = [("num_layers", c_int32), ("num_q_heads", c_int32), ("num_kv_heads", c_int32),
+                ("head_dim", c_int32), ("page_size", c_int32), ("chunk_tokens", c_int32),
+                ("num_pages", c_int64)]
+
+
+class c_kv_pool(ctypes.Structure):
+    _fields_ = [("base", c_void_p), ("layout", c_layout)]
+
+
+class c_block_table(ctypes.Structure):
+    _fields_ = [("pages", c_void_p), ("num_entries", c_int64), ("num_tokens", c_int64)]
+
+
+class c_staging(ctypes.Structure):
+    _fields_ = [("data", c_void_p), ("num_chunks", c_int64), ("per_layer_chunk_bytes", c_int64)]
+
+
+class c_pipeline_opts(ctypes.Structure):
+    _fields_ = [("mode", c_int32), ("rate_bytes_per_s", c_double), ("piece_bytes", c_int64),
+                ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
+                ("fault", c_int32), ("fault_layer", c_int32)]
+
+
+class c_request(ctypes.Structure):
+    _fields_ = [("prefix_tokens", c_int64), ("suffix_tokens", c_int64), ("block_table", POINTER(c_block_table)),
+                ("chunk_objects", POINTER(c_void_p)), ("device_payload", c_void_p), ("q", c_void_p),
+                ("k_new", c_void_p), ("v_new", c_void_p), ("out", c_void_p)]
+
+
+class c_request_stats(ctypes.Structure):
+    _fields_ = [("ttft_ms", c_double), ("produced_ms", POINTER(c_double)), ("landed_ms", POINTER(c_double)),
+                ("ingested_ms", POINTER(c_double)), ("done_ms", POINTER(c_double))]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2605_22850_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.oc_abi_version.restype = c_int
+        L.oc_last_error.restype = ctypes.c_char_p
+        L.oc_block_table_check.argtypes = [c_void_p, c_int64, c_int64, c_int64, c_int32]
+        L.oc_kv_layer_ingest.argtypes = [POINTER(c_staging), POINTER(c_block_table), POINTER(c_kv_pool), c_int32,
+                                         c_void_p]
+        L.oc_kv_layer_gather.argtypes = [POINTER(c_block_table), POINTER(c_kv_pool), c_int32, c_void_p, c_int64,
+                                         c_int64, c_void_p]
+        L.oc_attention_workspace_bytes.argtypes = [POINTER(c_layout), c_int64, c_int64]
+        L.oc_attention_workspace_bytes.restype = c_size_t
+        L.oc_suffix_prefill_layer.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, POINTER(c_kv_pool),
+                                              POINTER(c_block_table), c_int32, c_void_p, c_void_p, c_size_t,
+                                              c_void_p]
+        if hasattr(L, "oc_pipeline_run"):
+            L.oc_context_create.argtypes = [c_int, POINTER(c_kv_pool), POINTER(c_pipeline_opts), c_int64, c_int64,
+                                            POINTER(c_void_p)]
+            L.oc_context_create.restype = c_int
+            L.oc_pipeline_run.argtypes = [c_void_p, POINTER(c_request), c_int32, POINTER(c_request_stats)]
+            L.oc_pipeline_run.restype = c_int
+            L.oc_pipeline_last_ms.argtypes = [c_void_p]
+            L.oc_pipeline_last_ms.restype = c_double
+            L.oc_context_destroy.argtypes = [c_void_p]
+            L.oc_context_destroy.restype = None
+        for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather", "oc_suffix_prefill_layer"):
+            getattr(L, name).restype = c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != OC_OK:
+        raise OcError(rc, lib().oc_last_error().decode())
+
+
+@dataclass
+class Layout:
+    num_layers: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    chunk_tokens: int
+    num_pages: int
+
+    def c(self) -> c_layout:
+        return c_layout(self.num_layers, self.num_q_heads, self.num_kv_heads, self.head_dim, self.page_size,
+                        self.chunk_tokens, self.num_pages)
+
+    @property
+    def slice_bytes(self) -> int:
+        """S of eq. (1) with 2-byte elements."""
+        return 2 * self.chunk_tokens * self.num_kv_heads * self.head_dim * 2
+
+    @property
+    def pool_elems(self) -> int:
+        return self.num_layers * 2 * self.num_pages * self.num_kv_heads * self.page_size * self.head_dim
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def make_pool(pool, layout: Layout) -> c_kv_pool:
+    return c_kv_pool(_ptr(pool), layout.c())
+
+
+def make_table(pages, num_tokens: int) -> c_block_table:
+    n = 0 if pages is None else pages.numel()
+    return c_block_table(_ptr(pages) if n else None, n, num_tokens)
+
+
+def oc_abi_version() -> int:
+    return lib().oc_abi_version()
+
+
+def oc_block_table_check(host_pages, num_tokens: int, num_pages: int, page_size: int) -> None:
+    import numpy as np
+    a = np.ascontiguousarray(host_pages, dtype=np.int32)
+    _check(lib().oc_block_table_check(a.ctypes.data if a.size else None, a.size, num_tokens, num_pages, page_size))
+
+
+def oc_kv_layer_ingest(staging, num_chunks: int, pages, num_tokens: int, pool, layout: Layout, layer: int,
+                       stream=None) -> None:
+    st = c_staging(_ptr(staging), num_chunks, layout.slice_bytes)
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_kv_layer_ingest(ctypes.byref(st), ctypes.byref(bt), ctypes.byref(kp), layer, _stream(stream)))
+
+
+def oc_kv_layer_gather(pages, num_tokens: int, pool, layout: Layout, layer: int, staging_out, num_chunks: int,
+                       stream=None) -> None:
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_kv_layer_gather(ctypes.byref(bt), ctypes.byref(kp), layer, _ptr(staging_out), num_chunks,
+                                    layout.slice_bytes, _stream(stream)))
+
+
+def oc_attention_workspace_bytes(layout: Layout, prefix_tokens: int, suffix_tokens: int) -> int:
+    lay = layout.c()
+    n = lib().oc_attention_workspace_bytes(ctypes.byref(lay), prefix_tokens, suffix_tokens)
+    if n == 0:
+        raise OcError(OC_EINVAL, lib().oc_last_error().decode() or "unsupported attention shape")
+    return n
+
+
+def oc_suffix_prefill_layer(q, k_new, v_new, suffix_tokens: int, pool, layout: Layout, pages, num_tokens: int,
+                            layer: int, out, workspace, stream=None) -> None:
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_suffix_prefill_layer(_ptr(q), _ptr(k_new), _ptr(v_new), suffix_tokens, ctypes.byref(kp),
+                                         ctypes.byref(bt), layer, _ptr(out), _ptr(workspace), workspace.numel() *
+                                         workspace.element_size(), _stream(stream)))

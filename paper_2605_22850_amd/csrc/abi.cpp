@@ -1,0 +1,196 @@
+// C entry points for single-layer calls: argument validation, then launch.
+// Nothing is enqueued unless every check passes.
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+
+namespace oc {
+
+static thread_local std::string g_err;
+
+void set_error(const std::string &msg) { g_err = msg; }
+void clear_error() { g_err.clear(); }
+int fail(int status, const std::string &msg) {
+    g_err = msg;
+    return status;
+}
+int hip_fail(hipError_t e, const char *what) {
+    g_err = std::string(what) + ": " + hipGetErrorString(e);
+    return OC_EHIP;
+}
+
+static int check_layout(const oc_layout &l) {
+    if (l.num_layers < 1 || l.num_q_heads < 1 || l.num_kv_heads < 1 || l.head_dim < 1 || l.page_size < 1 ||
+        l.chunk_tokens < 1 || l.num_pages < 1)
+        return fail(OC_EINVAL, "layout fields must be positive");
+    if (l.num_q_heads % l.num_kv_heads != 0) return fail(OC_ESHAPE, "num_q_heads must be a multiple of num_kv_heads");
+    if (l.head_dim % 8 != 0) return fail(OC_ESHAPE, "head_dim must be a multiple of 8");
+    if (l.page_size % 8 != 0) return fail(OC_ESHAPE, "page_size must be a multiple of 8");
+    if (ingest_heads_per_block(l.num_kv_heads, l.head_dim, l.page_size) == 0)
+        return fail(OC_ESHAPE, "one page of one head does not fit the 64 KiB transpose stage");
+    return OC_OK;
+}
+
+static int check_table(const oc_block_table *bt, const oc_layout &l) {
+    if (!bt) return fail(OC_EINVAL, "block_table is NULL");
+    if (bt->num_tokens < 0 || bt->num_entries < 0) return fail(OC_EINVAL, "negative block table size");
+    const int64_t need = (bt->num_tokens + l.page_size - 1) / l.page_size;
+    if (bt->num_entries < need) return fail(OC_ERANGE, "block table shorter than the prefix needs");
+    if (need > 0 && !bt->pages) return fail(OC_EINVAL, "block table pages pointer is NULL");
+    if (need > l.num_pages) return fail(OC_ERANGE, "prefix needs more pages than the pool has");
+    return OC_OK;
+}
+
+static IngestArgs ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, int32_t layer,
+                              const void *staging) {
+    const oc_layout &l = pool->layout;
+    IngestArgs a{};
+    const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+    uint16_t *base = static_cast<uint16_t *>(pool->base);
+    a.staging = static_cast<const uint16_t *>(staging);
+    a.pool_k = base + ((int64_t)layer * 2 + 0) * l.num_pages * block;
+    a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
+    a.pages = bt->pages;
+    a.num_tokens = bt->num_tokens;
+    a.G = l.chunk_tokens;
+    a.n_kv = l.num_kv_heads;
+    a.d = l.head_dim;
+    a.Ps = l.page_size;
+    a.heads_per_block = ingest_heads_per_block(l.num_kv_heads, l.head_dim, l.page_size);
+    return a;
+}
+
+static int check_staging_shape(const oc_layout &l, const oc_block_table *bt, int64_t num_chunks,
+                               int64_t slice_bytes) {
+    const int64_t S = 2LL * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
+    if (num_chunks < 0) return fail(OC_EINVAL, "negative num_chunks");
+    if (slice_bytes != S)
+        return fail(OC_ESHAPE, "per_layer_chunk_bytes must equal 2*G*n_kv*d*2 = " + std::to_string(S));
+    if (num_chunks * l.chunk_tokens != bt->num_tokens)
+        return fail(OC_ESHAPE, "num_chunks * chunk_tokens must equal the block table's num_tokens");
+    return OC_OK;
+}
+
+}  // namespace oc
+
+using namespace oc;
+
+extern "C" {
+
+int oc_abi_version(void) { return OC_ABI_VERSION; }
+
+const char *oc_last_error(void) { return g_err.c_str(); }
+
+int oc_block_table_check(const int32_t *host_pages, int64_t num_entries, int64_t num_tokens, int64_t num_pages,
+                         int32_t page_size) {
+    clear_error();
+    if (page_size < 1 || num_tokens < 0 || num_entries < 0 || num_pages < 1)
+        return fail(OC_EINVAL, "bad sizes");
+    const int64_t need = (num_tokens + page_size - 1) / page_size;
+    if (num_entries < need) return fail(OC_ERANGE, "block table shorter than the prefix needs");
+    if (need > 0 && !host_pages) return fail(OC_EINVAL, "pages is NULL");
+    std::vector<unsigned char> seen((size_t)num_pages, 0);
+    for (int64_t i = 0; i < need; ++i) {
+        const int64_t p = host_pages[i];
+        if (p < 0 || p >= num_pages) return fail(OC_ERANGE, "page id " + std::to_string(p) + " out of range");
+        if (seen[(size_t)p]) return fail(OC_ERANGE, "page id " + std::to_string(p) + " repeats");
+        seen[(size_t)p] = 1;
+    }
+    return OC_OK;
+}
+
+int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_table, oc_kv_pool *kv_pool,
+                       int32_t layer, void *stream) {
+    clear_error();
+    if (!staging || !kv_pool) return fail(OC_EINVAL, "staging and kv_pool must not be NULL");
+    int rc = check_layout(kv_pool->layout);
+    if (rc) return rc;
+    const oc_layout &l = kv_pool->layout;
+    if ((rc = check_table(block_table, l))) return rc;
+    if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
+    if ((rc = check_staging_shape(l, block_table, staging->num_chunks, staging->per_layer_chunk_bytes))) return rc;
+    if (block_table->num_tokens == 0) return OC_OK;
+    if (!staging->data || !kv_pool->base) return fail(OC_EINVAL, "NULL data or pool base");
+    if (!aligned(staging->data, 16) || !aligned(kv_pool->base, 16))
+        return fail(OC_EALIGN, "staging data and pool base must be 16-byte aligned");
+    IngestArgs a = ingest_args(kv_pool, block_table, layer, staging->data);
+    const int64_t n_pages = (block_table->num_tokens + l.page_size - 1) / l.page_size;
+    OC_HIP(launch_ingest(a, n_pages, static_cast<hipStream_t>(stream)));
+    return OC_OK;
+}
+
+int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int32_t layer,
+                       void *staging_out, int64_t num_chunks, int64_t per_layer_chunk_bytes, void *stream) {
+    clear_error();
+    if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
+    int rc = check_layout(kv_pool->layout);
+    if (rc) return rc;
+    const oc_layout &l = kv_pool->layout;
+    if ((rc = check_table(block_table, l))) return rc;
+    if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
+    if ((rc = check_staging_shape(l, block_table, num_chunks, per_layer_chunk_bytes))) return rc;
+    if (block_table->num_tokens == 0) return OC_OK;
+    if (!staging_out || !kv_pool->base) return fail(OC_EINVAL, "NULL staging_out or pool base");
+    if (!aligned(staging_out, 16) || !aligned(kv_pool->base, 16))
+        return fail(OC_EALIGN, "staging and pool base must be 16-byte aligned");
+    IngestArgs a = ingest_args(kv_pool, block_table, layer, nullptr);
+    const int64_t n_pages = (block_table->num_tokens + l.page_size - 1) / l.page_size;
+    OC_HIP(launch_gather(a, static_cast<uint16_t *>(staging_out), n_pages, static_cast<hipStream_t>(stream)));
+    return OC_OK;
+}
+
+static int check_attention_layout(const oc_layout &l) {
+    int rc = check_layout(l);
+    if (rc) return rc;
+    if (l.head_dim != 64 && l.head_dim != 128) return fail(OC_ESHAPE, "attention supports head_dim 64 or 128");
+    if (l.page_size != 16) return fail(OC_ESHAPE, "attention supports page_size 16");
+    return OC_OK;
+}
+
+size_t oc_attention_workspace_bytes(const oc_layout *layout, int64_t prefix_tokens, int64_t suffix_tokens) {
+    clear_error();
+    if (!layout || prefix_tokens < 0 || suffix_tokens < 1 || check_attention_layout(*layout)) return 0;
+    AttnPlan p;
+    plan_attention(*layout, prefix_tokens, suffix_tokens, &p);
+    return p.total;
+}
+
+int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                            const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
+                            void *workspace, size_t workspace_bytes, void *stream) {
+    clear_error();
+    if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
+    int rc = check_attention_layout(kv_pool->layout);
+    if (rc) return rc;
+    const oc_layout &l = kv_pool->layout;
+    if ((rc = check_table(block_table, l))) return rc;
+    if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
+    if (suffix_tokens < 1) return fail(OC_EINVAL, "suffix_tokens must be >= 1");
+    if (!q || !k_new || !v_new || !out || !workspace) return fail(OC_EINVAL, "NULL tensor or workspace");
+    if (block_table->num_tokens > 0 && !kv_pool->base) return fail(OC_EINVAL, "NULL pool base");
+    if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(out, 16) ||
+        !aligned(kv_pool->base, 16))
+        return fail(OC_EALIGN, "q, k_new, v_new, out and pool base must be 16-byte aligned");
+    if (!aligned(workspace, 256)) return fail(OC_EALIGN, "workspace must be 256-byte aligned");
+    AttnPlan p;
+    plan_attention(l, block_table->num_tokens, suffix_tokens, &p);
+    if (workspace_bytes < p.total)
+        return fail(OC_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
+    AttnArgs a{};
+    const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+    const uint16_t *base = static_cast<const uint16_t *>(kv_pool->base);
+    a.q = static_cast<const uint16_t *>(q);
+    a.k_new = static_cast<const uint16_t *>(k_new);
+    a.v_new = static_cast<const uint16_t *>(v_new);
+    a.pool_k = base + ((int64_t)layer * 2 + 0) * l.num_pages * block;
+    a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
+    a.pages = block_table->pages;
+    a.out = static_cast<uint16_t *>(out);
+    a.ws = static_cast<unsigned char *>(workspace);
+    OC_HIP(launch_attention(p, a, static_cast<hipStream_t>(stream)));
+    return OC_OK;
+}
+
+}  // extern "C"

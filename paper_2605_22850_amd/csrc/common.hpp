@@ -1,0 +1,68 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "objectcache.h"
+
+namespace oc {
+
+// thread-local error message behind oc_last_error()
+void set_error(const std::string &msg);
+void clear_error();
+int fail(int status, const std::string &msg);
+int hip_fail(hipError_t e, const char *what);
+
+#define OC_HIP(call)                                 \
+    do {                                             \
+        hipError_t e_ = (call);                      \
+        if (e_ != hipSuccess) return oc::hip_fail(e_, #call); \
+    } while (0)
+
+inline bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// ---- ingest / gather ------------------------------------------------------
+struct IngestArgs {
+    const uint16_t *staging;   // one layer payload [N][2][G][n_kv][d]
+    uint16_t *pool_k;          // pool + ((layer*2+0)*P) * n_kv * Ps * d
+    uint16_t *pool_v;          // pool + ((layer*2+1)*P) * n_kv * Ps * d
+    const int32_t *pages;
+    int64_t num_tokens;        // T_p
+    int32_t G, n_kv, d, Ps;
+    int32_t heads_per_block;   // heads one workgroup moves
+};
+hipError_t launch_ingest(const IngestArgs &a, int64_t n_pages_used, hipStream_t s);
+hipError_t launch_gather(const IngestArgs &a, uint16_t *staging_out, int64_t n_pages_used,
+                         hipStream_t s);
+int ingest_heads_per_block(int n_kv, int d, int Ps);
+
+// ---- attention --------------------------------------------------------------
+struct AttnPlan {
+    int64_t Tp, Ts;
+    int32_t nq, nkv, grp, d;
+    int64_t rows;              // Ts * grp rows per KV head
+    int32_t m_tiles;           // row tiles per KV head
+    int32_t n_split;           // key-range splits
+    int64_t n_pre_pages;       // ceil(Tp / 16)
+    int64_t n_suf_pages;       // ceil(Ts / 16)
+    int64_t n_blocks;          // key blocks of 64 keys over prefix then suffix pages
+    int64_t blocks_per_split;
+    // workspace carve-up (byte offsets)
+    size_t off_ks, off_vs, off_o, off_ml, total;
+};
+int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *plan);
+
+struct AttnArgs {
+    const uint16_t *q, *k_new, *v_new;
+    const uint16_t *pool_k, *pool_v;   // layer bases as in IngestArgs
+    const int32_t *pages;
+    uint16_t *out;
+    unsigned char *ws;
+};
+hipError_t launch_attention(const AttnPlan &p, const AttnArgs &a, hipStream_t s);
+
+}  // namespace oc

@@ -1,0 +1,562 @@
+// Layerwise pipeline (Section 3.5, eq. (3)) with a host producer standing in
+// for the storage server's layerwise GET (Section 3.3 and the appendix
+// pseudocode): for each layer, in prefix order, the producer copies that
+// layer's slice of every matched chunk object into a pinned slot, paced to a
+// byte rate, and then signals layer-ready.  The driver thread lands the slot
+// in HBM with an asynchronous DMA on the copy stream and ingests it there;
+// the compute stream waits on the layer's ingested event and runs that
+// layer's attention.  So layer l+1 lands and is ingested while layer l
+// computes, and every hand-off is a HIP event, never a device-wide sync.
+//
+// Slot reuse: the pinned slot of item k is refilled for item k+slots only
+// after item k's DMA has completed (landed event); the HBM slot is reused
+// in copy-stream order, after the ingest that read it.
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "common.hpp"
+
+namespace oc {
+
+using Clock = std::chrono::steady_clock;
+
+struct Slot {
+    void *pinned = nullptr;
+    void *device = nullptr;
+};
+
+struct Context {
+    int device = 0;
+    oc_kv_pool pool{};
+    oc_pipeline_opts opts{};
+    int64_t max_prefix = 0, max_suffix = 0;
+    size_t slot_bytes = 0;
+    hipStream_t copy = nullptr, compute = nullptr;
+    std::vector<Slot> slots;
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+    std::vector<hipEvent_t> events;    // pool of timing events, reused across runs
+    double last_ms = 0.0;
+};
+
+// ---- shared state between the driver and the producer ----------------------
+struct RunShared {
+    std::mutex mu;
+    std::condition_variable cv;
+    int64_t ready = 0;            // items whose payload is complete in a pinned slot
+    int64_t landed_recorded = 0;  // items whose landed event has been recorded
+    bool abort = false;           // driver -> producer: stop now
+    int producer_status = OC_OK;  // producer -> driver
+    std::string producer_msg;
+};
+
+struct Item {
+    int32_t layer;
+    int32_t req;
+};
+
+static int fill_defaults(oc_pipeline_opts &o) {
+    if (o.piece_bytes <= 0) o.piece_bytes = 1 << 20;
+    if (o.slots <= 0) o.slots = 3;
+    if (o.producer_threads <= 0) o.producer_threads = 4;
+    if (o.timeout_ms <= 0) o.timeout_ms = 60000;
+    if (o.slots < 2) return fail(OC_EINVAL, "at least 2 staging slots are needed");
+    if (o.producer_threads > 64) return fail(OC_EINVAL, "producer_threads must be <= 64");
+    if (o.mode < OC_MODE_HBM_RESIDENT || o.mode > OC_MODE_PRODUCER) return fail(OC_EINVAL, "unknown mode");
+    if (o.rate_bytes_per_s < 0) return fail(OC_EINVAL, "negative rate");
+    return OC_OK;
+}
+
+static void release(Context *c) {
+    if (!c) return;
+    if (c->copy) hipStreamSynchronize(c->copy);
+    if (c->compute) hipStreamSynchronize(c->compute);
+    for (auto &s : c->slots) {
+        if (s.pinned) hipHostFree(s.pinned);
+        if (s.device) hipFree(s.device);
+    }
+    for (auto e : c->events) hipEventDestroy(e);
+    if (c->ws) hipFree(c->ws);
+    if (c->copy) hipStreamDestroy(c->copy);
+    if (c->compute) hipStreamDestroy(c->compute);
+    delete c;
+}
+
+// ---- producer -------------------------------------------------------------
+// Copies item after item into pinned slots.  Pieces of an item go to a pool
+// of worker threads; piece p of the run may start once the wall clock has
+// reached  t0 + (bytes delivered before it + its own bytes) / rate.
+struct Producer {
+    Context *c;
+    RunShared *sh;
+    const oc_request *reqs;
+    const std::vector<Item> *items;
+    Clock::time_point t0;
+    std::vector<double> *produced_ms;   // per item
+    std::vector<hipEvent_t> *landed;    // per item
+    double rate;
+    int64_t S;                          // bytes per chunk slice
+    int32_t L;
+
+    // per-item work shared with the workers
+    std::mutex wmu;
+    std::condition_variable wcv;
+    int64_t cur_item = -1, next_piece = 0, n_pieces = 0, pieces_done = 0, chunks_per_piece = 1;
+    double cum_before = 0.0;            // bytes delivered before the current item
+    bool stop = false;
+
+    bool aborted() {
+        std::lock_guard<std::mutex> g(sh->mu);
+        return sh->abort;
+    }
+
+    void worker() {
+        for (;;) {
+            int64_t item, p, cpp;
+            double cum;
+            {
+                std::unique_lock<std::mutex> lk(wmu);
+                wcv.wait(lk, [&] { return stop || (cur_item >= 0 && next_piece < n_pieces); });
+                if (stop) return;
+                item = cur_item;
+                p = next_piece++;
+                cpp = chunks_per_piece;
+                cum = cum_before;
+            }
+            const Item it = (*items)[item];
+            const oc_request &r = reqs[it.req];
+            const int64_t N = r.prefix_tokens / c->pool.layout.chunk_tokens;
+            const int64_t j0 = p * cpp, j1 = std::min(N, j0 + cpp);
+            if (rate > 0) {
+                const double t_release = (cum + (double)j1 * S) / rate;
+                const auto when = t0 + std::chrono::duration_cast<Clock::duration>(std::chrono::duration<double>(t_release));
+                // sleep most of the way, then spin for a microsecond-accurate release
+                for (;;) {
+                    auto now = Clock::now();
+                    if (now >= when) break;
+                    auto left = when - now;
+                    if (left > std::chrono::microseconds(200)) std::this_thread::sleep_for(left - std::chrono::microseconds(100));
+                }
+            }
+            unsigned char *dst = static_cast<unsigned char *>(c->slots[item % c->slots.size()].pinned);
+            for (int64_t j = j0; j < j1; ++j) {
+                const unsigned char *obj = static_cast<const unsigned char *>(r.chunk_objects[j]);
+                std::memcpy(dst + j * S, obj + (int64_t)it.layer * S, (size_t)S);
+            }
+            {
+                std::lock_guard<std::mutex> g(wmu);
+                ++pieces_done;
+            }
+            wcv.notify_all();
+        }
+    }
+
+    void set_error(int st, const char *msg) {
+        std::lock_guard<std::mutex> g(sh->mu);
+        if (sh->producer_status == OC_OK) {
+            sh->producer_status = st;
+            sh->producer_msg = msg;
+        }
+        sh->cv.notify_all();
+    }
+
+    void run() {
+        const int nw = c->opts.producer_threads;
+        std::vector<std::thread> pool;
+        pool.reserve(nw);
+        for (int i = 0; i < nw; ++i) pool.emplace_back([this] { worker(); });
+        double cum = 0.0;
+        const int64_t n_items = (int64_t)items->size();
+        const int64_t nslots = (int64_t)c->slots.size();
+        for (int64_t k = 0; k < n_items; ++k) {
+            const Item it = (*items)[k];
+            if (c->opts.fault != OC_FAULT_NONE && it.layer == c->opts.fault_layer) {
+                if (c->opts.fault == OC_FAULT_ABORT) {
+                    set_error(OC_EABORT, "producer aborted (injected fault)");
+                    break;
+                }
+                // injected stall: deliver nothing more until the driver gives up
+                std::unique_lock<std::mutex> lk(sh->mu);
+                sh->cv.wait(lk, [&] { return sh->abort; });
+                break;
+            }
+            // the pinned slot is free once the DMA of item k - slots has landed
+            if (k >= nslots) {
+                const int64_t prev = k - nslots;
+                std::unique_lock<std::mutex> lk(sh->mu);
+                sh->cv.wait(lk, [&] { return sh->abort || sh->landed_recorded > prev; });
+                if (sh->abort) break;
+                lk.unlock();
+                if (hipEventSynchronize((*landed)[prev]) != hipSuccess) {
+                    set_error(OC_EHIP, "hipEventSynchronize on a landed event failed");
+                    break;
+                }
+            }
+            if (aborted()) break;
+            const oc_request &r = reqs[it.req];
+            const int64_t N = r.prefix_tokens / c->pool.layout.chunk_tokens;
+            {
+                std::lock_guard<std::mutex> g(wmu);
+                chunks_per_piece = std::max<int64_t>(1, c->opts.piece_bytes / S);
+                n_pieces = (N + chunks_per_piece - 1) / chunks_per_piece;
+                next_piece = 0;
+                pieces_done = 0;
+                cum_before = cum;
+                cur_item = k;
+            }
+            wcv.notify_all();
+            {
+                std::unique_lock<std::mutex> lk(wmu);
+                wcv.wait(lk, [&] { return pieces_done == n_pieces; });
+                cur_item = -1;
+            }
+            cum += (double)N * S;
+            (*produced_ms)[k] = std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
+            {
+                std::lock_guard<std::mutex> g(sh->mu);
+                sh->ready = k + 1;
+            }
+            sh->cv.notify_all();
+        }
+        {
+            std::lock_guard<std::mutex> g(wmu);
+            stop = true;
+        }
+        wcv.notify_all();
+        for (auto &t : pool) t.join();
+    }
+};
+
+static int validate_requests(Context *c, const oc_request *reqs, int32_t n) {
+    const oc_layout &l = c->pool.layout;
+    const int mode = c->opts.mode;
+    for (int32_t i = 0; i < n; ++i) {
+        const oc_request &r = reqs[i];
+        const std::string who = "request " + std::to_string(i) + ": ";
+        if (!r.block_table) return fail(OC_EINVAL, who + "block_table is NULL");
+        if (r.prefix_tokens < 0 || r.suffix_tokens < 1) return fail(OC_EINVAL, who + "bad lengths");
+        if (r.prefix_tokens != r.block_table->num_tokens)
+            return fail(OC_ESHAPE, who + "prefix_tokens differs from the block table's num_tokens");
+        if (r.prefix_tokens % l.chunk_tokens) return fail(OC_ESHAPE, who + "prefix is not a whole number of chunks");
+        if (r.prefix_tokens > c->max_prefix || r.suffix_tokens > c->max_suffix)
+            return fail(OC_ERANGE, who + "longer than the context was created for");
+        const int64_t need = (r.prefix_tokens + l.page_size - 1) / l.page_size;
+        if (r.block_table->num_entries < need) return fail(OC_ERANGE, who + "block table too short");
+        if (need > 0 && !r.block_table->pages) return fail(OC_EINVAL, who + "NULL block table pages");
+        if (!r.q || !r.k_new || !r.v_new || !r.out) return fail(OC_EINVAL, who + "NULL q/k_new/v_new/out");
+        if (!aligned(r.q, 16) || !aligned(r.k_new, 16) || !aligned(r.v_new, 16) || !aligned(r.out, 16))
+            return fail(OC_EALIGN, who + "q/k_new/v_new/out must be 16-byte aligned");
+        if (mode == OC_MODE_DEVICE_STAGED && r.prefix_tokens > 0) {
+            if (!r.device_payload) return fail(OC_EINVAL, who + "DEVICE_STAGED needs device_payload");
+            if (!aligned(r.device_payload, 16)) return fail(OC_EALIGN, who + "device_payload must be 16-byte aligned");
+        }
+        if (mode == OC_MODE_PRODUCER && r.prefix_tokens > 0) {
+            if (!r.chunk_objects) return fail(OC_EINVAL, who + "PRODUCER needs chunk_objects");
+            const int64_t N = r.prefix_tokens / l.chunk_tokens;
+            for (int64_t j = 0; j < N; ++j)
+                if (!r.chunk_objects[j]) return fail(OC_EINVAL, who + "NULL chunk object");
+        }
+    }
+    return OC_OK;
+}
+
+static double ev_ms(hipEvent_t a, hipEvent_t b) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return -1.0;
+    return ms;
+}
+
+static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
+    const oc_layout &l = c->pool.layout;
+    const int32_t L = l.num_layers;
+    const int mode = c->opts.mode;
+    const int64_t b_tok = 2LL * l.num_kv_heads * l.head_dim * 2;     // bytes per token per layer
+    const int64_t S = b_tok * l.chunk_tokens;
+
+    // attention workspace large enough for every request
+    size_t ws_need = 0;
+    for (int32_t i = 0; i < n_reqs; ++i) {
+        AttnPlan p;
+        plan_attention(l, reqs[i].prefix_tokens, reqs[i].suffix_tokens, &p);
+        ws_need = std::max(ws_need, p.total);
+    }
+    if (ws_need > c->ws_bytes) {
+        if (c->ws) OC_HIP(hipFree(c->ws));
+        c->ws = nullptr;
+        c->ws_bytes = 0;
+        if (hipMalloc(&c->ws, ws_need) != hipSuccess) return fail(OC_ENOMEM, "attention workspace allocation failed");
+        c->ws_bytes = ws_need;
+    }
+
+    std::vector<Item> items;
+    for (int32_t layer = 0; layer < L; ++layer)
+        for (int32_t r = 0; r < n_reqs; ++r) items.push_back({layer, r});
+    const int64_t n_items = (int64_t)items.size();
+
+    // events: start + landed/ingested/done per item
+    const size_t n_ev = 1 + 3 * (size_t)n_items;
+    while (c->events.size() < n_ev) {
+        hipEvent_t e;
+        OC_HIP(hipEventCreate(&e));
+        c->events.push_back(e);
+    }
+    hipEvent_t ev_start = c->events[0];
+    std::vector<hipEvent_t> landed(c->events.begin() + 1, c->events.begin() + 1 + n_items);
+    std::vector<hipEvent_t> ingested(c->events.begin() + 1 + n_items, c->events.begin() + 1 + 2 * n_items);
+    std::vector<hipEvent_t> done(c->events.begin() + 1 + 2 * n_items, c->events.begin() + 1 + 3 * n_items);
+    std::vector<double> produced(n_items, -1.0);
+
+    OC_HIP(hipSetDevice(c->device));
+    OC_HIP(hipStreamSynchronize(c->copy));
+    OC_HIP(hipStreamSynchronize(c->compute));
+
+    RunShared sh;
+    Producer prod{};
+    std::thread producer_thread;
+    const hipStream_t first = mode == OC_MODE_HBM_RESIDENT ? c->compute : c->copy;
+    OC_HIP(hipEventRecord(ev_start, first));
+    if (mode != OC_MODE_HBM_RESIDENT) OC_HIP(hipStreamWaitEvent(c->compute, ev_start, 0));
+    const Clock::time_point t0 = Clock::now();
+
+    if (mode == OC_MODE_PRODUCER) {
+        prod.c = c;
+        prod.sh = &sh;
+        prod.reqs = reqs;
+        prod.items = &items;
+        prod.t0 = t0;
+        prod.produced_ms = &produced;
+        prod.landed = &landed;
+        prod.rate = c->opts.rate_bytes_per_s;
+        prod.S = S;
+        prod.L = L;
+        producer_thread = std::thread([&prod] { prod.run(); });
+    }
+
+    int status = OC_OK;
+    std::string msg;
+    for (int64_t k = 0; k < n_items && status == OC_OK; ++k) {
+        const Item it = items[k];
+        const oc_request &r = reqs[it.req];
+        const int64_t layer_bytes = r.prefix_tokens * b_tok;
+        const int64_t N = r.prefix_tokens / l.chunk_tokens;
+        const void *payload = nullptr;
+        if (mode == OC_MODE_PRODUCER) {
+            std::unique_lock<std::mutex> lk(sh.mu);
+            const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
+            const bool ok = sh.cv.wait_until(lk, deadline, [&] { return sh.ready > k || sh.producer_status != OC_OK; });
+            if (sh.producer_status != OC_OK) {
+                status = sh.producer_status;
+                msg = sh.producer_msg;
+                break;
+            }
+            if (!ok) {
+                status = OC_ETIMEOUT;
+                msg = "layer " + std::to_string(it.layer) + " of request " + std::to_string(it.req) +
+                      " did not arrive within " + std::to_string(c->opts.timeout_ms) + " ms";
+                break;
+            }
+            lk.unlock();
+            Slot &s = c->slots[k % c->slots.size()];
+            hipError_t e = layer_bytes ? hipMemcpyAsync(s.device, s.pinned, (size_t)layer_bytes,
+                                                        hipMemcpyHostToDevice, c->copy)
+                                       : hipSuccess;
+            if (e == hipSuccess) e = hipEventRecord(landed[k], c->copy);
+            {
+                std::lock_guard<std::mutex> g(sh.mu);
+                sh.landed_recorded = k + 1;
+            }
+            sh.cv.notify_all();
+            if (e != hipSuccess) {
+                status = hip_fail(e, "landing a layer payload");
+                msg = oc_last_error();
+                break;
+            }
+            payload = s.device;
+        } else if (mode == OC_MODE_DEVICE_STAGED) {
+            payload = static_cast<const unsigned char *>(r.device_payload) + (int64_t)it.layer * layer_bytes;
+            hipError_t e = hipEventRecord(landed[k], c->copy);
+            if (e != hipSuccess) {
+                status = hip_fail(e, "hipEventRecord");
+                msg = oc_last_error();
+                break;
+            }
+        }
+        hipError_t e = hipSuccess;
+        hipStream_t attn_stream = c->compute;
+        if (mode != OC_MODE_HBM_RESIDENT) {
+            if (N > 0) {
+                oc_kv_pool pool = c->pool;
+                oc_block_table bt = *r.block_table;
+                IngestArgs a{};
+                const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+                uint16_t *base = static_cast<uint16_t *>(pool.base);
+                a.staging = static_cast<const uint16_t *>(payload);
+                a.pool_k = base + ((int64_t)it.layer * 2 + 0) * l.num_pages * block;
+                a.pool_v = base + ((int64_t)it.layer * 2 + 1) * l.num_pages * block;
+                a.pages = bt.pages;
+                a.num_tokens = bt.num_tokens;
+                a.G = l.chunk_tokens;
+                a.n_kv = l.num_kv_heads;
+                a.d = l.head_dim;
+                a.Ps = l.page_size;
+                a.heads_per_block = ingest_heads_per_block(l.num_kv_heads, l.head_dim, l.page_size);
+                e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy);
+            }
+            if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
+            if (e == hipSuccess) e = hipStreamWaitEvent(c->compute, ingested[k], 0);
+        } else {
+            e = hipEventRecord(landed[k], c->compute);
+            if (e == hipSuccess) e = hipEventRecord(ingested[k], c->compute);
+        }
+        if (e == hipSuccess) {
+            AttnPlan p;
+            plan_attention(l, r.prefix_tokens, r.suffix_tokens, &p);
+            AttnArgs a{};
+            const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+            const uint16_t *base = static_cast<const uint16_t *>(c->pool.base);
+            const int64_t q_stride = r.suffix_tokens * l.num_q_heads * l.head_dim;
+            const int64_t kv_stride = r.suffix_tokens * l.num_kv_heads * l.head_dim;
+            a.q = static_cast<const uint16_t *>(r.q) + it.layer * q_stride;
+            a.k_new = static_cast<const uint16_t *>(r.k_new) + it.layer * kv_stride;
+            a.v_new = static_cast<const uint16_t *>(r.v_new) + it.layer * kv_stride;
+            a.out = static_cast<uint16_t *>(r.out) + it.layer * q_stride;
+            a.pool_k = base + ((int64_t)it.layer * 2 + 0) * l.num_pages * block;
+            a.pool_v = base + ((int64_t)it.layer * 2 + 1) * l.num_pages * block;
+            a.pages = r.block_table->pages;
+            a.ws = static_cast<unsigned char *>(c->ws);
+            e = launch_attention(p, a, attn_stream);
+        }
+        if (e == hipSuccess) e = hipEventRecord(done[k], attn_stream);
+        if (e != hipSuccess) {
+            status = hip_fail(e, "enqueueing a layer");
+            msg = oc_last_error();
+            break;
+        }
+    }
+
+    // stop the producer, then drain whatever was enqueued
+    {
+        std::lock_guard<std::mutex> g(sh.mu);
+        sh.abort = sh.abort || status != OC_OK;
+    }
+    sh.cv.notify_all();
+    if (producer_thread.joinable()) {
+        if (status == OC_OK) {
+            producer_thread.join();
+            if (sh.producer_status != OC_OK) {
+                status = sh.producer_status;
+                msg = sh.producer_msg;
+            }
+        } else {
+            {
+                std::lock_guard<std::mutex> g(sh.mu);
+                sh.abort = true;
+            }
+            sh.cv.notify_all();
+            producer_thread.join();
+        }
+    }
+    hipError_t e1 = hipStreamSynchronize(c->copy);
+    hipError_t e2 = hipStreamSynchronize(c->compute);
+    if (status != OC_OK) return fail(status, msg);
+    if (e1 != hipSuccess) return hip_fail(e1, "draining the copy stream");
+    if (e2 != hipSuccess) return hip_fail(e2, "draining the compute stream");
+
+    double last = 0.0;
+    for (int64_t k = 0; k < n_items; ++k) {
+        const Item it = items[k];
+        const double t_done = ev_ms(ev_start, done[k]);
+        last = std::max(last, t_done);
+        if (stats) {
+            oc_request_stats &st = stats[it.req];
+            if (it.layer == L - 1) st.ttft_ms = t_done;
+            if (st.produced_ms) st.produced_ms[it.layer] = produced[k];
+            if (st.landed_ms) st.landed_ms[it.layer] = mode == OC_MODE_HBM_RESIDENT ? 0.0 : ev_ms(ev_start, landed[k]);
+            if (st.ingested_ms) st.ingested_ms[it.layer] = ev_ms(ev_start, ingested[k]);
+            if (st.done_ms) st.done_ms[it.layer] = t_done;
+        }
+    }
+    c->last_ms = last;
+    return OC_OK;
+}
+
+}  // namespace oc
+
+using namespace oc;
+
+extern "C" {
+
+int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_opts *opts, int64_t max_prefix_tokens,
+                      int64_t max_suffix_tokens, void **ctx) {
+    clear_error();
+    if (!kv_pool || !ctx) return fail(OC_EINVAL, "kv_pool and ctx must not be NULL");
+    *ctx = nullptr;
+    if (max_prefix_tokens < 0 || max_suffix_tokens < 1) return fail(OC_EINVAL, "bad maximum lengths");
+    const oc_layout &l = kv_pool->layout;
+    if (oc_attention_workspace_bytes(&l, max_prefix_tokens, max_suffix_tokens) == 0)
+        return fail(OC_ESHAPE, std::string("unsupported layout: ") + oc_last_error());
+    if (!kv_pool->base || !aligned(kv_pool->base, 16)) return fail(OC_EALIGN, "pool base must be 16-byte aligned");
+    Context *c = new Context();
+    c->device = device;
+    c->pool = *kv_pool;
+    c->opts = opts ? *opts : oc_pipeline_opts{};
+    int rc = fill_defaults(c->opts);
+    if (rc) {
+        delete c;
+        return rc;
+    }
+    c->max_prefix = max_prefix_tokens;
+    c->max_suffix = max_suffix_tokens;
+    c->slot_bytes = (size_t)max_prefix_tokens * 2 * l.num_kv_heads * l.head_dim * 2;
+    if (hipSetDevice(device) != hipSuccess) {
+        delete c;
+        return fail(OC_EHIP, "hipSetDevice failed");
+    }
+    // default-priority, non-blocking streams
+    if (hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking) != hipSuccess ||
+        hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking) != hipSuccess) {
+        release(c);
+        return fail(OC_EHIP, "stream creation failed");
+    }
+    if (c->opts.mode == OC_MODE_PRODUCER && c->slot_bytes > 0) {
+        c->slots.resize((size_t)c->opts.slots);
+        for (auto &s : c->slots) {
+            if (hipHostMalloc(&s.pinned, c->slot_bytes, hipHostMallocDefault) != hipSuccess ||
+                hipMalloc(&s.device, c->slot_bytes) != hipSuccess) {
+                release(c);
+                return fail(OC_ENOMEM, "staging slot allocation failed");
+            }
+        }
+    }
+    AttnPlan p;
+    plan_attention(l, max_prefix_tokens, max_suffix_tokens, &p);
+    if (hipMalloc(&c->ws, p.total) != hipSuccess) {
+        release(c);
+        return fail(OC_ENOMEM, "attention workspace allocation failed");
+    }
+    c->ws_bytes = p.total;
+    *ctx = c;
+    return OC_OK;
+}
+
+int oc_pipeline_run(void *ctx, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
+    clear_error();
+    Context *c = static_cast<Context *>(ctx);
+    if (!c || !reqs || n_reqs < 1) return fail(OC_EINVAL, "NULL context/requests or n_reqs < 1");
+    int rc = validate_requests(c, reqs, n_reqs);
+    if (rc) return rc;
+    return run_pipeline(c, reqs, n_reqs, stats);
+}
+
+double oc_pipeline_last_ms(void *ctx) { return ctx ? static_cast<Context *>(ctx)->last_ms : 0.0; }
+
+void oc_context_destroy(void *ctx) { release(static_cast<Context *>(ctx)); }
+
+}  // extern "C"

@@ -1,0 +1,116 @@
+"""The C-ABI library loads, exports every symbol its header declares, and
+rejects bad arguments before launching anything (no GPU needed: every call
+here fails validation)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2605_22850_amd as oc
+from paper_2605_22850_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "objectcache.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(oc_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = oc.lib()
+    names = declared_functions()
+    assert len(names) >= 10
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, f"not exported: {missing}"
+    assert set(names) == set(L.EXPORTS)
+
+
+def test_abi_version():
+    assert oc.oc_abi_version() == 1
+
+
+def _layout(**kw):
+    base = dict(num_layers=2, num_q_heads=4, num_kv_heads=2, head_dim=64, page_size=16, chunk_tokens=16, num_pages=64)
+    base.update(kw)
+    return L.c_layout(*base.values())
+
+
+FAKE = 1 << 20            # aligned non-null "device" address; never dereferenced
+
+
+def _ingest(layout, num_chunks=16, slice_bytes=None, table_entries=16, num_tokens=256, layer=0, data=FAKE,
+            base=FAKE):
+    if slice_bytes is None:
+        slice_bytes = 2 * layout.chunk_tokens * layout.num_kv_heads * layout.head_dim * 2
+    st = L.c_staging(data, num_chunks, slice_bytes)
+    bt = L.c_block_table(FAKE, table_entries, num_tokens)
+    kp = L.c_kv_pool(base, layout)
+    return oc.lib().oc_kv_layer_ingest(ctypes.byref(st), ctypes.byref(bt), ctypes.byref(kp), layer, None)
+
+
+def test_ingest_validation():
+    lay = _layout()
+    assert _ingest(lay, slice_bytes=1000) == L.OC_ESHAPE
+    assert b"2*G*n_kv*d*2" in oc.lib().oc_last_error()
+    assert _ingest(lay, layer=2) == L.OC_ERANGE
+    assert _ingest(lay, layer=-1) == L.OC_ERANGE
+    assert _ingest(lay, table_entries=15) == L.OC_ERANGE
+    assert _ingest(lay, num_chunks=15) == L.OC_ESHAPE
+    assert _ingest(lay, data=FAKE + 8) == L.OC_EALIGN
+    assert _ingest(lay, base=FAKE + 2) == L.OC_EALIGN
+    assert _ingest(_layout(num_q_heads=3)) == L.OC_ESHAPE
+    assert _ingest(_layout(page_size=12)) == L.OC_ESHAPE
+    assert _ingest(_layout(head_dim=60)) == L.OC_ESHAPE
+    assert _ingest(_layout(num_pages=8)) == L.OC_ERANGE
+    # nothing to do is not an error
+    assert _ingest(lay, num_chunks=0, table_entries=0, num_tokens=0) == L.OC_OK
+    assert oc.lib().oc_kv_layer_ingest(None, None, None, 0, None) == L.OC_EINVAL
+
+
+def test_attention_validation():
+    lay = _layout()
+    bt = L.c_block_table(FAKE, 16, 256)
+    kp = L.c_kv_pool(FAKE, lay)
+    f = oc.lib().oc_suffix_prefill_layer
+    need = oc.lib().oc_attention_workspace_bytes(ctypes.byref(lay), 256, 32)
+    assert need > 0
+    args = [FAKE, FAKE, FAKE, 32, ctypes.byref(kp), ctypes.byref(bt), 0, FAKE, FAKE, need, None]
+    bad = list(args); bad[9] = need - 1
+    assert f(*bad) == L.OC_EINVAL and b"workspace too small" in oc.lib().oc_last_error()
+    bad = list(args); bad[3] = 0
+    assert f(*bad) == L.OC_EINVAL
+    bad = list(args); bad[0] = FAKE + 4
+    assert f(*bad) == L.OC_EALIGN
+    bad = list(args); bad[8] = FAKE + 16
+    assert f(*bad) == L.OC_EALIGN
+    bad = list(args); bad[6] = 5
+    assert f(*bad) == L.OC_ERANGE
+    lay96 = _layout(head_dim=96)
+    assert oc.lib().oc_attention_workspace_bytes(ctypes.byref(lay96), 256, 32) == 0
+    lay_p32 = _layout(page_size=32)
+    assert oc.lib().oc_attention_workspace_bytes(ctypes.byref(lay_p32), 256, 32) == 0
+
+
+def test_workspace_grows_with_lengths():
+    lay = _layout(num_layers=32, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=16384)
+    f = oc.lib().oc_attention_workspace_bytes
+    small = f(ctypes.byref(lay), 4096, 128)
+    big = f(ctypes.byref(lay), 65536, 512)
+    assert 0 < small < big < (1 << 30)
+
+
+def test_block_table_check():
+    oc.oc_block_table_check([3, 1, 2], 40, 4, 16)
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_block_table_check([3, 1, 3], 40, 4, 16)
+    assert e.value.status == L.OC_ERANGE
+    with pytest.raises(oc.OcError):
+        oc.oc_block_table_check([3, 1, 4], 40, 4, 16)
+    with pytest.raises(oc.OcError):
+        oc.oc_block_table_check([3, 1], 40, 4, 16)
+    oc.oc_block_table_check(np.zeros(0, np.int32), 0, 4, 16)

@@ -1,0 +1,140 @@
+"""GPU parity of the single-layer entry points against the CPU oracle:
+ingest bit-exact over the whole pool, attention within max|err| 2e-2 and
+relative L2 5e-3, plus the invariants (gather after scatter is the identity,
+a permuted block table gives bit-identical attention, cached-prefix attention
+equals recomputing the whole sequence)."""
+import zlib
+
+import numpy as np
+import pytest
+
+from tests.gpu_util import (LayerCase, SENTINEL, assert_attention_close, from_dev, require_gpu, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+    import torch
+    torch.cuda.synchronize()
+    yield
+    torch.cuda.synchronize()
+
+
+# (nq, nkv, d, G, Ps, n_chunks, Ts, P, L, layer)
+INGEST_CASES = {
+    "tiny": (4, 2, 64, 16, 16, 16, 32, 64, 2, 1),
+    "8b-4k-layer": (32, 8, 128, 16, 16, 256, 128, 1024, 2, 0),
+    "two-chunks-per-page-ragged": (8, 2, 128, 8, 16, 37, 17, 64, 2, 1),
+    "two-pages-per-chunk": (8, 4, 64, 32, 16, 9, 5, 40, 3, 2),
+    "one-chunk": (4, 4, 128, 16, 16, 1, 3, 4, 1, 0),
+    "70b-layer-slice": (64, 8, 128, 16, 16, 512, 64, 2048, 2, 1),
+}
+
+
+@pytest.mark.parametrize("name", list(INGEST_CASES))
+def test_ingest_bit_exact_whole_pool(name):
+    import torch
+    nq, nkv, d, G, Ps, n, Ts, P, L, layer = INGEST_CASES[name]
+    print(f"[ingest] {name}", flush=True)
+    c = LayerCase(nq, nkv, d, G, Ps, n, Ts, P, L, layer, seed=zlib.crc32(name.encode()) & 0xFFFF).upload()
+    c.run_ingest()
+    torch.cuda.synchronize()
+    got = from_dev(c.d_pool).reshape(c.pool_shape())
+    assert np.array_equal(got, c.expected_pool()), "pool differs from the oracle's scatter"
+
+
+@pytest.mark.parametrize("name", ["tiny", "two-chunks-per-page-ragged", "8b-4k-layer"])
+def test_gather_after_ingest_is_identity(name):
+    import torch
+    from paper_2605_22850_amd import oc_kv_layer_gather
+    nq, nkv, d, G, Ps, n, Ts, P, L, layer = INGEST_CASES[name]
+    print(f"[gather] {name}", flush=True)
+    c = LayerCase(nq, nkv, d, G, Ps, n, Ts, P, L, layer, seed=5).upload()
+    c.run_ingest()
+    back = torch.zeros_like(c.d_staging)
+    oc_kv_layer_gather(c.d_table, c.Tp, c.d_pool, c.layout, layer, back, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(back), c.staging)
+
+
+def test_ingest_copies_special_bit_patterns():
+    import torch
+    print("[ingest] special bits", flush=True)
+    c = LayerCase(4, 2, 64, 16, 16, 4, 4, 8, 1, 0, seed=3)
+    pats = np.array([0x7FC1, 0xFF80, 0x0001, 0x8001, 0x7F80, 0xFFFF, 0x0000, 0x8000], np.uint16)
+    c.staging = np.resize(pats, c.staging.size).astype(np.uint16)
+    c.upload(fill=0x1234)
+    c.run_ingest()
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(c.d_pool).reshape(c.pool_shape()), c.expected_pool(fill=0x1234))
+
+
+# (nq, nkv, d, G, Ps, n_chunks, Ts, P, L, layer)
+ATTN_CASES = {
+    "tiny-l0": (4, 2, 64, 16, 16, 16, 32, 64, 2, 0),
+    "tiny-l1": (4, 2, 64, 16, 16, 16, 32, 64, 2, 1),
+    "8b-4k": (32, 8, 128, 16, 16, 256, 128, 1024, 2, 1),
+    "no-prefix": (8, 2, 128, 16, 16, 0, 40, 8, 1, 0),
+    "one-suffix-token": (8, 2, 128, 16, 16, 20, 1, 64, 1, 0),
+    "ragged-prefix-nan-slots": (8, 2, 128, 8, 16, 37, 17, 64, 2, 1),
+    "mha": (4, 4, 128, 16, 16, 10, 33, 32, 1, 0),
+    "gqa8": (64, 8, 128, 16, 16, 64, 64, 128, 1, 0),
+    "d64-long-suffix": (6, 3, 64, 16, 16, 5, 130, 16, 1, 0),
+    "suffix-spans-tiles": (32, 8, 128, 16, 16, 33, 100, 80, 1, 0),
+}
+
+
+@pytest.mark.parametrize("name", list(ATTN_CASES))
+def test_attention_matches_oracle(name):
+    import torch
+    nq, nkv, d, G, Ps, n, Ts, P, L, layer = ATTN_CASES[name]
+    print(f"[attention] {name}", flush=True)
+    c = LayerCase(nq, nkv, d, G, Ps, n, Ts, P, L, layer, seed=(zlib.crc32(name.encode()) & 0xFFF) + 1).upload()
+    if n:
+        c.run_ingest()
+    out = c.run_attention()
+    torch.cuda.synchronize()
+    assert_attention_close(from_dev(out), c.expected_attention(), name)
+
+
+def test_attention_permuted_table_is_bit_identical():
+    import torch
+    print("[attention] permuted table", flush=True)
+    base = dict(nq=32, nkv=8, d=128, G=16, Ps=16, n_chunks=64, Ts=48, P=256, L=1, layer=0, seed=9)
+    a = LayerCase(**base, table=np.arange(64, dtype=np.int32)).upload()
+    rng = np.random.default_rng(4)
+    b = LayerCase(**base, table=rng.permutation(256)[:64].astype(np.int32)).upload()
+    a.run_ingest()
+    b.run_ingest()
+    oa, ob = a.run_attention(), b.run_attention()
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(oa), from_dev(ob))
+
+
+def test_cached_prefix_equals_full_recompute():
+    # attention of the suffix over the cached (paged) prefix equals the last
+    # rows of attending over the whole sequence with no cache at all
+    import torch
+    from paper_2605_22850_amd import oc_attention_workspace_bytes, oc_suffix_prefill_layer
+    print("[attention] cached == recompute", flush=True)
+    c = LayerCase(16, 4, 128, 16, 16, 24, 40, 64, 1, 0, seed=12).upload()
+    c.run_ingest()
+    cached = from_dev(c.run_attention())
+    k, v = c.logical_kv()
+    Tall = c.Tp + c.Ts
+    rng = np.random.default_rng(2)
+    import kvgen
+    q_pre = kvgen.f32_to_bf16_bits(rng.standard_normal((c.Tp, c.nq, c.d)).astype(np.float32))
+    q_all = to_dev(np.concatenate([q_pre, c.q]), "bf16")
+    k_all = to_dev(np.concatenate([k, c.k_new]), "bf16")
+    v_all = to_dev(np.concatenate([v, c.v_new]), "bf16")
+    ws = torch.empty(oc_attention_workspace_bytes(c.layout, 0, Tall), dtype=torch.uint8, device="cuda")
+    out = torch.empty((Tall, c.nq, c.d), dtype=torch.bfloat16, device="cuda")
+    oc_suffix_prefill_layer(q_all, k_all, v_all, Tall, c.d_pool, c.layout, None, 0, 0, out, ws)
+    torch.cuda.synchronize()
+    full = from_dev(out)[c.Tp:]
+    f = lambda x: (x.astype(np.uint32) << 16).view(np.float32)
+    assert np.abs(f(full) - f(cached)).max() <= 2e-2
+    assert_attention_close(full, c.expected_attention(), "recompute")

@@ -201,3 +201,74 @@ def oc_suffix_prefill_layer(q, k_new, v_new, suffix_tokens: int, pool, layout: L
     _check(lib().oc_suffix_prefill_layer(_ptr(q), _ptr(k_new), _ptr(v_new), suffix_tokens, ctypes.byref(kp),
                                          ctypes.byref(bt), layer, _ptr(out), _ptr(workspace), workspace.numel() *
                                          workspace.element_size(), _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# pipeline
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Request:
+    """One request of a pipeline run (tensors are torch device tensors)."""
+    prefix_tokens: int
+    suffix_tokens: int
+    pages: object                      # device int32 block table (None when prefix_tokens == 0)
+    q: object                          # [L][Ts][nq][d] bf16
+    k_new: object                      # [L][Ts][nkv][d] bf16
+    v_new: object                      # [L][Ts][nkv][d] bf16
+    out: object                        # [L][Ts][nq][d] bf16
+    chunk_objects: object = None       # host numpy uint16 [N][L * S/2], one chunk object per row
+    device_payload: object = None      # device [L][Tp * b] bytes, layer payloads back to back
+
+
+def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, max_suffix_tokens: int,
+                      rate_bytes_per_s: float = 0.0, piece_bytes: int = 0, slots: int = 0,
+                      producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
+                      fault_layer: int = 0, device: int = 0):
+    opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
+                           fault_layer)
+    kp = make_pool(pool, layout)
+    ctx = c_void_p()
+    _check(lib().oc_context_create(device, ctypes.byref(kp), ctypes.byref(opts), max_prefix_tokens,
+                                   max_suffix_tokens, ctypes.byref(ctx)))
+    return ctx
+
+
+def oc_context_destroy(ctx) -> None:
+    lib().oc_context_destroy(ctx)
+
+
+def oc_pipeline_last_ms(ctx) -> float:
+    return lib().oc_pipeline_last_ms(ctx)
+
+
+def oc_pipeline_run(ctx, requests: Sequence[Request], num_layers: int):
+    """Run all layers of all requests; returns one dict of timings per request."""
+    n = len(requests)
+    creqs = (c_request * n)()
+    keep = []
+    stats = (c_request_stats * n)()
+    arrays = []
+    for i, r in enumerate(requests):
+        bt = make_table(r.pages, r.prefix_tokens)
+        keep.append(bt)
+        objs = None
+        if r.chunk_objects is not None and r.prefix_tokens > 0:
+            co = r.chunk_objects
+            if not co.flags["C_CONTIGUOUS"]:
+                raise ValueError("chunk_objects must be C-contiguous")
+            row = co.strides[0]
+            objs = (c_void_p * co.shape[0])(*[co.ctypes.data + j * row for j in range(co.shape[0])])
+            keep.append(objs)
+        creqs[i] = c_request(r.prefix_tokens, r.suffix_tokens, ctypes.pointer(bt), objs,
+                             _ptr(r.device_payload), _ptr(r.q), _ptr(r.k_new), _ptr(r.v_new), _ptr(r.out))
+        per = [(c_double * num_layers)() for _ in range(4)]
+        arrays.append(per)
+        stats[i] = c_request_stats(0.0, *per)
+    _check(lib().oc_pipeline_run(ctx, creqs, n, stats))
+    out = []
+    for i in range(n):
+        p = arrays[i]
+        out.append({"ttft_ms": stats[i].ttft_ms, "produced_ms": list(p[0]), "landed_ms": list(p[1]),
+                    "ingested_ms": list(p[2]), "done_ms": list(p[3])})
+    return out

@@ -113,3 +113,73 @@ def assert_attention_close(got_bf16: np.ndarray, ref: np.ndarray, what=""):
     assert np.isfinite(max_abs) and max_abs <= ATOL and rel <= RTOL_L2, \
         f"{what}: max|err|={max_abs:.3e} (<= {ATOL}), rel L2={rel:.3e} (<= {RTOL_L2})"
     return max_abs, rel
+
+
+class RequestSet:
+    """Several requests sharing one pool, every layer: chunk objects, block
+    tables and per-layer suffix tensors, all from kvgen."""
+
+    def __init__(self, L, nq, nkv, d, prefix_tokens, suffix_tokens, pool_pages, seed=1, G=16, Ps=16):
+        from paper_2605_22850_amd import Layout
+        self.L, self.nq, self.nkv, self.d, self.G, self.Ps = L, nq, nkv, d, G, Ps
+        self.prefix, self.suffix, self.P, self.seed = list(prefix_tokens), list(suffix_tokens), pool_pages, seed
+        self.layout = Layout(L, nq, nkv, d, Ps, G, pool_pages)
+        self.slice_elems = 2 * G * nkv * d
+        self.objs = [kvgen.chunk_objects(seed, r, L, tp // G, self.slice_elems) for r, tp in enumerate(self.prefix)]
+        self.tables = kvgen.block_tables(seed, [-(-tp // Ps) for tp in self.prefix], pool_pages)
+        self.q, self.k_new, self.v_new = [], [], []
+        for r, ts in enumerate(self.suffix):
+            self.q.append(np.stack([kvgen.suffix_tensor(seed, kvgen.KIND_Q, r, l, (ts, nq, d)) for l in range(L)]))
+            self.k_new.append(np.stack([kvgen.suffix_tensor(seed, kvgen.KIND_KNEW, r, l, (ts, nkv, d))
+                                        for l in range(L)]))
+            self.v_new.append(np.stack([kvgen.suffix_tensor(seed, kvgen.KIND_VNEW, r, l, (ts, nkv, d))
+                                        for l in range(L)]))
+
+    def chunk_rows(self, r):
+        # one row per chunk object: the object's L slices back to back
+        return self.objs[r].reshape(self.objs[r].shape[0], -1)
+
+    def pool_shape(self):
+        return oracle.pool_shape(self.L, self.P, self.nkv, self.Ps, self.d)
+
+    def expected_pool(self, fill=SENTINEL, layers=None):
+        pool = np.full(self.pool_shape(), fill, dtype=np.uint16)
+        for r, tp in enumerate(self.prefix):
+            if tp == 0:
+                continue
+            chunks = [np.ascontiguousarray(self.objs[r][j]).view(np.uint8).reshape(-1)
+                      for j in range(self.objs[r].shape[0])]
+            for l in (range(self.L) if layers is None else layers):
+                staging = oracle.assemble_layer(chunks, self.slice_elems * 2, l)
+                oracle.ingest_layer(staging, tp // self.G, self.G, self.nkv, self.d, self.Ps, self.tables[r], pool, l)
+        return pool
+
+    def expected_out(self, r, l, rows=None):
+        chunks = [np.ascontiguousarray(self.objs[r][j]).reshape(-1) for j in range(self.objs[r].shape[0])]
+        if chunks:
+            k, v = oracle.logical_kv(chunks, self.G, self.nkv, self.d, l)
+        else:
+            k = v = np.zeros((0, self.nkv, self.d), np.uint16)
+        return oracle.attention(self.q[r][l], k, v, self.k_new[r][l], self.v_new[r][l], rows=rows)
+
+    def upload(self, fill=SENTINEL, with_payload=False):
+        import torch
+        from paper_2605_22850_amd import Request
+        self.d_pool = torch.full((int(np.prod(self.pool_shape())),), np.int16(np.uint16(fill).view(np.int16)),
+                                 dtype=torch.int16, device="cuda")
+        self.reqs = []
+        for r, (tp, ts) in enumerate(zip(self.prefix, self.suffix)):
+            pages = torch.from_numpy(self.tables[r].copy()).cuda() if tp else None
+            payload = None
+            if with_payload and tp:
+                # layer-major payloads: layer l = every chunk's slice l, in prefix order
+                payload = to_dev(np.ascontiguousarray(self.objs[r].transpose(1, 0, 2)).reshape(-1))
+            out = torch.zeros((self.L, ts, self.nq, self.d), dtype=torch.bfloat16, device="cuda")
+            self.reqs.append(Request(tp, ts, pages, to_dev(self.q[r], "bf16"), to_dev(self.k_new[r], "bf16"),
+                                     to_dev(self.v_new[r], "bf16"), out, chunk_objects=self.chunk_rows(r),
+                                     device_payload=payload))
+        return self
+
+    def context(self, mode, **kw):
+        from paper_2605_22850_amd import oc_context_create
+        return oc_context_create(self.d_pool, self.layout, mode, max(self.prefix), max(self.suffix), **kw)

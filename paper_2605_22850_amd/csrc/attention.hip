@@ -1,24 +1,30 @@
 // Suffix-prefill GQA attention over a paged cached prefix plus the new
 // suffix tokens (the per-layer compute C_l of eq. (3)).
 //
-// Work split: for each KV head g, the query rows are the (suffix token,
-// query head of g's group) pairs, token-major, so one 32-row MFMA column
-// block shares tokens across the group's heads (GQA packing).  A workgroup
-// (4 wavefronts x 32 rows) owns a 128-row tile and one contiguous range of
-// 64-key blocks; key ranges are split over workgroups (split-KV) so long
-// prefixes fill the chip, and a combine kernel merges the splits by their
-// log-sum-exp.  Workgroups that share (KV head, split) -- and therefore read
-// the same K/V pages -- are launched onto the same XCD back to back so their
-// re-reads hit that XCD's L2.
+// Work split: for each KV head g the query rows are the (suffix token, query
+// head of g's group) pairs, token-major, so one 32-row MFMA block shares
+// tokens across the group's heads (GQA packing).  A workgroup of 4 wavefronts
+// owns 4 x 64 rows and one contiguous range of 64-key blocks; key ranges are
+// split over workgroups (split-KV) so long prefixes fill the chip, and a
+// combine kernel merges the splits by log-sum-exp.  Workgroups that read the
+// same K/V pages (same KV head and split) are dispatched back to back onto
+// the same XCD, so their re-reads hit that XCD's L2.
 //
-// Per 64-key block: the workgroup stages K ([key][dim]) and V ([dim][key],
-// as the pool stores it) into LDS, each wavefront computes S^T = K Q^T with
-// bf16 MFMA 32x32x16 (fp32 accumulate), updates the online softmax in
-// registers (each lane owns one query column; the two half-waves combine
-// their maxima), converts P to bf16 and accumulates O^T += V^T P.  Rows of
-// the K tile are fed to the MFMA in an order that leaves each half-wave
-// holding eight consecutive keys of P per MFMA step, which matches eight
-// consecutive keys of one V row in LDS: both operands load as 16-byte vectors.
+// Per 64-key block: K ([key][dim]) and V ([dim][key], as the pool stores it)
+// are staged into double-buffered LDS tiles whose 16-byte columns are XOR
+// swizzled by row, so the MFMA operand reads (one row per lane) are free of
+// bank conflicts; the global loads for block b+2 are in flight while block b
+// computes, with a single barrier per block.  Each wavefront computes
+// S^T = K Q^T for its two 32-query blocks with bf16 MFMA 32x32x16 (fp32
+// accumulate; every K fragment read from LDS feeds both blocks), runs the
+// online softmax with one query column per lane (the two half-waves combine
+// their maxima with a lane swap; the running maximum is only raised -- and O
+// rescaled -- when a block's maximum exceeds it by more than 2^8), converts P
+// to bf16 and accumulates O^T += V^T P, each V fragment again feeding both
+// blocks.  The K tile's rows are fed to the MFMA in an order (bits 2 and 3 of
+// the row swapped) that leaves each half-wave holding eight consecutive keys
+// of P, matching eight consecutive keys of one V row: both operands load as
+// 16-byte vectors without an in-register transpose.
 #include <math.h>
 
 #include "common.hpp"
@@ -26,19 +32,21 @@
 namespace oc {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int PAGE = 16;          // tokens per pool page (attention requires page_size 16)
 constexpr int KB = 64;            // keys per block = 4 pages
-constexpr int WAVES = 4;
-constexpr int QW = 32;            // query rows per wavefront
-constexpr int TILE_ROWS = WAVES * QW;
+constexpr int WAVES = 8;          // two per SIMD: one's softmax overlaps the other's MFMAs
+constexpr int QB = 1;             // 32-row query blocks per wavefront
+constexpr int WAVE_ROWS = 32 * QB;
+constexpr int TILE_ROWS = WAVES * WAVE_ROWS;
 constexpr int THREADS = WAVES * 64;
-constexpr int TARGET_WGS = 512;   // two workgroups per CU on 256 CUs
+constexpr int TARGET_WGS = 256;   // one workgroup per CU
+constexpr float RESCALE_SLACK = 8.0f;   // log2 units the running max may lag
 
 struct KParams {
     const uint16_t *q;
@@ -72,23 +80,62 @@ __global__ __launch_bounds__(256) void suffix_pack_kernel(const uint16_t *__rest
     }
 }
 
-__device__ inline float wave_partner(float x) { return __shfl_xor(x, 32); }
+// value of the lane 32 positions away (the other half of the wavefront)
+__device__ inline float half_swap_max(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float half_swap_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Workgroup barrier that waits only for this wavefront's LDS operations.
+// (__syncthreads() would also wait for every outstanding global load, which
+// would stall the register prefetch of the block after next.)
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // tile row r of a 32-key MFMA tile reads physical key perm(r): bits 2 and 3 swapped
 __device__ inline int key_perm(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
+// LDS element offset of 16-byte column c of K tile row r (D/8 columns per row)
+template <int D>
+__device__ inline int k_lds(int r, int c) {
+    constexpr int NS = D / 8;
+    return r * D + ((c ^ (r & (NS - 1))) << 3);
+}
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+typedef __attribute__((address_space(1))) const void *gbl_ptr_t;
+
+// one 16-byte global -> LDS copy per lane; the wavefront's 64 lanes fill 1 KiB
+// of LDS starting at `lds_chunk`, lane i at byte 16*i
+__device__ inline void dma16(const uint16_t *src, uint16_t *lds_chunk) {
+    __builtin_amdgcn_global_load_lds((gbl_ptr_t)src, (lds_ptr_t)lds_chunk, 16, 0, 0);
+}
+
+template <int N>
+__device__ inline void wait_vmcnt() {
+    static_assert(N == 0 || N == 2 || N == 4, "unexpected count");
+    if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+}
+
 template <int D>
 __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
-    constexpr int KS = D + 8;      // padded LDS row of K (elements)
-    constexpr int VS = KB + 8;     // padded LDS row of V
-    constexpr int D8 = D / 8;
-    constexpr int PIECES = PAGE * D8;            // 16-byte pieces per page block
-    constexpr int PPT = 4 * PIECES / THREADS;    // pieces per thread per tile
-    static_assert(PPT >= 1 && (4 * PIECES) % THREADS == 0, "tile does not divide over the workgroup");
-    __shared__ __align__(16) uint16_t sk[KB * KS];
-    __shared__ __align__(16) uint16_t sv[D * VS];
+    constexpr int TILE = KB * D;                   // elements of one K (or V) tile
+    constexpr int CHUNKS = TILE * 2 / 1024;        // 1 KiB DMA chunks per tile
+    constexpr int CPW = CHUNKS / WAVES;            // chunks per wavefront per tile
+    constexpr int KROWS = 512 / D;                 // K rows per chunk
+    constexpr int CPP = D / 32;                    // chunks per page (K and V alike)
+    constexpr int NDMA = 2 * CPW;                  // DMA instructions per wavefront per block
+    constexpr int NBUF = 3;
+    static_assert(CPW >= 1 && CHUNKS % WAVES == 0, "tile does not divide");
+    extern __shared__ __align__(1024) uint16_t lds[];   // [NBUF][K tile, V tile]
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int col = lane & 31, half = lane >> 5;
 
     // XCD-aware decode: workgroup w runs on XCD w % 8; all row tiles of one
@@ -100,18 +147,20 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     const int mt = local % p.m_tiles;
     const int g = gamma / p.n_split, split = gamma - g * p.n_split;
 
-    const int64_t row = (int64_t)mt * TILE_ROWS + wave * QW + col;
-    const bool row_ok = row < p.rows;
-    const int64_t tok = row_ok ? row / p.grp : 0;
-    const int head = g * p.grp + (row_ok ? (int)(row % p.grp) : 0);
-
-    bf16x8 qop[D / 16];
-    {
-        const uint16_t *qr = p.q + (tok * p.nq + head) * D + half * 8;
+    int tok[QB];
+    bool row_ok[QB];
+    bf16x8 qop[QB][D / 16];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + qb * 32 + col;
+        row_ok[qb] = row < p.rows;
+        tok[qb] = row_ok[qb] ? (int)(row / p.grp) : 0;
+        const int head = g * p.grp + (row_ok[qb] ? (int)(row % p.grp) : 0);
+        const uint16_t *qr = p.q + ((int64_t)tok[qb] * p.nq + head) * D + half * 8;
 #pragma unroll
         for (int ds = 0; ds < D / 16; ++ds) {
-            u32x4 v = row_ok ? *reinterpret_cast<const u32x4 *>(qr + ds * 16) : u32x4{0, 0, 0, 0};
-            qop[ds] = __builtin_bit_cast(bf16x8, v);
+            u32x4 v = row_ok[qb] ? *reinterpret_cast<const u32x4 *>(qr + ds * 16) : u32x4{0, 0, 0, 0};
+            qop[qb][ds] = __builtin_bit_cast(bf16x8, v);
         }
     }
 
@@ -125,184 +174,212 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
         if (b1 > last_page / 4 + 1) b1 = last_page / 4 + 1;
     }
     const int64_t full_pre_pages = p.Tp / PAGE;
+    const int64_t head_block = (int64_t)PAGE * D;      // elements of one (page, head) block
 
-    f32x16 oacc[D / 32];
-#pragma unroll
-    for (int et = 0; et < D / 32; ++et) oacc[et] = f32x16{};
-    float m_run = -__builtin_inff(), l_run = 0.f;
-
-    u32x4 kreg[PPT], vreg[PPT];
-    auto load_block = [&](int64_t b) {
-#pragma unroll
-        for (int u = 0; u < PPT; ++u) {
-            const int piece = u * THREADS + tid;
-            const int pg = piece / PIECES, within = piece - pg * PIECES;
-            const int64_t v = b * 4 + pg;
-            const uint16_t *kb = nullptr, *vb = nullptr;
-            if (v < p.n_pre_pages) {
-                const int64_t page = p.pages[v];
-                kb = p.pool_k + (page * p.nkv + g) * (int64_t)(PAGE * D);
-                vb = p.pool_v + (page * p.nkv + g) * (int64_t)(PAGE * D);
-            } else if (v - p.n_pre_pages < p.n_suf_pages) {
-                const int64_t su = v - p.n_pre_pages;
-                kb = p.ks + (su * p.nkv + g) * (int64_t)(PAGE * D);
-                vb = p.vs + (su * p.nkv + g) * (int64_t)(PAGE * D);
-            }
-            if (kb) {
-                kreg[u] = *reinterpret_cast<const u32x4 *>(kb + within * 8);
-                vreg[u] = *reinterpret_cast<const u32x4 *>(vb + within * 8);
-            } else {
-                kreg[u] = u32x4{0, 0, 0, 0};
-                vreg[u] = u32x4{0, 0, 0, 0};
-            }
+    // ---- global -> LDS copy of one 64-key block (4 pages) ----
+    // K tile: [key][dim], 16-byte columns XOR-swizzled by key row, so the
+    // MFMA reads (one key row per lane) hit distinct banks; each lane fetches
+    // the global piece that belongs at its fixed LDS position.  V tile:
+    // page-major [page][dim][16 keys], i.e. the pool's page blocks copied
+    // as they are.  Every 1 KiB chunk comes from a single page.
+    auto page_src = [&](int64_t v, const uint16_t *&kb, const uint16_t *&vb) {
+        if (v < p.n_pre_pages) {
+            const int64_t page = p.pages[v];
+            kb = p.pool_k + (page * p.nkv + g) * head_block;
+            vb = p.pool_v + (page * p.nkv + g) * head_block;
+        } else {
+            int64_t su = v - p.n_pre_pages;
+            if (su >= p.n_suf_pages) su = 0;   // past the end: any finite page, fully masked
+            kb = p.ks + (su * p.nkv + g) * head_block;
+            vb = p.vs + (su * p.nkv + g) * head_block;
         }
     };
-    auto store_block = [&](int64_t b) {
+    auto issue_block = [&](int64_t b, int buf) {
+        uint16_t *kt_lds = lds + buf * 2 * TILE;
+        uint16_t *vt_lds = kt_lds + TILE;
 #pragma unroll
-        for (int u = 0; u < PPT; ++u) {
-            const int piece = u * THREADS + tid;
-            const int pg = piece / PIECES, within = piece - pg * PIECES;
-            const int s = within / D8, e8 = within - s * D8;          // K block [slot][dim]
-            *reinterpret_cast<u32x4 *>(&sk[(pg * PAGE + s) * KS + e8 * 8]) = kreg[u];
-            const int e = within >> 1, sh = within & 1;                // V block [dim][slot]
-            u32x4 vv = vreg[u];
-            const int64_t v = b * 4 + pg;
-            if (v == full_pre_pages && v < p.n_pre_pages) {
-                // last, partial prefix page: slots past Tp may hold anything;
-                // zero them so masked keys contribute exactly nothing
-                const int valid = (int)(p.Tp - v * PAGE) - sh * 8;
-                uint16_t t[8];
-                __builtin_memcpy(t, &vv, 16);
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    if (i >= valid) t[i] = 0;
-                __builtin_memcpy(&vv, t, 16);
-            }
-            *reinterpret_cast<u32x4 *>(&sv[e * VS + pg * PAGE + sh * 8]) = vv;
+        for (int u = 0; u < CPW; ++u) {
+            const int q = u * WAVES + wave;                   // chunk index, uniform per wavefront
+            const int pg = q / CPP;                           // its page within the block
+            const int qi = q % CPP;                           // chunk within the page
+            const uint16_t *kb, *vb;
+            page_src(b * 4 + pg, kb, vb);
+            const int r = qi * KROWS + lane / (D / 8);        // key row within the page
+            const int c = (lane % (D / 8)) ^ ((pg * PAGE + r) & (D / 8 - 1));
+            dma16(kb + r * D + c * 8, kt_lds + q * 512);
+            dma16(vb + qi * 512 + lane * 8, vt_lds + q * 512);
         }
     };
 
-    const int krow_base = key_perm(col);
-    if (b0 < b1) {
-        load_block(b0);
-        store_block(b0);
-        __syncthreads();
+    f32x16 oacc[QB][D / 32];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int et = 0; et < D / 32; ++et) oacc[qb][et] = f32x16{};
+    float m_run[QB], l_run[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        m_run[qb] = -__builtin_inff();
+        l_run[qb] = 0.f;
     }
-    for (int64_t b = b0; b < b1; ++b) {
-        const bool more = b + 1 < b1;
-        if (more) load_block(b + 1);
+    const int krow = key_perm(col);
 
-        // S^T = K Q^T for two 32-key tiles
-        f32x16 sacc[2];
+    if (b0 < b1) issue_block(b0, 0);
+    if (b0 + 1 < b1) issue_block(b0 + 1, 1);
+    for (int64_t b = b0; b < b1; ++b) {
+        const int i = (int)(b - b0);
+        const int buf = i % NBUF;
+        // this block's copies are done (the next block's may still fly),
+        // and every wavefront is past the block that last used buffer i+2
+        if (b + 1 < b1) wait_vmcnt<NDMA>();
+        else wait_vmcnt<0>();
+        lds_barrier();
+        if (b + 2 < b1) issue_block(b + 2, (i + 2) % NBUF);
+        const uint16_t *K = lds + buf * 2 * TILE;
+        uint16_t *V = const_cast<uint16_t *>(K) + TILE;
+
+        const bool edge = (b + 1) * 4 > full_pre_pages;   // block holds a partial page or suffix keys
+        if (edge && b * 4 <= full_pre_pages && full_pre_pages < p.n_pre_pages) {
+            // last, partial prefix page: its slots past Tp may hold anything;
+            // zero them so masked keys contribute exactly nothing
+            const int pg = (int)(full_pre_pages - b * 4), k0 = (int)(p.Tp % PAGE);
+            for (int idx = tid; idx < D * (PAGE - k0); idx += THREADS) {
+                const int e = idx / (PAGE - k0), k = k0 + idx % (PAGE - k0);
+                V[(pg * D + e) * PAGE + k] = 0;
+            }
+            lds_barrier();
+        }
+
+        // S^T = K Q^T: two 32-key tiles x QB 32-query blocks
+        f32x16 sacc[QB][2];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-            sacc[kt] = f32x16{};
-            const uint16_t *kr = &sk[(kt * 32 + krow_base) * KS + half * 8];
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) sacc[qb][kt] = f32x16{};
 #pragma unroll
             for (int ds = 0; ds < D / 16; ++ds) {
-                bf16x8 a = *reinterpret_cast<const bf16x8 *>(kr + ds * 16);
-                sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[ds], sacc[kt], 0, 0, 0);
+                const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(&K[k_lds<D>(kt * 32 + krow, ds * 2 + half)]);
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb)
+                    sacc[qb][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qop[qb][ds], sacc[qb][kt], 0, 0, 0);
             }
         }
 
-        // mask keys past the prefix end or past this row's own suffix token
-        if ((b + 1) * 4 > full_pre_pages) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (edge) {
+            // keys [0, pe) of the block are prefix keys; suffix keys start at ps;
+            // a row sees suffix key (block position k) when k - ps <= its token
+            const int pe = (int)(p.Tp - b * KB);
+            const int ps = (int)(p.n_pre_pages * PAGE - b * KB);
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
+            for (int qb = 0; qb < QB; ++qb) {
+                const int lim = tok[qb] + ps;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kin = kt * 32 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
-                    const int64_t v = b * 4 + (kin >> 4);
-                    const int64_t slot = kin & 15;
-                    bool ok;
-                    if (v < p.n_pre_pages) ok = v * PAGE + slot < p.Tp;
-                    else ok = (v - p.n_pre_pages) * PAGE + slot <= tok;
-                    if (!ok) sacc[kt][i] = -__builtin_inff();
-                }
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int i2 = 0; i2 < 16; ++i2) {
+                        const int kin = kt * 32 + (i2 < 8 ? i2 : 8 + i2) + 8 * half;
+                        // branch-free: bitwise predicate, then a bitwise select of
+                        // the score or -inf (a short-circuit form was compiled into
+                        // divergent branches that dropped the kept value)
+                        const uint32_t keep = 0u - (uint32_t)((kin < pe) | ((kin >= ps) & (kin <= lim)));
+                        sacc[qb][kt][i2] = __uint_as_float((__float_as_uint(sacc[qb][kt][i2]) & keep) |
+                                                           (0xff800000u & ~keep));
+                    }
             }
         }
 
-        float mx = -__builtin_inff();
+        // online softmax, one query column per lane: block maximum first
+        float m_use[QB];
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
-        mx = fmaxf(mx, wave_partner(mx));
-        const float m_new = fmaxf(m_run, mx * p.scale_log2);
-        const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        m_run = m_new;
-
-        float lsum = 0.f;
-        bf16x8 pop[2][2];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-                f32x8 pv;
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    const float e = __builtin_amdgcn_exp2f(fmaf(sacc[kt][hf * 8 + i], p.scale_log2, -m_use));
-                    lsum += e;
-                    pv[i] = e;
-                }
-                pop[kt][hf] = __builtin_convertvector(pv, bf16x8);
-            }
-        }
-        l_run = l_run * alpha + lsum;
-
-        // O^T += V^T P
-#pragma unroll
-        for (int et = 0; et < D / 32; ++et) {
-            oacc[et] *= alpha;
-            const uint16_t *vr = &sv[(et * 32 + col) * VS + half * 8];
+        for (int qb = 0; qb < QB; ++qb) {
+            float mx = -__builtin_inff();
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                for (int hf = 0; hf < 2; ++hf) {
-                    bf16x8 a = *reinterpret_cast<const bf16x8 *>(vr + kt * 32 + hf * 16);
-                    oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pop[kt][hf], oacc[et], 0, 0, 0);
-                }
+                for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, sacc[qb][kt][i2]);
+            const float mblk = half_swap_max(mx) * p.scale_log2;
+            if (__any(mblk > m_run[qb] + RESCALE_SLACK)) {
+                const float m_new = fmaxf(m_run[qb], mblk);
+                const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - (m_new == -__builtin_inff() ? 0.f : m_new));
+                m_run[qb] = m_new;
+                l_run[qb] *= alpha;
+#pragma unroll
+                for (int et = 0; et < D / 32; ++et) oacc[qb][et] *= alpha;
+            }
+            m_use[qb] = m_run[qb] == -__builtin_inff() ? 0.f : m_run[qb];
         }
 
-        __syncthreads();
-        if (more) {
-            store_block(b + 1);
-            __syncthreads();
-        }
+        // P = 2^(s*scale - m), converted to bf16 eight keys at a time just
+        // before the MFMAs that consume it; O^T += V^T P
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                bf16x8 pf[QB];
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) {
+                    f32x8 pv;
+                    float lsum = 0.f;
+#pragma unroll
+                    for (int i2 = 0; i2 < 8; ++i2) {
+                        const float e = __builtin_amdgcn_exp2f(fmaf(sacc[qb][kt][hf * 8 + i2], p.scale_log2, -m_use[qb]));
+                        lsum += e;
+                        pv[i2] = e;
+                    }
+                    l_run[qb] += lsum;
+                    pf[qb] = __builtin_convertvector(pv, bf16x8);
+                }
+#pragma unroll
+                for (int et = 0; et < D / 32; ++et) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(&V[((kt * 2 + hf) * D + et * 32 + col) * PAGE + half * 8]);
+#pragma unroll
+                    for (int qb = 0; qb < QB; ++qb)
+                        oacc[qb][et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[qb], oacc[qb][et], 0, 0, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
     }
 
-    const float l_tot = l_run + wave_partner(l_run);
-    if (!row_ok) return;
-    if (p.n_split == 1) {
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        uint16_t *orow = p.out + (tok * p.nq + head) * D;
 #pragma unroll
-        for (int et = 0; et < D / 32; ++et)
+    for (int qb = 0; qb < QB; ++qb) {
+        const float l_tot = half_swap_sum(l_run[qb]);
+        if (!row_ok[qb]) continue;
+        const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + qb * 32 + col;
+        if (p.n_split == 1) {
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            const int head = g * p.grp + (int)(row % p.grp);
+            uint16_t *orow = p.out + ((int64_t)tok[qb] * p.nq + head) * D;
 #pragma unroll
-            for (int vq = 0; vq < 4; ++vq) {
-                f32x4 o4 = {oacc[et][vq * 4 + 0] * inv, oacc[et][vq * 4 + 1] * inv, oacc[et][vq * 4 + 2] * inv,
-                            oacc[et][vq * 4 + 3] * inv};
-                typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-                bf16x4 b4 = __builtin_convertvector(o4, bf16x4);
-                *reinterpret_cast<bf16x4 *>(orow + et * 32 + vq * 8 + half * 4) = b4;
+            for (int et = 0; et < D / 32; ++et)
+#pragma unroll
+                for (int vq = 0; vq < 4; ++vq) {
+                    f32x4 o4 = {oacc[qb][et][vq * 4 + 0], oacc[qb][et][vq * 4 + 1], oacc[qb][et][vq * 4 + 2],
+                                oacc[qb][et][vq * 4 + 3]};
+                    *reinterpret_cast<bf16x4 *>(orow + et * 32 + vq * 8 + half * 4) =
+                        __builtin_convertvector(o4 * inv, bf16x4);
+                }
+        } else {
+            const int64_t prow = ((int64_t)split * p.nkv + g) * p.rows_pad + row;
+            float *orow = p.o_part + prow * D;
+#pragma unroll
+            for (int et = 0; et < D / 32; ++et)
+#pragma unroll
+                for (int vq = 0; vq < 4; ++vq) {
+                    f32x4 o4 = {oacc[qb][et][vq * 4 + 0], oacc[qb][et][vq * 4 + 1], oacc[qb][et][vq * 4 + 2],
+                                oacc[qb][et][vq * 4 + 3]};
+                    *reinterpret_cast<f32x4 *>(orow + et * 32 + vq * 8 + half * 4) = o4;
+                }
+            if (half == 0) {
+                p.ml_part[prow * 2 + 0] = m_run[qb];
+                p.ml_part[prow * 2 + 1] = l_tot;
             }
-    } else {
-        const int64_t prow = ((int64_t)split * p.nkv + g) * p.rows_pad + row;
-        float *orow = p.o_part + prow * D;
-#pragma unroll
-        for (int et = 0; et < D / 32; ++et)
-#pragma unroll
-            for (int vq = 0; vq < 4; ++vq) {
-                f32x4 o4 = {oacc[et][vq * 4 + 0], oacc[et][vq * 4 + 1], oacc[et][vq * 4 + 2], oacc[et][vq * 4 + 3]};
-                *reinterpret_cast<f32x4 *>(orow + et * 32 + vq * 8 + half * 4) = o4;
-            }
-        if (half == 0) {
-            p.ml_part[prow * 2 + 0] = m_run;
-            p.ml_part[prow * 2 + 1] = l_tot;
         }
     }
 }
+
+template <int D>
+constexpr size_t attn_lds_bytes() { return (size_t)3 * 2 * KB * D * 2; }
 
 // Merge the splits of each row: weights 2^(m_s - M), normalised by the
 // matching sum of l_s; bf16 out.
@@ -331,9 +408,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(KParams p) {
     const float inv = L > 0.f ? 1.f / L : 0.f;
     const int64_t tok = row / p.grp;
     const int head = g * p.grp + (int)(row % p.grp);
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    bf16x4 b4 = __builtin_convertvector(acc * inv, bf16x4);
-    *reinterpret_cast<bf16x4 *>(p.out + (tok * p.nq + head) * D + c4 * 4) = b4;
+    *reinterpret_cast<bf16x4 *>(p.out + (tok * p.nq + head) * D + c4 * 4) = __builtin_convertvector(acc * inv, bf16x4);
 }
 
 // ---------------------------------------------------------------------------
@@ -408,7 +483,14 @@ static hipError_t launch_d(const AttnPlan &pl, const AttnArgs &a, hipStream_t s)
                        pl.nkv, D);
     const int64_t groups_per_xcd = (p.n_groups + 7) / 8;
     const int64_t grid = 8 * groups_per_xcd * pl.m_tiles;
-    hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((unsigned)grid), dim3(THREADS), 0, s, p);
+    static bool lds_set = false;
+    if (!lds_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_fwd_kernel<D>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds_bytes<D>());
+        if (e != hipSuccess) return e;
+        lds_set = true;
+    }
+    hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((unsigned)grid), dim3(THREADS), attn_lds_bytes<D>(), s, p);
     if (pl.n_split > 1) {
         constexpr int RPB = 256 / (D / 4);
         const int64_t nrows = (int64_t)pl.nkv * pl.rows;

@@ -57,7 +57,7 @@ typedef struct {
     int32_t num_kv_heads;   /* n_kv                                           */
     int32_t head_dim;       /* d, 64 or 128                                   */
     int32_t page_size;      /* tokens per pool page, a multiple of 8          */
-    int32_t chunk_tokens;   /* G, tokens per stored chunk                     */
+    int32_t chunk_tokens;   /* G, tokens per stored chunk, a multiple of 8    */
     int64_t num_pages;      /* P, pages in the pool                           */
 } oc_layout;
 

@@ -28,8 +28,7 @@ static int check_layout(const oc_layout &l) {
     if (l.num_q_heads % l.num_kv_heads != 0) return fail(OC_ESHAPE, "num_q_heads must be a multiple of num_kv_heads");
     if (l.head_dim % 8 != 0) return fail(OC_ESHAPE, "head_dim must be a multiple of 8");
     if (l.page_size % 8 != 0) return fail(OC_ESHAPE, "page_size must be a multiple of 8");
-    if (ingest_heads_per_block(l.num_kv_heads, l.head_dim, l.page_size) == 0)
-        return fail(OC_ESHAPE, "one page of one head does not fit the 64 KiB transpose stage");
+    if (l.chunk_tokens % 8 != 0) return fail(OC_ESHAPE, "chunk_tokens must be a multiple of 8");
     return OC_OK;
 }
 
@@ -58,7 +57,6 @@ static IngestArgs ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, 
     a.n_kv = l.num_kv_heads;
     a.d = l.head_dim;
     a.Ps = l.page_size;
-    a.heads_per_block = ingest_heads_per_block(l.num_kv_heads, l.head_dim, l.page_size);
     return a;
 }
 

@@ -182,9 +182,13 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     // the global piece that belongs at its fixed LDS position.  V tile:
     // page-major [page][dim][16 keys], i.e. the pool's page blocks copied
     // as they are.  Every 1 KiB chunk comes from a single page.
+    // the block table is read-only here: load it through the constant address
+    // space so the uniform page lookups become scalar loads
+    const __attribute__((address_space(4))) int32_t *pages_c =
+        (const __attribute__((address_space(4))) int32_t *)p.pages;
     auto page_src = [&](int64_t v, const uint16_t *&kb, const uint16_t *&vb) {
         if (v < p.n_pre_pages) {
-            const int64_t page = p.pages[v];
+            const int64_t page = pages_c[v];
             kb = p.pool_k + (page * p.nkv + g) * head_block;
             vb = p.pool_v + (page * p.nkv + g) * head_block;
         } else {

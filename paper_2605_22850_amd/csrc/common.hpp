@@ -33,12 +33,10 @@ struct IngestArgs {
     const int32_t *pages;
     int64_t num_tokens;        // T_p
     int32_t G, n_kv, d, Ps;
-    int32_t heads_per_block;   // heads one workgroup moves
 };
 hipError_t launch_ingest(const IngestArgs &a, int64_t n_pages_used, hipStream_t s);
 hipError_t launch_gather(const IngestArgs &a, uint16_t *staging_out, int64_t n_pages_used,
                          hipStream_t s);
-int ingest_heads_per_block(int n_kv, int d, int Ps);
 
 // ---- attention --------------------------------------------------------------
 struct AttnPlan {

@@ -406,7 +406,6 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 a.n_kv = l.num_kv_heads;
                 a.d = l.head_dim;
                 a.Ps = l.page_size;
-                a.heads_per_block = ingest_heads_per_block(l.num_kv_heads, l.head_dim, l.page_size);
                 e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy);
             }
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);

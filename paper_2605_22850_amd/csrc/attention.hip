@@ -254,22 +254,25 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
             lds_barrier();
         }
 
-        // S^T = K Q^T: two 32-key tiles x QB 32-query blocks
+        // S^T = K Q^T for both 32-key halves of the block, issued back to back
+        // so the MFMAs of the second half run while the first half's softmax
+        // executes on the vector ALU
         f32x16 sacc[QB][2];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
+            bf16x8 kf[D / 16];
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb) sacc[qb][kt] = f32x16{};
+            for (int ds = 0; ds < D / 16; ++ds)
+                kf[ds] = *reinterpret_cast<const bf16x8 *>(&K[k_lds<D>(kt * 32 + krow, ds * 2 + half)]);
 #pragma unroll
-            for (int ds = 0; ds < D / 16; ++ds) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(&K[k_lds<D>(kt * 32 + krow, ds * 2 + half)]);
+            for (int qb = 0; qb < QB; ++qb) {
+                sacc[qb][kt] = f32x16{};
 #pragma unroll
-                for (int qb = 0; qb < QB; ++qb)
-                    sacc[qb][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qop[qb][ds], sacc[qb][kt], 0, 0, 0);
+                for (int ds = 0; ds < D / 16; ++ds)
+                    sacc[qb][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ds], qop[qb][ds], sacc[qb][kt], 0, 0, 0);
             }
         }
 
-        __builtin_amdgcn_sched_barrier(0);
         if (edge) {
             // keys [0, pe) of the block are prefix keys; suffix keys start at ps;
             // a row sees suffix key (block position k) when k - ps <= its token
@@ -293,31 +296,29 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
             }
         }
 
-        // online softmax, one query column per lane: block maximum first
-        float m_use[QB];
+        // online softmax per 32-key half, one query column per lane; the
+        // running maximum is raised (and O rescaled) only when it lags the
+        // half's maximum by more than 2^RESCALE_SLACK
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-            float mx = -__builtin_inff();
+        for (int kt = 0; kt < 2; ++kt) {
+            float m_use[QB];
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
+            for (int qb = 0; qb < QB; ++qb) {
+                float mx = -__builtin_inff();
 #pragma unroll
                 for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, sacc[qb][kt][i2]);
-            const float mblk = half_swap_max(mx) * p.scale_log2;
-            if (__any(mblk > m_run[qb] + RESCALE_SLACK)) {
-                const float m_new = fmaxf(m_run[qb], mblk);
-                const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - (m_new == -__builtin_inff() ? 0.f : m_new));
-                m_run[qb] = m_new;
-                l_run[qb] *= alpha;
+                const float mblk = half_swap_max(mx) * p.scale_log2;
+                if (__any(mblk > m_run[qb] + RESCALE_SLACK)) {
+                    const float m_new = fmaxf(m_run[qb], mblk);
+                    const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - (m_new == -__builtin_inff() ? 0.f : m_new));
+                    m_run[qb] = m_new;
+                    l_run[qb] *= alpha;
 #pragma unroll
-                for (int et = 0; et < D / 32; ++et) oacc[qb][et] *= alpha;
+                    for (int et = 0; et < D / 32; ++et) oacc[qb][et] *= alpha;
+                }
+                m_use[qb] = m_run[qb] == -__builtin_inff() ? 0.f : m_run[qb];
             }
-            m_use[qb] = m_run[qb] == -__builtin_inff() ? 0.f : m_run[qb];
-        }
-
-        // P = 2^(s*scale - m), converted to bf16 eight keys at a time just
-        // before the MFMAs that consume it; O^T += V^T P
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
+            // P = 2^(s*scale - m) as bf16, eight keys per MFMA operand; O^T += V^T P
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf) {
                 bf16x8 pf[QB];
@@ -341,8 +342,8 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
                     for (int qb = 0; qb < QB; ++qb)
                         oacc[qb][et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[qb], oacc[qb][et], 0, 0, 0);
                 }
-                __builtin_amdgcn_sched_barrier(0);
             }
+        }
     }
 
 #pragma unroll

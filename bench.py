@@ -1,30 +1,40 @@
 #!/usr/bin/env python3
 """Benchmark of the layerwise prefix-KV hot path on one MI355X.
 
-A step is one pass of the whole path over one request with its payloads
-already in HBM: for every layer, ingest (unpack + scatter into the paged
-pool) on the copy stream, then that layer's suffix-prefill attention on the
-compute stream as soon as the layer's ingested event fires -- all layers,
-two streams, per-layer events.
+A step is one pass of the whole path over one batch of requests whose layer
+payloads are already in HBM: for every layer, ingest (unpack + scatter into
+the paged pool) on the copy stream, then that layer's suffix-prefill
+attention on the compute stream once the layer's ingested event has fired --
+all layers, two streams, per-layer events.
 
-Reported (one JSON line):
-  value            KV ingest GB/s = algorithmic bytes (read + write of every
-                   layer payload) / summed ingest kernel time, timed with HIP
-                   events on the copy stream over the timed steps
-  roofline         ingest against 8 TB/s HBM
-  attention        attention TFLOP/s (attention-only pass) against 2.5 PFLOP/s
-  ttft_ms          HBM-resident / device-staged / producer uncapped / producer
-                   capped at 12.5 GB/s (100 Gbps), mean and std over trials
-                   after the first
-  added_ttft_ms    capped producer minus HBM-resident, and the eq. (3) floor
-  cpu_baseline     the CPU oracle's ingest on the host, GB/s
+Reported (one JSON line on stdout):
+  value          KV ingest GB/s inside the timed steps: algorithmic bytes
+                 (read + write of every layer payload) / summed ingest time,
+                 each ingest bracketed by HIP events on the copy stream
+  roofline       that ingest against 8 TB/s HBM; traffic = HBM bytes per
+                 launch from the committed FETCH_SIZE/WRITE_SIZE summary,
+                 null when the kernel source has changed since
+  ingest_isolated  the same kernel launched back to back with nothing beside
+                 it (kernel capability, not the step)
+  attention      attention TFLOP/s per layer (HBM-resident pass) against the
+                 2.5 PFLOP/s bf16 dense MFMA peak
+  ttft_ms        HBM-resident / device-staged / producer uncapped / producer
+                 capped at 12.5 GB/s (100 Gbps), mean and std over trials
+                 after the first
+  added_ttft_ms  capped producer minus HBM-resident, beside the eq. (3) floor
+  cpu_baseline   the CPU oracle on a bounded sample, on this host
+
+``--profile-summary DB...`` turns rocprofv3 output of this script into the
+markdown kept under profiles/ (no GPU needed).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -36,6 +46,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "KV ingest GB/s (%HBM peak); added TTFT vs HBM-resident KV, 4K/64K prefix"
+INGEST_SRC = os.path.join(ROOT, "paper_2605_22850_amd", "csrc", "ingest.hip")
+CALIB_BYTES = 1 << 30          # plain device-to-device copy used to scale the HBM byte counters
+CALIB_COPIES = 3
 
 
 def log(*a):
@@ -64,7 +77,36 @@ def layerwise_floor(X, C):
     return t + C[-1]
 
 
-def setup(wl, log_every=8):
+def file_sha256(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"kv_ingest_kernel_{workload}_hbm_traffic.md")
+
+
+def read_traffic(workload):
+    """HBM bytes per ingest launch from the committed counter summary, or
+    None when there is none or the kernel source changed after it was taken."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    text = open(path).read()
+    m_b = re.search(r"^traffic_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    m_s = re.search(r"^kernel_source_sha256:\s*([0-9a-f]{64})", text, re.M)
+    if not (m_b and m_s):
+        return None, "counter summary unreadable"
+    if m_s.group(1) != file_sha256(INGEST_SRC):
+        return None, "kernel changed since the counters were taken"
+    return float(m_b.group(1)), os.path.relpath(path, ROOT)
+
+
+# ---------------------------------------------------------------------------
+# GPU legs
+# ---------------------------------------------------------------------------
+
+def setup(wl):
     import torch
     import kvgen
     import paper_2605_22850_amd as oc
@@ -75,12 +117,12 @@ def setup(wl, log_every=8):
     pool = torch.zeros(layout.pool_elems, dtype=torch.int16, device="cuda")
     tables = kvgen.block_tables(wl.seed, [wl.pages_needed(r) for r in range(wl.n_requests)], wl.pool_pages)
     reqs, objs_all = [], []
+    b = 2 * nkv * d * 2
     for r in range(wl.n_requests):
         tp, ts = wl.prefix_tokens[r], wl.suffix_tokens[r]
         n = wl.n_chunks(r)
         objs = kvgen.chunk_objects(wl.seed, r, L, n, wl.slice_elems, threads=16)    # [N][L][S/2]
         objs_all.append(objs)
-        b = 2 * nkv * d * 2
         payload = torch.empty(L * tp * b // 2, dtype=torch.int16, device="cuda")
         for l in range(L):
             lay = np.ascontiguousarray(objs[:, l, :]).reshape(-1).view(np.int16)
@@ -112,6 +154,76 @@ def run_mode(oc, pool, layout, wl, reqs, mode, trials, **kw):
     return out
 
 
+def copy_calibration():
+    """Plain device-to-device copies of a known size; their byte counters
+    scale the ingest kernel's."""
+    import torch
+    src = torch.ones(CALIB_BYTES // 2, dtype=torch.int16, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(CALIB_COPIES):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def isolated_ingest(oc, wl, layout, pool, reqs, passes):
+    """Ingest of every layer of every request, back to back on one stream,
+    nothing else running; per-launch HIP events."""
+    import torch
+    s = torch.cuda.Stream()
+    b = 2 * wl.num_kv_heads * wl.head_dim * 2
+    evs = []
+    with torch.cuda.stream(s):
+        for _ in range(passes):
+            for l in range(wl.num_layers):
+                for r, rq in enumerate(reqs):
+                    tp = wl.prefix_tokens[r]
+                    n = tp // wl.chunk_tokens
+                    st = rq.device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(s)
+                    oc.oc_kv_layer_ingest(st, n, rq.pages, tp, pool, layout, l, s)
+                    e1.record(s)
+                    evs.append((e0, e1, 2.0 * tp * b))
+    s.synchronize()
+    ms = sum(e0.elapsed_time(e1) for e0, e1, _ in evs)
+    nbytes = sum(x for _, _, x in evs)
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"value": round(gbs, 2), "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "launches": len(evs), "mean_launch_us": round(ms / len(evs) * 1e3, 3),
+            "how": f"{passes} passes over all {wl.num_layers} layer payloads ({nbytes / len(evs) / 2**20:.0f} MiB "
+                   f"read + written per launch), one stream, nothing beside it"}
+
+
+def ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev):
+    """TTFT of the four modes (HBM-resident and device-staged trials given),
+    added TTFT at the cap, the eq. (3) floor and the device-staged gate."""
+    L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
+    trials = max(2, args.trials)
+    ttft = {"hbm_resident": mean_std(x[0] for x in hbm[1:]), "device_staged": mean_std(x[0] for x in dev[1:])}
+    res = {}
+    if not args.no_producer:
+        unc = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=0.0)
+        log(f"[bench] {wl.name} producer uncapped trials done")
+        cap = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=args.cap)
+        log(f"[bench] {wl.name} producer capped trials done")
+        ttft["producer_uncapped"] = mean_std(x[0] for x in unc[1:])
+        ttft["producer_capped"] = mean_std(x[0] for x in cap[1:])
+        # eq. (3) floor at the cap: X_l = bytes of layer l / cap, C_l = measured device-staged per-layer time
+        layer_bytes = sum(wl.prefix_tokens) * b
+        X = [layer_bytes / args.cap * 1e3] * L
+        C = [ttft["device_staged"][0] / L] * L
+        floor = layerwise_floor(X, C)
+        res = {"added_ttft_ms": round(ttft["producer_capped"][0] - ttft["hbm_resident"][0], 3),
+               "eq3_floor_ms": round(floor, 3),
+               "cap_vs_floor": round(ttft["producer_capped"][0] / floor, 4),
+               "arrival_floor_ms": round(L * layer_bytes / args.cap * 1e3, 3)}
+    res["gates"] = {"device_staged_over_hbm": round((ttft["device_staged"][0] - ttft["hbm_resident"][0]) /
+                                                    ttft["hbm_resident"][0], 4)}
+    return ttft, res
+
+
 def cpu_baseline(wl, objs_all, tables, budget_s):
     """The CPU oracle, as it stands, on a bounded sample of the same workload."""
     import oracle
@@ -140,8 +252,7 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
     threads = len(os.sched_getaffinity(0))
     rows, flops, asecs = [], 0.0, 0.0
     step = max(1, ts // 64)
-    cand = list(range(ts - 1, -1, -step))
-    for i in cand:
+    for i in range(ts - 1, -1, -step):
         if asecs > budget_s * 0.5 and rows:
             break
         t = time.perf_counter()
@@ -151,13 +262,209 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
         flops += 4.0 * nq * d * (tp + i + 1)
     return {
         "value": round(ingest_gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-        "sample": f"oracle byte-loop ingest of {layers} of {L} layers of request 0 ({layers * tp} tokens); "
-                  f"the oracle's single-threaded scatter",
-        "attention": {"gflops": round(flops / asecs / 1e9, 4), "threads": threads, "rows": len(rows),
+        "sample": f"oracle byte-loop ingest (single thread) of {layers} of {L} layer payloads of request 0 "
+                  f"({layers * tp} tokens x {2 * nkv * d * 2} B, read + written)",
+        "attention": {"gflops": round(flops / asecs / 1e9, 4), "cores": threads, "rows": len(rows),
                       "sample": f"float64 attention of {len(rows)} suffix rows x {nq} heads of layer 0 over "
-                                f"{tp} prefix keys"},
+                                f"{tp} prefix keys, {threads} threads"},
         "seconds": round(secs + asecs, 2),
     }
+
+
+def run_bench(args):
+    import torch
+    import kvgen
+    import paper_2605_22850_amd as oc
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    wl = kvgen.workload(args.workload)
+    L, nq, nkv, d, R = wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.n_requests
+    b = 2 * nkv * d * 2
+    layout, pool, reqs, objs_all, tables = setup(wl)
+    if args.copy_calibration:
+        copy_calibration()
+        log("[bench] copy calibration done")
+
+    # ---- timed steps: device-staged pipeline, all layers ----
+    for i in range(args.warmup):
+        run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, 1)
+        log(f"[bench] warmup {i + 1}/{args.warmup}")
+    ctx = oc.oc_context_create(pool, layout, oc.OC_MODE_DEVICE_STAGED, max(wl.prefix_tokens),
+                               max(wl.suffix_tokens))
+    stats_all = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        stats_all.append(oc.oc_pipeline_run(ctx, reqs, L))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    oc.oc_context_destroy(ctx)
+    log(f"[bench] {args.steps} steps in {wall:.3f} s")
+    ingest_ms, n_ingest = 0.0, 0
+    for st in stats_all:
+        for rst in st:
+            for l in range(L):
+                ingest_ms += rst["ingested_ms"][l] - rst["landed_ms"][l]
+                n_ingest += 1
+    ingest_bytes_per_step = 2.0 * sum(wl.prefix_tokens) * b * L       # read + write, every layer
+    value = ingest_bytes_per_step * args.steps / (ingest_ms / 1e3) / 1e9
+    per_launch_bytes = ingest_bytes_per_step / (L * R)
+    mean_launch_us = ingest_ms / n_ingest * 1e3
+    traffic, traffic_src = read_traffic(wl.name)
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall / args.steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded N(0,1) bf16 KV/Q, Fisher-Yates block tables",
+        "config": {"workload": wl.name, "layers": L, "q_heads": nq, "kv_heads": nkv, "head_dim": d,
+                   "prefix_tokens": wl.prefix_tokens if R > 1 else wl.prefix_tokens[0],
+                   "suffix_tokens": wl.suffix_tokens if R > 1 else wl.suffix_tokens[0],
+                   "page_tokens": wl.page_size, "chunk_tokens": wl.chunk_tokens, "pool_pages": wl.pool_pages,
+                   "step": "device-staged pipeline: per layer ingest (copy stream) then attention (compute "
+                           "stream), all layers"},
+        "roofline": {"bound": "hbm", "kernel": "kv_ingest_kernel", "achieved": round(value, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "traffic_source": traffic_src,
+                     "bytes_per_launch": per_launch_bytes, "launches": n_ingest,
+                     "mean_launch_us": round(mean_launch_us, 3)},
+    }
+
+    # ---- TTFT modes ----
+    trials = max(2, args.trials)
+    hbm = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_HBM_RESIDENT, trials)
+    log("[bench] hbm-resident trials done")
+    dev = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, trials)
+    log("[bench] device-staged trials done")
+    t_hbm = [x[0] for x in hbm[1:]]
+    t_dev = [x[0] for x in dev[1:]]
+    # attention of one request's layer: from the event before it to the one after it, HBM-resident
+    op_ms, op_flops = 0.0, 0.0
+    for _, st in hbm[1:]:
+        for r, rst in enumerate(st):
+            for l in range(L):
+                op_ms += rst["done_ms"][l] - rst["ingested_ms"][l]
+                op_flops += attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r])
+    attn_tflops = op_flops / (op_ms / 1e3) / 1e12
+    flops_per_layer = sum(attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r]) for r in range(R))
+    layer_tflops = flops_per_layer / (sum(t_hbm) / len(t_hbm) / L / 1e3) / 1e12
+    line["attention"] = {
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)},
+        "flops_per_layer": flops_per_layer, "op_ms_per_request_layer": round(op_ms / (len(hbm[1:]) * L * R), 4),
+        "what": "suffix K/V pack + attention + split combine of one layer, HIP events around them",
+        "tflops_whole_pass": round(layer_tflops, 2),
+    }
+    line["ttft_ms"], res = ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev)
+    line.update(res)
+    if args.second_workload and args.second_workload != wl.name:
+        wl2 = kvgen.workload(args.second_workload)
+        del hbm, dev
+        lay2, pool2, reqs2, _, _ = setup(wl2)
+        hbm2 = run_mode(oc, pool2, lay2, wl2, reqs2, oc.OC_MODE_HBM_RESIDENT, trials)
+        dev2 = run_mode(oc, pool2, lay2, wl2, reqs2, oc.OC_MODE_DEVICE_STAGED, trials)
+        t2, res2 = ttft_legs(oc, wl2, lay2, pool2, reqs2, args, hbm2, dev2)
+        line["second_workload"] = {"workload": wl2.name, "ttft_ms": t2, **res2}
+        del pool2, reqs2
+        log(f"[bench] {wl2.name} ttft legs done")
+    if args.isolated_passes > 0:
+        line["ingest_isolated"] = isolated_ingest(oc, wl, layout, pool, reqs, args.isolated_passes)
+        log("[bench] isolated ingest done")
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        line["cpu_baseline"] = cpu_baseline(wl, objs_all, tables, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# rocprofv3 output -> markdown
+# ---------------------------------------------------------------------------
+
+def _short(name):
+    n = name.replace("void ", "")
+    if n.startswith("at::native"):
+        return "torch " + ("fill" if "Fill" in n else "elementwise")
+    return n.split("(")[0]
+
+
+def profile_summary(paths, workload, warmup, steps):
+    import sqlite3
+    import kvgen
+    wl = kvgen.workload(workload)
+    per_run = wl.num_layers * sum(1 for t in wl.prefix_tokens if t > 0)
+    lo, hi = warmup * per_run, (warmup + steps) * per_run
+    b = 2 * wl.num_kv_heads * wl.head_dim * 2
+    out = []
+    counters = {}
+    for path in paths:
+        c = sqlite3.connect(path)
+        has_pmc = c.execute("select count(*) from counters_collection").fetchone()[0] > 0
+        if not has_pmc:
+            out.append(f"### Kernel trace: `{os.path.basename(path)}`\n")
+            out.append("| kernel | calls | total ms | average us | % |\n|---|---|---|---|---|")
+            for name, calls, tot, avg, pct in c.execute(
+                    "select name,total_calls,total_duration,average,percentage from top_kernels"):
+                # this view reports microseconds
+                out.append(f"| `{_short(name)}` | {calls} | {tot / 1e3:.3f} | {avg:.3f} | {pct:.2f} |")
+            rows = list(c.execute("select name,start,end,vgpr_count,accum_vgpr_count,lds_size,grid_x "
+                                  "from kernels order by start"))
+            ing = [r for r in rows if "kv_ingest_kernel" in r[0]]
+            att = [r for r in rows if "attn_fwd_kernel" in r[0]]
+            out.append("")
+            for label, ks in (("kv_ingest_kernel", ing), ("attn_fwd_kernel", att)):
+                sel = ks[lo:hi]
+                if not sel:
+                    continue
+                dur = [(r[2] - r[1]) / 1e3 for r in sel]
+                out.append(f"- `{label}` in the timed steps (launches {lo}..{hi - 1} in start order, "
+                           f"warmup {warmup} x {per_run} skipped): {len(sel)} launches, mean {np.mean(dur):.3f} us, "
+                           f"min {min(dur):.3f}, max {max(dur):.3f}; VGPR {sel[0][3]}, AGPR {sel[0][4]}, "
+                           f"LDS {sel[0][5]} B, grid {sel[0][6]} threads")
+                if label == "kv_ingest_kernel":
+                    nbytes = 2.0 * sum(wl.prefix_tokens) * b / len(wl.prefix_tokens)
+                    out.append(f"  - algorithmic bytes per launch {nbytes:.0f} -> "
+                               f"{nbytes / (np.mean(dur) * 1e-6) / 1e9:.1f} GB/s")
+            out.append("")
+        else:
+            rows = list(c.execute("select dispatch_id,kernel_name,counter_name,value,start,end "
+                                  "from counters_collection order by start"))
+            by_disp = {}
+            for disp, name, cn, val, st, en in rows:
+                e = by_disp.setdefault(disp, {"name": name, "start": st, "end": en, "c": {}})
+                e["c"][cn] = e["c"].get(cn, 0.0) + val
+            disp = sorted(by_disp.values(), key=lambda e: e["start"])
+            ing = [e for e in disp if "kv_ingest_kernel" in e["name"]]
+            first_ing = ing[0]["start"] if ing else float("inf")
+            cal = [e for e in disp if "copyBuffer" in e["name"] and e["start"] < first_ing
+                   and e["end"] - e["start"] > 20000]
+            sel = ing[lo:hi]
+            for cn in sorted({k for e in sel for k in e["c"]}):
+                counters[cn] = {"ingest_kib": float(np.mean([e["c"][cn] for e in sel])),
+                                "calib_kib": float(sum(e["c"].get(cn, 0.0) for e in cal)),
+                                "calib_dispatches": len(cal), "ingest_dispatches": len(sel),
+                                "db": os.path.basename(path)}
+    if counters:
+        nbytes = 2.0 * sum(wl.prefix_tokens) * b / len(wl.prefix_tokens)
+        out.append("### HBM byte counters (kv_ingest_kernel, timed-step launches)\n")
+        out.append("| counter | per ingest launch (KiB) | calibration copies (KiB) | scale | "
+                   "scaled bytes per launch |\n|---|---|---|---|---|")
+        total = 0.0
+        for cn, v in counters.items():
+            expect = CALIB_COPIES * CALIB_BYTES / 1024.0
+            scale = expect / v["calib_kib"] if v["calib_kib"] > 0 else float("nan")
+            scaled = v["ingest_kib"] * 1024.0 * scale
+            total += scaled
+            out.append(f"| {cn} | {v['ingest_kib']:.0f} | {v['calib_kib']:.0f} ({v['calib_dispatches']} "
+                       f"dispatches) | {scale:.4f} | {scaled:.0f} |")
+        out.append("")
+        out.append(f"Algorithmic bytes per launch: {nbytes:.0f} (read + write of the layer payload); "
+                   f"measured / algorithmic = {total / nbytes:.4f}.\n")
+        if len(counters) >= 2:
+            out.append(f"traffic_bytes_per_launch: {total:.0f}")
+            out.append(f"kernel_source_sha256: {file_sha256(INGEST_SRC)}")
+    return "\n".join(out)
 
 
 def main():
@@ -170,113 +477,24 @@ def main():
     ap.add_argument("--cap", type=float, default=12.5e9, help="producer rate cap, bytes/s (12.5e9 = 100 Gbps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-producer", action="store_true", help="skip the producer TTFT modes")
+    ap.add_argument("--isolated-passes", type=int, default=2, help="passes of the isolated ingest leg (0: skip)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--second-workload", default="8b-4k",
+                    help="workload whose TTFT legs are reported beside the main one ('' to skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help=f"{CALIB_COPIES} plain {CALIB_BYTES >> 20} MiB device copies before the steps")
+    ap.add_argument("--profile-summary", nargs="+", metavar="DB",
+                    help="print a markdown summary of rocprofv3 databases of a run of this script")
     args = ap.parse_args()
 
+    if args.profile_summary:
+        print(profile_summary(args.profile_summary, args.workload, args.warmup, args.steps))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the path has no cross-GPU part (see DESIGN.md for how it would "
+        print("bench.py measures one GPU: the path has no cross-GPU part (DESIGN.md describes how it would "
               "shard); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
-
-    import torch
-    import kvgen
-    import paper_2605_22850_amd as oc
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    torch.cuda.set_device(0)
-    wl = kvgen.workload(args.workload)
-    L, nq, nkv, d = wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
-    b = 2 * nkv * d * 2
-    layout, pool, reqs, objs_all, tables = setup(wl)
-
-    # ---- timed steps: device-staged pipeline, all layers ----
-    for i in range(args.warmup):
-        run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, 1)
-        log(f"[bench] warmup {i + 1}/{args.warmup}")
-    ctx = oc.oc_context_create(pool, layout, oc.OC_MODE_DEVICE_STAGED, max(wl.prefix_tokens),
-                               max(wl.suffix_tokens))
-    ingest_ms, stage_ms, stats_all = 0.0, [], []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        st = oc.oc_pipeline_run(ctx, reqs, L)
-        stats_all.append(st)
-        stage_ms.append(oc.oc_pipeline_last_ms(ctx))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    oc.oc_context_destroy(ctx)
-    log(f"[bench] {args.steps} steps in {wall:.3f} s")
-    n_ingest = 0
-    for st in stats_all:
-        for rst in st:
-            for l in range(L):
-                ingest_ms += rst["ingested_ms"][l] - rst["landed_ms"][l]
-                n_ingest += 1
-    ingest_bytes_per_step = 2.0 * sum(wl.prefix_tokens) * b * L       # read + write, every layer
-    value = ingest_bytes_per_step * args.steps / (ingest_ms / 1e3) / 1e9
-    per_launch_bytes = 2.0 * sum(wl.prefix_tokens) * b / wl.n_requests
-    mean_launch_us = ingest_ms / n_ingest * 1e3
-
-    # ---- TTFT modes ----
-    trials = max(2, args.trials)
-    hbm = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_HBM_RESIDENT, trials)
-    log("[bench] hbm-resident trials done")
-    dev = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, trials)
-    log("[bench] device-staged trials done")
-    t_hbm = [x[0] for x in hbm[1:]]
-    t_dev = [x[0] for x in dev[1:]]
-    # attention: per-layer compute of the attention-only pass
-    total_flops = sum(attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r]) for r in range(wl.n_requests)) * L
-    attn_tflops = total_flops / (sum(t_hbm) / len(t_hbm) / 1e3) / 1e12
-    ttft = {"hbm_resident": mean_std(t_hbm), "device_staged": mean_std(t_dev)}
-    res = {}
-    if not args.no_producer:
-        unc = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=0.0)
-        log("[bench] producer uncapped trials done")
-        cap = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=args.cap)
-        log("[bench] producer capped trials done")
-        ttft["producer_uncapped"] = mean_std(x[0] for x in unc[1:])
-        ttft["producer_capped"] = mean_std(x[0] for x in cap[1:])
-        # eq. (3) floor at the cap: X_l = bytes of layer l / cap, C_l = measured device-staged per-layer time
-        layer_bytes = sum(wl.prefix_tokens) * b
-        X = [layer_bytes / args.cap * 1e3] * L
-        C = [ttft["device_staged"][0] / L] * L
-        floor = layerwise_floor(X, C)
-        res = {"added_ttft_ms": round(ttft["producer_capped"][0] - ttft["hbm_resident"][0], 3),
-               "eq3_floor_ms": round(floor, 3),
-               "cap_vs_floor": round(ttft["producer_capped"][0] / floor, 4),
-               "arrival_floor_ms": round(L * layer_bytes / args.cap * 1e3, 3)}
-    gates = {"device_staged_over_hbm": round((ttft["device_staged"][0] - ttft["hbm_resident"][0]) /
-                                             ttft["hbm_resident"][0], 4)}
-
-    line = {
-        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(wall / args.steps * 1e3, 3), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic: seeded N(0,1) bf16 KV/Q, Fisher-Yates block tables",
-        "config": {"workload": wl.name, "layers": L, "q_heads": nq, "kv_heads": nkv, "head_dim": d,
-                   "prefix_tokens": wl.prefix_tokens if wl.n_requests > 1 else wl.prefix_tokens[0],
-                   "suffix_tokens": wl.suffix_tokens if wl.n_requests > 1 else wl.suffix_tokens[0],
-                   "page_tokens": wl.page_size, "chunk_tokens": wl.chunk_tokens, "pool_pages": wl.pool_pages,
-                   "step": "device-staged pipeline: per layer ingest (copy stream) then attention (compute "
-                           "stream), all layers"},
-        "roofline": {"bound": "hbm", "kernel": "kv_ingest_kernel", "achieved": round(value, 2),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": per_launch_bytes,
-                     "mean_launch_us": round(mean_launch_us, 3)},
-        "attention": {"tflops": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
-                      "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
-                      "flops_per_layer": total_flops / L,
-                      "ms_per_layer": round(ttft["hbm_resident"][0] / L, 4)},
-        "ttft_ms": ttft, **res, "gates": gates,
-        "device_staged_ms": mean_std(stage_ms),
-    }
-    if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle) ...")
-        line["cpu_baseline"] = cpu_baseline(wl, objs_all, tables, args.cpu_budget)
-    print(json.dumps(line), flush=True)
+    run_bench(args)
 
 
 if __name__ == "__main__":

@@ -210,7 +210,10 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
 
 /* Run the pipeline over n_reqs requests for all L layers; synchronous.
  * stats (optional) has n_reqs entries.  On OC_ETIMEOUT / OC_EABORT the run is
- * stopped, all enqueued GPU work is drained and the context stays usable. */
+ * stopped, all enqueued GPU work is drained and the context stays usable.
+ * The run's GPU work starts after all work enqueued so far on the device's
+ * null (legacy default) stream; work on other streams that writes the pool,
+ * tables or tensors of reqs must be complete before the call. */
 int oc_pipeline_run(void *ctx, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats);
 
 /* Time of the whole last run (ms, start -> last layer of the last request). */

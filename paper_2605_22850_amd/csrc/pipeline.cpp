@@ -43,6 +43,7 @@ struct Context {
     void *ws = nullptr;
     size_t ws_bytes = 0;
     std::vector<hipEvent_t> events;    // pool of timing events, reused across runs
+    hipEvent_t caller_done = nullptr;  // null-stream work enqueued before a run
     double last_ms = 0.0;
 };
 
@@ -83,6 +84,7 @@ static void release(Context *c) {
         if (s.device) hipFree(s.device);
     }
     for (auto e : c->events) hipEventDestroy(e);
+    if (c->caller_done) hipEventDestroy(c->caller_done);
     if (c->ws) hipFree(c->ws);
     if (c->copy) hipStreamDestroy(c->copy);
     if (c->compute) hipStreamDestroy(c->compute);
@@ -316,6 +318,12 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     OC_HIP(hipSetDevice(c->device));
     OC_HIP(hipStreamSynchronize(c->copy));
     OC_HIP(hipStreamSynchronize(c->compute));
+    // The context's streams are non-blocking, so nothing orders them after
+    // what the caller enqueued on the null stream (filling the pool, copying
+    // tables and suffix tensors): wait for that work on the device first.
+    OC_HIP(hipEventRecord(c->caller_done, nullptr));
+    OC_HIP(hipStreamWaitEvent(c->copy, c->caller_done, 0));
+    OC_HIP(hipStreamWaitEvent(c->compute, c->caller_done, 0));
 
     RunShared sh;
     Producer prod{};
@@ -523,6 +531,10 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
         hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking) != hipSuccess) {
         release(c);
         return fail(OC_EHIP, "stream creation failed");
+    }
+    if (hipEventCreateWithFlags(&c->caller_done, hipEventDisableTiming) != hipSuccess) {
+        release(c);
+        return fail(OC_EHIP, "event creation failed");
     }
     if (c->opts.mode == OC_MODE_PRODUCER && c->slot_bytes > 0) {
         c->slots.resize((size_t)c->opts.slots);

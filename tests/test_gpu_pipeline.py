@@ -8,7 +8,7 @@ import time
 import numpy as np
 import pytest
 
-from tests.gpu_util import RequestSet, assert_attention_close, from_dev, require_gpu
+from tests.gpu_util import SENTINEL, RequestSet, assert_attention_close, from_dev, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -84,6 +84,27 @@ def test_two_slot_ring_with_racing_producer():
     assert np.array_equal(got, _outs(rs)[0])
     for l in (0, 5):
         assert_attention_close(got[l], rs.expected_out(0, l), f"layer {l}")
+
+
+def test_run_waits_for_null_stream_work():
+    # the 1 GiB pool is refilled 16 times on torch's default stream right
+    # before the run, with no synchronisation in between: the run must start
+    # after those fills, or they would overwrite pages it has ingested
+    import paper_2605_22850_amd as oc
+    print("[pipeline] ordering after null-stream work", flush=True)
+    rs = RequestSet(2, 4, 2, 64, [256], [32], 65536, seed=3).upload(with_payload=True)
+    want = rs.expected_pool()
+    ctx = rs.context(oc.OC_MODE_DEVICE_STAGED)
+    try:
+        fill = np.int16(np.uint16(SENTINEL).view(np.int16))
+        for _ in range(16):
+            rs.d_pool.fill_(fill)
+        oc.oc_pipeline_run(ctx, rs.reqs, rs.L)
+    finally:
+        oc.oc_context_destroy(ctx)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want)
+    for l in range(rs.L):
+        assert_attention_close(from_dev(rs.reqs[0].out)[l], rs.expected_out(0, l), f"layer {l}")
 
 
 def test_batch_of_requests_sharing_pool_and_rate():

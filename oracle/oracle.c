@@ -19,9 +19,9 @@
  *
  * bfloat16 values travel as uint16 bit patterns and are widened exactly.
  * Pool layout (a design choice; the paper leaves the paged layout to the
- * serving engine):  pool[L][2][P][n_kv][block], where the block of (layer,
- * K, page, head) is [slot][dim] and the block of (layer, V, page, head) is
- * [dim][slot].
+ * serving engine):  pool[L][2][P][n_kv][Ps][d] -- for each layer, K then V;
+ * each (page, head) block holds its page's slots in order, one d-element row
+ * per slot, for K and V alike.
  */
 #include <math.h>
 #include <pthread.h>
@@ -66,9 +66,7 @@ void oco_logical_kv(const uint16_t *const *chunks, int64_t n_chunks, int32_t G, 
 static int64_t pool_index(int32_t l, int32_t m, int64_t page, int32_t h, int32_t slot, int32_t e,
                           int64_t P, int32_t n_kv, int32_t Ps, int32_t d) {
     int64_t block = (((int64_t)l * 2 + m) * P + page) * n_kv + h;
-    int64_t base = block * (int64_t)Ps * d;
-    if (m == 0) return base + (int64_t)slot * d + e;   /* K: [slot][dim] */
-    return base + (int64_t)e * Ps + slot;              /* V: [dim][slot] */
+    return (block * Ps + slot) * (int64_t)d + e;       /* [slot][dim] for K and V */
 }
 
 /* Scatter one layer's staging payload (concatenated layer slices of n_chunks

@@ -80,16 +80,15 @@ SENTINEL = 0xBEEF
 
 def _numpy_scatter(staging, n_chunks, G, nkv, d, Ps, table, pool, layer):
     """Independent formulation: reshape + fancy indexing.  The block table
-    maps logical token T to (page table[T // Ps], slot T % Ps); K pages are
-    [slot][dim], V pages [dim][slot]."""
+    maps logical token T to (page table[T // Ps], slot T % Ps); K and V
+    pages are [slot][dim]."""
     L, _, P = pool.shape[:3]
     x = staging.reshape(n_chunks, 2, G, nkv, d).transpose(1, 0, 2, 3, 4).reshape(2, n_chunks * G, nkv, d)
     T = np.arange(n_chunks * G)
     pages, slots = table[T // Ps], T % Ps
-    k_view = pool.reshape(L, 2, P, nkv, Ps, d)
-    v_view = pool.reshape(L, 2, P, nkv, d, Ps)
-    k_view[layer, 0, pages, :, slots, :] = x[0]
-    v_view[layer, 1, pages, :, :, slots] = x[1]
+    view = pool.reshape(L, 2, P, nkv, Ps, d)
+    view[layer, 0, pages, :, slots, :] = x[0]
+    view[layer, 1, pages, :, slots, :] = x[1]
 
 
 @pytest.mark.parametrize("G,Ps,n_chunks,nkv,d", [
@@ -137,9 +136,9 @@ def test_paged_read_returns_logical_token():
             page, slot = table[T // Ps], T % Ps
             for h in range(nkv):
                 blk_k = pool[layer, 0, page, h].reshape(Ps, d)
-                blk_v = pool[layer, 1, page, h].reshape(d, Ps)
+                blk_v = pool[layer, 1, page, h].reshape(Ps, d)
                 assert np.array_equal(blk_k[slot], k[T, h])
-                assert np.array_equal(blk_v[:, slot], v[T, h])
+                assert np.array_equal(blk_v[slot], v[T, h])
 
 
 def test_ingest_copies_nan_and_denormal_bits():

@@ -57,15 +57,14 @@ typedef struct {
     int32_t num_kv_heads;   /* n_kv                                           */
     int32_t head_dim;       /* d, 64 or 128                                   */
     int32_t page_size;      /* tokens per pool page, a multiple of 8          */
-    int32_t chunk_tokens;   /* G, tokens per stored chunk, a multiple of 8    */
+    int32_t chunk_tokens;   /* G, tokens per stored chunk                     */
     int64_t num_pages;      /* P, pages in the pool                           */
 } oc_layout;
 
 /* Paged KV pool, device memory of L*2*P*n_kv*page_size*d bfloat16 values laid
- * out [L][2][P][n_kv][block].  The block of (layer, K, page, head) is
- * [slot][dim]; the block of (layer, V, page, head) is [dim][slot] (values
- * transposed inside the page so the attention reads keys contiguously).
- * 16-byte aligned. */
+ * out [L][2][P][n_kv][page_size][d]: per layer the K region then the V
+ * region; each (page, head) block holds its slots in order, one d-element
+ * row per slot, for K and V alike.  16-byte aligned. */
 typedef struct {
     void *base;
     oc_layout layout;
@@ -121,7 +120,8 @@ int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_p
                        int32_t layer, void *staging_out, int64_t num_chunks,
                        int64_t per_layer_chunk_bytes, void *stream);
 
-/* Bytes of device workspace oc_suffix_prefill_layer needs for these lengths. */
+/* Bytes of device workspace oc_suffix_prefill_layer needs for these lengths
+ * (at least 256; 0 means the layout or lengths are not supported). */
 size_t oc_attention_workspace_bytes(const oc_layout *layout, int64_t prefix_tokens,
                                     int64_t suffix_tokens);
 

@@ -28,7 +28,6 @@ static int check_layout(const oc_layout &l) {
     if (l.num_q_heads % l.num_kv_heads != 0) return fail(OC_ESHAPE, "num_q_heads must be a multiple of num_kv_heads");
     if (l.head_dim % 8 != 0) return fail(OC_ESHAPE, "head_dim must be a multiple of 8");
     if (l.page_size % 8 != 0) return fail(OC_ESHAPE, "page_size must be a multiple of 8");
-    if (l.chunk_tokens % 8 != 0) return fail(OC_ESHAPE, "chunk_tokens must be a multiple of 8");
     return OC_OK;
 }
 
@@ -115,7 +114,7 @@ int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_ta
         return fail(OC_EALIGN, "staging data and pool base must be 16-byte aligned");
     IngestArgs a = ingest_args(kv_pool, block_table, layer, staging->data);
     const int64_t n_pages = (block_table->num_tokens + l.page_size - 1) / l.page_size;
-    OC_HIP(launch_ingest(a, n_pages, static_cast<hipStream_t>(stream)));
+    OC_HIP(launch_ingest(a, n_pages, static_cast<hipStream_t>(stream), false));
     return OC_OK;
 }
 

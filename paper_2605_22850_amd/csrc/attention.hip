@@ -3,28 +3,28 @@
 //
 // Work split: for each KV head g the query rows are the (suffix token, query
 // head of g's group) pairs, token-major, so one 32-row MFMA block shares
-// tokens across the group's heads (GQA packing).  A workgroup of 4 wavefronts
-// owns 4 x 64 rows and one contiguous range of 64-key blocks; key ranges are
-// split over workgroups (split-KV) so long prefixes fill the chip, and a
-// combine kernel merges the splits by log-sum-exp.  Workgroups that read the
-// same K/V pages (same KV head and split) are dispatched back to back onto
+// tokens across the group's heads (GQA packing).  A workgroup of 8
+// wavefronts owns 8 x 32 rows and one contiguous range of 64-key blocks; key
+// ranges are split over workgroups (split-KV) so long prefixes fill the chip,
+// and a combine kernel merges the splits by log-sum-exp.  Workgroups that read
+// the same K/V pages (same KV head and split) are dispatched back to back onto
 // the same XCD, so their re-reads hit that XCD's L2.
 //
-// Per 64-key block: K ([key][dim]) and V ([dim][key], as the pool stores it)
-// are staged into double-buffered LDS tiles whose 16-byte columns are XOR
-// swizzled by row, so the MFMA operand reads (one row per lane) are free of
-// bank conflicts; the global loads for block b+2 are in flight while block b
-// computes, with a single barrier per block.  Each wavefront computes
-// S^T = K Q^T for its two 32-query blocks with bf16 MFMA 32x32x16 (fp32
-// accumulate; every K fragment read from LDS feeds both blocks), runs the
-// online softmax with one query column per lane (the two half-waves combine
-// their maxima with a lane swap; the running maximum is only raised -- and O
-// rescaled -- when a block's maximum exceeds it by more than 2^8), converts P
-// to bf16 and accumulates O^T += V^T P, each V fragment again feeding both
-// blocks.  The K tile's rows are fed to the MFMA in an order (bits 2 and 3 of
-// the row swapped) that leaves each half-wave holding eight consecutive keys
-// of P, matching eight consecutive keys of one V row: both operands load as
-// 16-byte vectors without an in-register transpose.
+// Per 64-key block: the K and V rows of four pages ([slot][dim] pool blocks,
+// or for the suffix the k_new / v_new rows themselves) are copied straight
+// into token-major LDS tiles by the global->LDS load path, three blocks in
+// flight, one barrier per block.  The tiles' 16-byte columns are XOR-swizzled
+// by row so the operand reads are free of bank conflicts.  Each wavefront
+// computes S^T = K Q^T for its 32 queries with bf16 MFMA 32x32x16 (fp32
+// accumulate), runs the online softmax with one query column per lane (the
+// two half-waves combine their maxima with a lane swap; the running maximum
+// is only raised -- and O rescaled -- when a block's maximum exceeds it by more
+// than 2^8), converts P to bf16 and accumulates O^T += V^T P.  The V^T operand
+// (eight consecutive keys of one dimension per lane) comes from two
+// transposing LDS reads of the token-major V tile.  The K tile's rows are fed
+// to the MFMA in an order (bits 2 and 3 of the row swapped) that leaves each
+// half-wave holding eight consecutive keys of P, matching those eight keys of
+// the V operand.
 #include <math.h>
 
 #include "common.hpp"
@@ -52,33 +52,13 @@ struct KParams {
     const uint16_t *q;
     const uint16_t *pool_k, *pool_v;
     const int32_t *pages;
-    const uint16_t *ks, *vs;      // suffix pages packed like pool pages
+    const uint16_t *k_new, *v_new;   // suffix rows [Ts][nkv][D]
     float *o_part, *ml_part;
     uint16_t *out;
     int64_t Tp, Ts, rows, rows_pad, n_pre_pages, n_suf_pages, n_blocks, blocks_per_split;
     int nq, nkv, grp, m_tiles, n_split, n_groups;
     float scale_log2;
 };
-
-// ---------------------------------------------------------------------------
-// suffix K/V into page-shaped blocks (K [slot][dim], V [dim][slot]), zero past Ts
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void suffix_pack_kernel(const uint16_t *__restrict__ k_new,
-                                                          const uint16_t *__restrict__ v_new,
-                                                          uint16_t *__restrict__ ks, uint16_t *__restrict__ vs,
-                                                          int64_t Ts, int nkv, int d) {
-    const int64_t u = blockIdx.x;
-    const int h = blockIdx.y;
-    const int n = PAGE * d;
-    for (int idx = threadIdx.x; idx < n; idx += 256) {
-        int s = idx / d, e = idx - s * d;
-        int64_t T = u * PAGE + s;
-        ks[((u * nkv + h) * PAGE + s) * d + e] = T < Ts ? k_new[(T * nkv + h) * d + e] : (uint16_t)0;
-        int e2 = idx / PAGE, s2 = idx - e2 * PAGE;
-        int64_t T2 = u * PAGE + s2;
-        vs[((u * nkv + h) * d + e2) * PAGE + s2] = T2 < Ts ? v_new[(T2 * nkv + h) * d + e2] : (uint16_t)0;
-    }
-}
 
 // value of the lane 32 positions away (the other half of the wavefront)
 __device__ inline float half_swap_max(float x) {
@@ -105,7 +85,17 @@ __device__ inline int k_lds(int r, int c) {
     return r * D + ((c ^ (r & (NS - 1))) << 3);
 }
 
+// XOR applied to the 16-byte column index of V tile row r.  The transposing
+// reads of the PV operand take 4 dims x 4 keys per 16-lane group, from rows
+// that differ in their low key bits; this spreads those rows over all banks.
+template <int D>
+__device__ inline int v_swz(int r) {
+    if constexpr (D == 128) return 4 * (r & 3);
+    else return 4 * ((r >> 1) & 1);
+}
+
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(1))) const void *gbl_ptr_t;
 
 // one 16-byte global -> LDS copy per lane; the wavefront's 64 lanes fill 1 KiB
@@ -186,18 +176,6 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     // space so the uniform page lookups become scalar loads
     const __attribute__((address_space(4))) int32_t *pages_c =
         (const __attribute__((address_space(4))) int32_t *)p.pages;
-    auto page_src = [&](int64_t v, const uint16_t *&kb, const uint16_t *&vb) {
-        if (v < p.n_pre_pages) {
-            const int64_t page = pages_c[v];
-            kb = p.pool_k + (page * p.nkv + g) * head_block;
-            vb = p.pool_v + (page * p.nkv + g) * head_block;
-        } else {
-            int64_t su = v - p.n_pre_pages;
-            if (su >= p.n_suf_pages) su = 0;   // past the end: any finite page, fully masked
-            kb = p.ks + (su * p.nkv + g) * head_block;
-            vb = p.vs + (su * p.nkv + g) * head_block;
-        }
-    };
     auto issue_block = [&](int64_t b, int buf) {
         uint16_t *kt_lds = lds + buf * 2 * TILE;
         uint16_t *vt_lds = kt_lds + TILE;
@@ -205,13 +183,25 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
         for (int u = 0; u < CPW; ++u) {
             const int q = u * WAVES + wave;                   // chunk index, uniform per wavefront
             const int pg = q / CPP;                           // its page within the block
-            const int qi = q % CPP;                           // chunk within the page
-            const uint16_t *kb, *vb;
-            page_src(b * 4 + pg, kb, vb);
-            const int r = qi * KROWS + lane / (D / 8);        // key row within the page
-            const int c = (lane % (D / 8)) ^ ((pg * PAGE + r) & (D / 8 - 1));
-            dma16(kb + r * D + c * 8, kt_lds + q * 512);
-            dma16(vb + qi * 512 + lane * 8, vt_lds + q * 512);
+            const int r = (q % CPP) * KROWS + lane / (D / 8); // key row within the page
+            const int ck = (lane % (D / 8)) ^ (r & (D / 8 - 1));
+            const int cv = (lane % (D / 8)) ^ v_swz<D>(r);
+            const int64_t v = b * 4 + pg;                     // page of the key sequence
+            const uint16_t *krow, *vrow;
+            if (v < p.n_pre_pages) {
+                const int64_t blk = ((int64_t)pages_c[v] * p.nkv + g) * head_block + r * D;
+                krow = p.pool_k + blk;
+                vrow = p.pool_v + blk;
+            } else {
+                // suffix token; rows past the last one repeat it (finite, and masked)
+                int64_t T = (v - p.n_pre_pages) * PAGE + r;
+                if (T > p.Ts - 1) T = p.Ts - 1;
+                const int64_t row = (T * p.nkv + g) * D;
+                krow = p.k_new + row;
+                vrow = p.v_new + row;
+            }
+            dma16(krow + ck * 8, kt_lds + q * 512);
+            dma16(vrow + cv * 8, vt_lds + q * 512);
         }
     };
 
@@ -227,6 +217,20 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
         l_run[qb] = 0.f;
     }
     const int krow = key_perm(col);
+    // Transposing V reads: in each 16-lane group, source lane 4j+q names the
+    // four dims [4q, 4q+4) of key row j; output lane i then holds dim i of
+    // the four rows.  Group k covers dims 16*(k%2) + [0,16) and keys
+    // 8*(k/2) + [0,4) of the 16-key slice (the second read adds 4 rows).
+    int voff[D / 32];
+    {
+        const int k16 = lane >> 4, j = (lane >> 2) & 3, q4 = lane & 3;
+        const int key = 8 * (k16 >> 1) + j;
+#pragma unroll
+        for (int et = 0; et < D / 32; ++et) {
+            const int dim = et * 32 + 16 * (k16 & 1) + 4 * q4;
+            voff[et] = key * D + (((dim >> 3) ^ v_swz<D>(key)) << 3) + (dim & 7);
+        }
+    }
 
     if (b0 < b1) issue_block(b0, 0);
     if (b0 + 1 < b1) issue_block(b0 + 1, 1);
@@ -247,10 +251,7 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
             // last, partial prefix page: its slots past Tp may hold anything;
             // zero them so masked keys contribute exactly nothing
             const int pg = (int)(full_pre_pages - b * 4), k0 = (int)(p.Tp % PAGE);
-            for (int idx = tid; idx < D * (PAGE - k0); idx += THREADS) {
-                const int e = idx / (PAGE - k0), k = k0 + idx % (PAGE - k0);
-                V[(pg * D + e) * PAGE + k] = 0;
-            }
+            for (int idx = tid; idx < D * (PAGE - k0); idx += THREADS) V[(pg * PAGE + k0) * D + idx] = 0;
             lds_barrier();
         }
 
@@ -337,7 +338,10 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
                 }
 #pragma unroll
                 for (int et = 0; et < D / 32; ++et) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(&V[((kt * 2 + hf) * D + et * 32 + col) * PAGE + half * 8]);
+                    const uint16_t *vp = V + voff[et] + (kt * 32 + hf * 16) * D;
+                    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)vp);
+                    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vp + 4 * D));
+                    const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
                     for (int qb = 0; qb < QB; ++qb)
                         oacc[qb][et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[qb], oacc[qb][et], 0, 0, 0);
@@ -442,15 +446,11 @@ int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *pl) {
     p.n_split = (int)((p.n_blocks + p.blocks_per_split - 1) / p.blocks_per_split);
     const int64_t rows_pad = (int64_t)p.m_tiles * TILE_ROWS;
     size_t off = 0;
-    p.off_ks = off;
-    off = round_up(off + (size_t)p.n_suf_pages * p.nkv * PAGE * p.d * 2, 256);
-    p.off_vs = off;
-    off = round_up(off + (size_t)p.n_suf_pages * p.nkv * PAGE * p.d * 2, 256);
     p.off_o = off;
     if (p.n_split > 1) off = round_up(off + (size_t)p.n_split * p.nkv * rows_pad * p.d * 4, 256);
     p.off_ml = off;
     if (p.n_split > 1) off = round_up(off + (size_t)p.n_split * p.nkv * rows_pad * 2 * 4, 256);
-    p.total = off;
+    p.total = off > 256 ? off : 256;   // never 0: a size of 0 reports an unsupported shape
     *pl = p;
     return OC_OK;
 }
@@ -462,8 +462,8 @@ static hipError_t launch_d(const AttnPlan &pl, const AttnArgs &a, hipStream_t s)
     p.pool_k = a.pool_k;
     p.pool_v = a.pool_v;
     p.pages = a.pages;
-    p.ks = reinterpret_cast<const uint16_t *>(a.ws + pl.off_ks);
-    p.vs = reinterpret_cast<const uint16_t *>(a.ws + pl.off_vs);
+    p.k_new = a.k_new;
+    p.v_new = a.v_new;
     p.o_part = reinterpret_cast<float *>(a.ws + pl.off_o);
     p.ml_part = reinterpret_cast<float *>(a.ws + pl.off_ml);
     p.out = a.out;
@@ -483,9 +483,6 @@ static hipError_t launch_d(const AttnPlan &pl, const AttnArgs &a, hipStream_t s)
     p.n_groups = pl.nkv * pl.n_split;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
 
-    hipLaunchKernelGGL(suffix_pack_kernel, dim3((unsigned)pl.n_suf_pages, (unsigned)pl.nkv), dim3(256), 0, s,
-                       a.k_new, a.v_new, const_cast<uint16_t *>(p.ks), const_cast<uint16_t *>(p.vs), pl.Ts,
-                       pl.nkv, D);
     const int64_t groups_per_xcd = (p.n_groups + 7) / 8;
     const int64_t grid = 8 * groups_per_xcd * pl.m_tiles;
     static bool lds_set = false;

@@ -33,10 +33,14 @@ struct IngestArgs {
     const int32_t *pages;
     int64_t num_tokens;        // T_p
     int32_t G, n_kv, d, Ps;
+    // filled by the launcher
+    int64_t region;            // pool_v - pool_k, elements
+    int32_t d8, lg_d8, lg_ps, lg_nkv, lg_g;
 };
-hipError_t launch_ingest(const IngestArgs &a, int64_t n_pages_used, hipStream_t s);
-hipError_t launch_gather(const IngestArgs &a, uint16_t *staging_out, int64_t n_pages_used,
-                         hipStream_t s);
+// beside_compute: launched to run next to the attention kernel (more bytes in
+// flight per thread) rather than alone on the GPU
+hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool beside_compute);
+hipError_t launch_gather(IngestArgs a, uint16_t *staging_out, int64_t n_pages_used, hipStream_t s);
 
 // ---- attention --------------------------------------------------------------
 struct AttnPlan {
@@ -49,8 +53,8 @@ struct AttnPlan {
     int64_t n_suf_pages;       // ceil(Ts / 16)
     int64_t n_blocks;          // key blocks of 64 keys over prefix then suffix pages
     int64_t blocks_per_split;
-    // workspace carve-up (byte offsets)
-    size_t off_ks, off_vs, off_o, off_ml, total;
+    // workspace carve-up (byte offsets): split partials
+    size_t off_o, off_ml, total;
 };
 int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *plan);
 

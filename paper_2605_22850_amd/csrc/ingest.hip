@@ -2,14 +2,18 @@
 // of the matched chunk objects, Section 3.3) and scatter it into the paged
 // pool through the block table.
 //
-// One thread moves one 8-token x 8-dim block of one head: eight 16-byte
-// rows of K and eight of V.  K rows keep their [slot][dim] order; V rows are
-// transposed in registers (16-bit lane permutes) and leave as eight 16-byte
-// runs of the pool's [dim][slot] V block.  Neighbouring threads take
-// neighbouring 8-dim groups, so every load and K store is a contiguous
-// 256-byte run per (token, head) across 16 lanes.  No LDS and little index
-// arithmetic: the kernel is pure HBM traffic and stays small enough (<= 64
-// VGPRs) to run beside the attention kernel of the previous layer.
+// Both sides keep one head's d-element row per token, so the scatter is a
+// copy of 16-byte pieces with remapped addresses: the payload holds the rows
+// of a chunk token-major ([K|V][token][head][dim]), the pool holds them per
+// (page, head) block ([slot][dim]).  Two launch shapes:
+//  - alone on the GPU (the single-layer entry point, the first layer of a
+//    run): pieces numbered by (page of the prefix, head), then K/V, slot and
+//    16-byte column, two per thread, 256 pieces apart, so a wavefront writes
+//    1 KiB of one block contiguously and many short wavefronts stream;
+//  - beside the attention kernel of an earlier layer, where one ingest
+//    wavefront per SIMD fits: a thread takes 8 slots x one 16-byte column of
+//    one (page, head) block and moves its K rows, then its V rows (8 loads in
+//    flight, one page lookup per 256 bytes moved).
 #include "common.hpp"
 
 namespace oc {
@@ -18,140 +22,169 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 
-// Column k of an 8x8 block of 16-bit elements whose row i is in[i]
-// (8 elements, two per dword).
-__device__ inline u32x4 column8(const u32x4 (&in)[8], int k) {
-    const int w = k >> 1;
-    uint32_t o[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const uint32_t a = in[2 * j][w], b = in[2 * j + 1][w];
-        o[j] = (k & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+// Piece p -> (payload offset, pool offset from the K region base).  With
+// POW2 every divisor (d/8, page size, KV heads, chunk size) is a power of two
+// and the decode is shifts and masks.
+template <bool POW2>
+__device__ inline bool piece_offsets(const IngestArgs &a, int64_t p, int64_t n_units, int64_t &pay, int64_t &pool) {
+    const int d = a.d, nkv = a.n_kv, Ps = a.Ps, G = a.G;
+    int64_t unit, q, T, j, t0;
+    int c, slot, kv, h;
+    if (POW2) {
+        c = (int)(p & (a.d8 - 1));
+        slot = (int)((p >> a.lg_d8) & (Ps - 1));
+        kv = (int)((p >> (a.lg_d8 + a.lg_ps)) & 1);
+        unit = p >> (a.lg_d8 + a.lg_ps + 1);
+        h = (int)(unit & (nkv - 1));
+        q = unit >> a.lg_nkv;
+        T = (q << a.lg_ps) + slot;
+        j = T >> a.lg_g;
+        t0 = T & (G - 1);
+    } else {
+        const int64_t unit_pieces = 2LL * Ps * a.d8;
+        unit = p / unit_pieces;
+        const int pi = (int)(p - unit * unit_pieces);
+        c = pi % a.d8;
+        slot = (pi / a.d8) % Ps;
+        kv = pi / (a.d8 * Ps);
+        q = unit / nkv;
+        h = (int)(unit - q * nkv);
+        T = q * Ps + slot;
+        j = T / G;
+        t0 = T - j * G;
     }
-    return u32x4{o[0], o[1], o[2], o[3]};
+    if (unit >= n_units || T >= a.num_tokens) return false;
+    const int64_t D = (int64_t)nkv * d;
+    pay = ((j * 2 + kv) * G + t0) * D + (int64_t)h * d + c * 8;
+    const int64_t page = a.pages[q];
+    pool = kv * a.region + ((page * nkv + h) * Ps + slot) * (int64_t)d + c * 8;
+    return true;
 }
 
-struct Unit {
-    int64_t q;      // block-table index (page of the prefix)
-    int h, s8, e8;  // head, 8-slot group, 8-dim group
-};
+// FORWARD: payload -> pool (ingest); otherwise pool -> payload (gather).
+template <int U, bool POW2, bool FORWARD>
+__device__ inline void copy_pieces(const IngestArgs &a, uint16_t *payload_out, int64_t n_units) {
+    const int64_t first = (int64_t)blockIdx.x * kThreads * U + threadIdx.x;
+    u32x4 r[U];
+    int64_t keep[U];   // the offset the store needs: pool (ingest) or payload (gather)
+    bool ok[U];
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+        int64_t pay = 0, pool = 0;
+        ok[i] = piece_offsets<POW2>(a, first + (int64_t)i * kThreads, n_units, pay, pool);
+        if (ok[i]) r[i] = *reinterpret_cast<const u32x4 *>(FORWARD ? a.staging + pay : a.pool_k + pool);
+        keep[i] = FORWARD ? pool : pay;
+    }
+#pragma unroll
+    for (int i = 0; i < U; ++i)
+        if (ok[i]) *reinterpret_cast<u32x4 *>(FORWARD ? a.pool_k + keep[i] : payload_out + keep[i]) = r[i];
+}
 
-__device__ inline Unit unit_of(int64_t u, int d8, int s8n, int nkv) {
-    Unit r;
-    r.e8 = (int)(u % d8);
-    int64_t rest = u / d8;
-    r.s8 = (int)(rest % s8n);
-    rest /= s8n;
-    r.h = (int)(rest % nkv);
-    r.q = rest / nkv;
+template <int U, bool POW2>
+__global__ __launch_bounds__(kThreads, 8) void kv_ingest_kernel(IngestArgs a, int64_t n_units) {
+    copy_pieces<U, POW2, true>(a, nullptr, n_units);
+}
+
+// 8 slots x one 16-byte column of one (page, head) block, K then V.
+__global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs a, int64_t n_rows8) {
+    const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (u >= n_rows8) return;
+    const int d = a.d, Ps = a.Ps, G = a.G, nkv = a.n_kv;
+    const int c = (int)(u % a.d8);
+    int64_t rest = u / a.d8;
+    const int s8 = (int)(rest % (Ps / 8));
+    rest /= Ps / 8;
+    const int h = (int)(rest % nkv);
+    const int64_t q = rest / nkv;
+    const int64_t D = (int64_t)nkv * d;
+    const int64_t T0 = q * Ps + s8 * 8;                  // first token of the 8
+    const int64_t left = a.num_tokens - T0;
+    const int valid = left < 8 ? (int)left : 8;          // tokens inside the prefix
+    const int64_t page = a.pages[q];
+    uint16_t *kdst = a.pool_k + ((page * nkv + h) * Ps + s8 * 8) * (int64_t)d + c * 8;
+    const int64_t col = (int64_t)h * d + c * 8;
+    // payload row of token T0 + i, K matrix (the V row is G*D further on)
+    int64_t src[8];
+    if (G % 8 == 0) {
+        // the 8 tokens sit in one chunk, one payload row apart
+        const int64_t j = T0 / G, t0 = T0 - j * G;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) src[i] = (j * 2 * G + t0 + i) * D + col;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int64_t T = T0 + i, j = T / G;
+            src[i] = (j * 2 * G + (T - j * G)) * D + col;
+        }
+    }
+    u32x4 r[8];
+#pragma unroll
+    for (int kv = 0; kv < 2; ++kv) {
+        const int64_t off = kv * (int64_t)G * D;
+        uint16_t *dst = kdst + kv * a.region;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (i < valid) r[i] = *reinterpret_cast<const u32x4 *>(a.staging + src[i] + off);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (i < valid) *reinterpret_cast<u32x4 *>(dst + i * d) = r[i];
+    }
+}
+
+template <bool POW2>
+__global__ __launch_bounds__(kThreads, 8) void kv_gather_kernel(IngestArgs a, uint16_t *payload, int64_t n_units) {
+    copy_pieces<2, POW2, false>(a, payload, n_units);
+}
+
+static bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+static int lg(int64_t x) {
+    int r = 0;
+    while ((1LL << r) < x) ++r;
     return r;
 }
 
-__global__ __launch_bounds__(kThreads, 8) void kv_ingest_kernel(IngestArgs a, int64_t n_units) {
-    const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (u >= n_units) return;
-    const int d = a.d, Ps = a.Ps, G = a.G, nkv = a.n_kv;
-    const Unit w = unit_of(u, d >> 3, Ps >> 3, nkv);
-    const int64_t D = (int64_t)nkv * d;
-    const int64_t T0 = w.q * Ps + w.s8 * 8;                  // first token of the unit
-    const int64_t rest = a.num_tokens - T0;
-    const int valid = rest < 8 ? (int)rest : 8;              // tokens of the unit inside the prefix
-    const int64_t page = a.pages[w.q];
-    // G is a multiple of 8, so the unit's 8 tokens sit in one chunk
-    const int64_t j = T0 / G, t0 = T0 - j * G;
-    const uint16_t *src = a.staging + (j * 2 * G + t0) * D + (int64_t)w.h * d + w.e8 * 8;
-    const int64_t blk = (page * nkv + w.h) * (int64_t)Ps * d;  // (page, head) block
-
-    u32x4 r[8];
-    // K: rows straight to [slot][dim]
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (i < valid) r[i] = *reinterpret_cast<const u32x4 *>(src + i * D);
-    uint16_t *kdst = a.pool_k + blk + (int64_t)(w.s8 * 8) * d + w.e8 * 8;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (i < valid) *reinterpret_cast<u32x4 *>(kdst + i * d) = r[i];
-
-    // V: rows in, transposed, out as [dim][slot]
-    const uint16_t *vsrc = src + (int64_t)G * D;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        r[i] = i < valid ? *reinterpret_cast<const u32x4 *>(vsrc + i * D) : u32x4{0, 0, 0, 0};
-    // each column leaves as soon as it is formed, freeing its source dwords
-    uint16_t *vdst = a.pool_v + blk + (int64_t)(w.e8 * 8) * Ps + w.s8 * 8;
-    if (valid == 8) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) *reinterpret_cast<u32x4 *>(vdst + k * Ps) = column8(r, k);
-    } else {
-        // last, partial page: write only the slots that hold prefix tokens
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const u32x4 ck = column8(r, k);
-            uint16_t v[8];
-            __builtin_memcpy(v, &ck, 16);
-            for (int i = 0; i < valid; ++i) vdst[k * Ps + i] = v[i];
-        }
-    }
+// Fills the derived fields; returns whether the shift decode applies.
+static bool prepare(IngestArgs &a) {
+    a.d8 = a.d / 8;
+    a.region = (int64_t)(a.pool_v - a.pool_k);
+    const bool p2 = pow2(a.d8) && pow2(a.Ps) && pow2(a.n_kv) && pow2(a.G);
+    a.lg_d8 = lg(a.d8);
+    a.lg_ps = lg(a.Ps);
+    a.lg_nkv = lg(a.n_kv);
+    a.lg_g = lg(a.G);
+    return p2;
 }
 
-// Inverse: pool pages back into the staging layout (same units, transposes reversed).
-__global__ __launch_bounds__(kThreads, 8) void kv_gather_kernel(IngestArgs a, uint16_t *staging, int64_t n_units) {
-    const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (u >= n_units) return;
-    const int d = a.d, Ps = a.Ps, G = a.G, nkv = a.n_kv;
-    const Unit w = unit_of(u, d >> 3, Ps >> 3, nkv);
-    const int64_t D = (int64_t)nkv * d;
-    const int64_t T0 = w.q * Ps + w.s8 * 8;
-    const int64_t rest = a.num_tokens - T0;
-    const int valid = rest < 8 ? (int)rest : 8;
-    const int64_t page = a.pages[w.q];
-    const int64_t j = T0 / G, t0 = T0 - j * G;
-    uint16_t *dst = staging + (j * 2 * G + t0) * D + (int64_t)w.h * d + w.e8 * 8;
-    const int64_t blk = (page * nkv + w.h) * (int64_t)Ps * d;
-
-    u32x4 r[8];
-    const uint16_t *ksrc = a.pool_k + blk + (int64_t)(w.s8 * 8) * d + w.e8 * 8;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (i < valid) r[i] = *reinterpret_cast<const u32x4 *>(ksrc + i * d);
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (i < valid) *reinterpret_cast<u32x4 *>(dst + i * D) = r[i];
-
-    const uint16_t *vsrc = a.pool_v + blk + (int64_t)(w.e8 * 8) * Ps + w.s8 * 8;
-    if (valid == 8) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) r[k] = *reinterpret_cast<const u32x4 *>(vsrc + k * Ps);
-    } else {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            uint16_t v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-            for (int i = 0; i < valid; ++i) v[i] = vsrc[k * Ps + i];
-            __builtin_memcpy(&r[k], v, 16);
-        }
-    }
-    uint16_t *vdst = dst + (int64_t)G * D;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (i < valid) *reinterpret_cast<u32x4 *>(vdst + i * D) = column8(r, i);
+template <int U>
+static void launch_u(const IngestArgs &a, bool p2, int64_t n_units, hipStream_t s) {
+    const int64_t n = n_units * 2 * a.Ps * a.d8;
+    const dim3 grid((unsigned)((n + kThreads * U - 1) / (kThreads * U)));
+    if (p2) hipLaunchKernelGGL((kv_ingest_kernel<U, true>), grid, dim3(kThreads), 0, s, a, n_units);
+    else hipLaunchKernelGGL((kv_ingest_kernel<U, false>), grid, dim3(kThreads), 0, s, a, n_units);
 }
 
-static int64_t n_units(const IngestArgs &a, int64_t n_pages_used) {
-    return n_pages_used * a.n_kv * (a.d / 8) * (a.Ps / 8);
-}
-
-hipError_t launch_ingest(const IngestArgs &a, int64_t n_pages_used, hipStream_t s) {
+hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool beside_compute) {
     if (n_pages_used == 0) return hipSuccess;
-    const int64_t n = n_units(a, n_pages_used);
-    hipLaunchKernelGGL(kv_ingest_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, s, a, n);
+    const bool p2 = prepare(a);
+    const int64_t n_units = n_pages_used * a.n_kv;
+    if (beside_compute) {
+        const int64_t n = n_pages_used * a.n_kv * (a.Ps / 8) * a.d8;
+        hipLaunchKernelGGL(kv_ingest_rows_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                           s, a, n);
+    } else {
+        launch_u<2>(a, p2, n_units, s);
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_gather(const IngestArgs &a, uint16_t *staging_out, int64_t n_pages_used, hipStream_t s) {
+hipError_t launch_gather(IngestArgs a, uint16_t *payload_out, int64_t n_pages_used, hipStream_t s) {
     if (n_pages_used == 0) return hipSuccess;
-    const int64_t n = n_units(a, n_pages_used);
-    hipLaunchKernelGGL(kv_gather_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, s, a,
-                       staging_out, n);
+    const bool p2 = prepare(a);
+    const int64_t n_units = n_pages_used * a.n_kv;
+    const int64_t n = n_units * 2 * a.Ps * a.d8;
+    const dim3 grid((unsigned)((n + kThreads * 2 - 1) / (kThreads * 2)));
+    if (p2) hipLaunchKernelGGL(kv_gather_kernel<true>, grid, dim3(kThreads), 0, s, a, payload_out, n_units);
+    else hipLaunchKernelGGL(kv_gather_kernel<false>, grid, dim3(kThreads), 0, s, a, payload_out, n_units);
     return hipGetLastError();
 }
 

@@ -414,7 +414,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 a.n_kv = l.num_kv_heads;
                 a.d = l.head_dim;
                 a.Ps = l.page_size;
-                e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy);
+                e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy, k > 0);
             }
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
             if (e == hipSuccess) e = hipStreamWaitEvent(c->compute, ingested[k], 0);

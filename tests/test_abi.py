@@ -66,7 +66,7 @@ def test_ingest_validation():
     assert _ingest(_layout(num_q_heads=3)) == L.OC_ESHAPE
     assert _ingest(_layout(page_size=12)) == L.OC_ESHAPE
     assert _ingest(_layout(head_dim=60)) == L.OC_ESHAPE
-    assert _ingest(_layout(chunk_tokens=12), num_chunks=21, num_tokens=252) == L.OC_ESHAPE
+    assert _ingest(_layout(chunk_tokens=0)) == L.OC_EINVAL
     assert _ingest(_layout(num_pages=8)) == L.OC_ERANGE
     # nothing to do is not an error
     assert _ingest(lay, num_chunks=0, table_entries=0, num_tokens=0) == L.OC_OK

@@ -167,16 +167,27 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     const int64_t head_block = (int64_t)PAGE * D;      // elements of one (page, head) block
 
     // ---- global -> LDS copy of one 64-key block (4 pages) ----
-    // K tile: [key][dim], 16-byte columns XOR-swizzled by key row, so the
-    // MFMA reads (one key row per lane) hit distinct banks; each lane fetches
-    // the global piece that belongs at its fixed LDS position.  V tile:
-    // page-major [page][dim][16 keys], i.e. the pool's page blocks copied
-    // as they are.  Every 1 KiB chunk comes from a single page.
-    // the block table is read-only here: load it through the constant address
-    // space so the uniform page lookups become scalar loads
+    // Both tiles are token-major ([key][dim]) with 16-byte columns XOR-swizzled
+    // by key row (K for the S reads, V for the transposing PV reads); each
+    // lane fetches the global piece that belongs at its fixed LDS position.
+    // Every 1 KiB chunk comes from a single page; a wavefront copies CPW
+    // chunks of each tile.  The base pointers stay in registers, and the page
+    // ids of a block are loaded (scalar loads through the constant address
+    // space) one block ahead of its copy, so no copy waits on a lookup.
+    const uint16_t *const pool_k = p.pool_k, *const pool_v = p.pool_v;
+    const uint16_t *const k_new = p.k_new, *const v_new = p.v_new;
+    const int64_t n_pre_pages = p.n_pre_pages, Ts = p.Ts;
+    const int nkv = p.nkv;
     const __attribute__((address_space(4))) int32_t *pages_c =
         (const __attribute__((address_space(4))) int32_t *)p.pages;
-    auto issue_block = [&](int64_t b, int buf) {
+    auto load_pids = [&](int64_t b, int32_t (&pid)[CPW]) {
+#pragma unroll
+        for (int u = 0; u < CPW; ++u) {
+            const int64_t v = b * 4 + (u * WAVES + wave) / CPP;
+            pid[u] = v < n_pre_pages ? pages_c[v] : 0;
+        }
+    };
+    auto issue_block = [&](int64_t b, int buf, const int32_t (&pid)[CPW]) {
         uint16_t *kt_lds = lds + buf * 2 * TILE;
         uint16_t *vt_lds = kt_lds + TILE;
 #pragma unroll
@@ -188,17 +199,17 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
             const int cv = (lane % (D / 8)) ^ v_swz<D>(r);
             const int64_t v = b * 4 + pg;                     // page of the key sequence
             const uint16_t *krow, *vrow;
-            if (v < p.n_pre_pages) {
-                const int64_t blk = ((int64_t)pages_c[v] * p.nkv + g) * head_block + r * D;
-                krow = p.pool_k + blk;
-                vrow = p.pool_v + blk;
+            if (v < n_pre_pages) {
+                const int64_t blk = ((int64_t)pid[u] * nkv + g) * head_block + r * D;
+                krow = pool_k + blk;
+                vrow = pool_v + blk;
             } else {
                 // suffix token; rows past the last one repeat it (finite, and masked)
-                int64_t T = (v - p.n_pre_pages) * PAGE + r;
-                if (T > p.Ts - 1) T = p.Ts - 1;
-                const int64_t row = (T * p.nkv + g) * D;
-                krow = p.k_new + row;
-                vrow = p.v_new + row;
+                int64_t T = (v - n_pre_pages) * PAGE + r;
+                if (T > Ts - 1) T = Ts - 1;
+                const int64_t row = (T * nkv + g) * D;
+                krow = k_new + row;
+                vrow = v_new + row;
             }
             dma16(krow + ck * 8, kt_lds + q * 512);
             dma16(vrow + cv * 8, vt_lds + q * 512);
@@ -232,17 +243,27 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
         }
     }
 
-    if (b0 < b1) issue_block(b0, 0);
-    if (b0 + 1 < b1) issue_block(b0 + 1, 1);
-    for (int64_t b = b0; b < b1; ++b) {
-        const int i = (int)(b - b0);
+    const int nb = (int)(b1 > b0 ? b1 - b0 : 0);
+    int32_t pid[CPW];
+    if (nb > 0) {
+        load_pids(b0, pid);
+        issue_block(b0, 0, pid);
+    }
+    if (nb > 1) {
+        load_pids(b0 + 1, pid);
+        issue_block(b0 + 1, 1, pid);
+    }
+    if (nb > 2) load_pids(b0 + 2, pid);
+    for (int i = 0; i < nb; ++i) {
+        const int64_t b = b0 + i;
         const int buf = i % NBUF;
         // this block's copies are done (the next block's may still fly),
         // and every wavefront is past the block that last used buffer i+2
-        if (b + 1 < b1) wait_vmcnt<NDMA>();
+        if (i + 1 < nb) wait_vmcnt<NDMA>();
         else wait_vmcnt<0>();
         lds_barrier();
-        if (b + 2 < b1) issue_block(b + 2, (i + 2) % NBUF);
+        if (i + 2 < nb) issue_block(b + 2, (i + 2) % NBUF, pid);
+        if (i + 3 < nb) load_pids(b + 3, pid);
         const uint16_t *K = lds + buf * 2 * TILE;
         uint16_t *V = const_cast<uint16_t *>(K) + TILE;
 

@@ -7,7 +7,10 @@ Closed forms written from the paper:
   * eq. (3): layerwise-prefetch TTFT  X_0 + sum_{l<L-1} max(X_{l+1}, C_l) + C_{L-1};
   * Section 5.3: overlap requirement B_req = D_l / t_l with
     D_l = 2*n_kv*d*p*(P*r);
-  * Section 3.6, eq. (4): per-layer stall and the zero-stall rate r* = s/c.
+  * Section 3.6, eq. (4): per-layer stall and the zero-stall rate r* = s/c;
+  * Section 3.6, eqs. (5)-(7) and the evaluation's baselines: per-request
+    bandwidth under a shared cap B -- Equal, KV-prop, BW-prop, Stall-opt and
+    Calibrated Stall-opt.
 """
 from __future__ import annotations
 
@@ -59,3 +62,75 @@ def per_layer_stall(s: float, r: float, c: float) -> float:
 
 def zero_stall_rate(s: float, c: float) -> float:
     return s / c
+
+
+# ---------------------------------------------------------------------------
+# bandwidth allocation under a shared cap (Section 3.6; the baselines of the
+# multi-tenant evaluation).  s[i]: KV bytes request i transfers per layer;
+# c[i]: its per-layer compute window in seconds; B: shared budget in bytes/s.
+# ---------------------------------------------------------------------------
+
+def alloc_equal(B: float, n: int):
+    """Equal: the same share for every active request."""
+    return [B / n] * n
+
+
+def alloc_kv_prop(B: float, s: Sequence[float]):
+    """KV-prop: shares proportional to the retrieved KV bytes (per layer
+    bytes are the total over L, so the proportion is the same)."""
+    tot = float(sum(s))
+    return [B * x / tot for x in s]
+
+
+def alloc_bw_prop(B: float, s: Sequence[float], c: Sequence[float]):
+    """BW-prop: shares proportional to the zero-stall rates r*_i = s_i/c_i."""
+    rs = [zero_stall_rate(a, b) for a, b in zip(s, c)]
+    tot = sum(rs)
+    return [B * x / tot for x in rs]
+
+
+def stall_opt(B: float, s: Sequence[float], caps: Sequence[float]):
+    """eq. (6): minimise sum_i s_i / r_i  s.t.  sum_i r_i = B, 0 < r_i <= cap_i.
+
+    The objective is convex; at the optimum every request below its cap has
+    the same marginal value s_i / r_i^2 = lambda, so r_i = min(cap_i,
+    sqrt(s_i / lambda)).  sum_i r_i(lambda) falls as lambda grows: bisect on
+    lambda until the budget is met.  When the caps fit in B every request
+    gets its cap and the rest of the budget stays unassigned."""
+    if sum(caps) <= B:
+        return list(caps)
+
+    def total(lam):
+        return sum(min(cp, (x / lam) ** 0.5) for x, cp in zip(s, caps))
+
+    lo, hi = 1e-300, 1.0
+    while total(hi) > B:          # grow hi until the rates fit
+        hi *= 4.0
+    while total(lo) < B:          # lambda small enough that every request is capped
+        lo /= 4.0
+    for _ in range(400):
+        mid = (lo * hi) ** 0.5
+        if total(mid) > B:
+            lo = mid
+        else:
+            hi = mid
+        if hi / lo < 1 + 1e-15:
+            break
+    lam = (lo * hi) ** 0.5
+    return [min(cp, (x / lam) ** 0.5) for x, cp in zip(s, caps)]
+
+
+def alloc_stall_opt(B: float, s: Sequence[float], c: Sequence[float]):
+    """Stall-opt (eqs. (5)-(6)): caps at the zero-stall rates."""
+    return stall_opt(B, s, [zero_stall_rate(a, b) for a, b in zip(s, c)])
+
+
+def alloc_cal_stall_opt(B: float, s: Sequence[float], c: Sequence[float], delta: float):
+    """Calibrated Stall-opt (eq. (7)): the same program with the targets
+    r*_i + delta as caps."""
+    return stall_opt(B, s, [zero_stall_rate(a, b) + delta for a, b in zip(s, c)])
+
+
+def total_stall(s: Sequence[float], c: Sequence[float], r: Sequence[float]) -> float:
+    """Sum of the per-layer stalls of eq. (4)."""
+    return sum(per_layer_stall(a, x, b) for a, b, x in zip(s, c, r))

@@ -149,9 +149,35 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
  * computes.  The producer stands in for the storage server's layerwise GET:
  * it assembles each layer payload from the chunk objects in prefix order
  * (appendix pseudocode "layerwise GET"), paced to a byte rate, and signals
- * layer-ready.  With several requests, layers are delivered layer-major,
- * request-minor (round-robin), all requests sharing one rate.
+ * layer-ready.  With several requests sharing one rate (OC_ALLOC_FIFO),
+ * layers are delivered layer-major, request-minor (round-robin); with an
+ * allocation policy each request gets its own rate for the run (one
+ * scheduling epoch) and the producer dispatches their payload pieces by
+ * weighted deficit round robin (Section 3.6 and its appendix pseudocode).
  * ------------------------------------------------------------------------- */
+
+/* Per-request bandwidth under a shared cap (Section 3.6; the baselines of the
+ * multi-tenant evaluation).  Request i moves s_i bytes per layer and has a
+ * compute window of c_i seconds per layer; r*_i = s_i / c_i is its zero-stall
+ * rate (eq. (4)). */
+typedef enum {
+    OC_ALLOC_FIFO = 0,          /* no per-request rates: one shared stream            */
+    OC_ALLOC_EQUAL = 1,         /* B / n each                                           */
+    OC_ALLOC_KV_PROP = 2,       /* proportional to s_i                                  */
+    OC_ALLOC_BW_PROP = 3,       /* proportional to r*_i                                 */
+    OC_ALLOC_STALL_OPT = 4,     /* eqs. (5)-(6): min sum s_i/r_i, sum r_i = B, r_i <= r*_i */
+    OC_ALLOC_CAL_STALL_OPT = 5  /* eq. (7): the same with r_i <= r*_i + margin          */
+} oc_alloc_policy;
+
+/* Host-only: rates_out[i] (bytes/s) for n requests under budget B (bytes/s).
+ * layer_bytes[i] = s_i > 0; layer_compute_s[i] = c_i > 0 (needed by BW_PROP,
+ * STALL_OPT, CAL_STALL_OPT; may be NULL otherwise); margin = delta >= 0 (used by
+ * CAL_STALL_OPT).  Stall-opt policies leave budget unassigned when every
+ * request's cap fits.  Returns OC_OK, or OC_EINVAL for bad input or
+ * OC_ALLOC_FIFO.  Arrays are caller-owned; nothing is retained. */
+int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes,
+                          const double *layer_compute_s, double budget_bytes_per_s,
+                          double margin_bytes_per_s, double *rates_out);
 
 typedef enum {
     OC_MODE_HBM_RESIDENT = 0,  /* pool already holds the prefix: attention only          */
@@ -174,6 +200,8 @@ typedef struct {
     int32_t timeout_ms;        /* wait limit per layer (default 60000 when 0)              */
     int32_t fault;             /* oc_fault, test injection                                 */
     int32_t fault_layer;       /* layer at which the fault triggers                        */
+    int32_t alloc_policy;      /* oc_alloc_policy (PRODUCER mode); budget = rate_bytes_per_s */
+    double margin_bytes_per_s; /* delta of OC_ALLOC_CAL_STALL_OPT                          */
 } oc_pipeline_opts;
 
 /* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */
@@ -189,6 +217,8 @@ typedef struct {
     const void *k_new;                    /* device [L][T_s][n_kv][d]                      */
     const void *v_new;                    /* device [L][T_s][n_kv][d]                      */
     void *out;                            /* device [L][T_s][n_q][d]                       */
+    double layer_compute_s;               /* c_i for the allocation policies (seconds per
+                                             layer); ignored under OC_ALLOC_FIFO            */
 } oc_request;
 
 /* Per-request timings (milliseconds from the start of the run, all on one
@@ -199,6 +229,7 @@ typedef struct {
     double *landed_ms;         /* device: payload in HBM (layer-ready)             */
     double *ingested_ms;       /* device: ingest kernel finished                   */
     double *done_ms;           /* device: attention finished                       */
+    double rate_bytes_per_s;   /* the request's allocated rate (0 under FIFO)      */
 } oc_request_stats;
 
 /* Create a context on `device` for one pool.  Allocates the streams, events,

@@ -7,5 +7,5 @@ from ._lib import (  # noqa: F401
     EXPORTS, LIB_PATH, OC_FAULT_ABORT, OC_FAULT_NONE, OC_FAULT_STALL, OC_MODE_DEVICE_STAGED, OC_MODE_HBM_RESIDENT,
     OC_MODE_PRODUCER, Layout, OcError, Request, lib, oc_abi_version, oc_attention_workspace_bytes,
     oc_block_table_check, oc_context_create, oc_context_destroy, oc_kv_layer_gather, oc_kv_layer_ingest,
-    oc_pipeline_last_ms, oc_pipeline_run, oc_suffix_prefill_layer,
+    oc_pipeline_last_ms, oc_pipeline_run, oc_suffix_prefill_layer, oc_bandwidth_allocate, ALLOC_POLICIES,
 )

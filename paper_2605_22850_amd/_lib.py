@@ -21,11 +21,12 @@ OC_OK, OC_EINVAL, OC_ESHAPE, OC_EALIGN, OC_ERANGE, OC_EHIP, OC_ETIMEOUT, OC_ENOM
     0, -1, -2, -3, -4, -5, -6, -7, -8
 OC_MODE_HBM_RESIDENT, OC_MODE_DEVICE_STAGED, OC_MODE_PRODUCER = 0, 1, 2
 OC_FAULT_NONE, OC_FAULT_STALL, OC_FAULT_ABORT = 0, 1, 2
+ALLOC_POLICIES = {"fifo": 0, "equal": 1, "kv_prop": 2, "bw_prop": 3, "stall_opt": 4, "cal_stall_opt": 5}
 
 EXPORTS = [
     "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather",
     "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
-    "oc_pipeline_last_ms", "oc_context_destroy",
+    "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate",
 ]
 
 
@@ -56,18 +57,20 @@ class c_staging(ctypes.Structure):
 class c_pipeline_opts(ctypes.Structure):
     _fields_ = [("mode", c_int32), ("rate_bytes_per_s", c_double), ("piece_bytes", c_int64),
                 ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
-                ("fault", c_int32), ("fault_layer", c_int32)]
+                ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
+                ("margin_bytes_per_s", c_double)]
 
 
 class c_request(ctypes.Structure):
     _fields_ = [("prefix_tokens", c_int64), ("suffix_tokens", c_int64), ("block_table", POINTER(c_block_table)),
                 ("chunk_objects", POINTER(c_void_p)), ("device_payload", c_void_p), ("q", c_void_p),
-                ("k_new", c_void_p), ("v_new", c_void_p), ("out", c_void_p)]
+                ("k_new", c_void_p), ("v_new", c_void_p), ("out", c_void_p), ("layer_compute_s", c_double)]
 
 
 class c_request_stats(ctypes.Structure):
     _fields_ = [("ttft_ms", c_double), ("produced_ms", POINTER(c_double)), ("landed_ms", POINTER(c_double)),
-                ("ingested_ms", POINTER(c_double)), ("done_ms", POINTER(c_double))]
+                ("ingested_ms", POINTER(c_double)), ("done_ms", POINTER(c_double)),
+                ("rate_bytes_per_s", c_double)]
 
 
 _lib = None
@@ -101,7 +104,10 @@ def lib():
             L.oc_pipeline_last_ms.restype = c_double
             L.oc_context_destroy.argtypes = [c_void_p]
             L.oc_context_destroy.restype = None
-        for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather", "oc_suffix_prefill_layer"):
+        L.oc_bandwidth_allocate.argtypes = [c_int32, c_int32, POINTER(c_double), POINTER(c_double), c_double, c_double,
+                                            POINTER(c_double)]
+        for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather", "oc_suffix_prefill_layer",
+                     "oc_bandwidth_allocate"):
             getattr(L, name).restype = c_int
         _lib = L
     return _lib
@@ -219,14 +225,16 @@ class Request:
     out: object                        # [L][Ts][nq][d] bf16
     chunk_objects: object = None       # host numpy uint16 [N][L * S/2], one chunk object per row
     device_payload: object = None      # device [L][Tp * b] bytes, layer payloads back to back
+    layer_compute_s: float = 0.0       # per-layer compute window for the allocation policies
 
 
 def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, max_suffix_tokens: int,
                       rate_bytes_per_s: float = 0.0, piece_bytes: int = 0, slots: int = 0,
                       producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
-                      fault_layer: int = 0, device: int = 0):
+                      fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0):
+    pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
-                           fault_layer)
+                           fault_layer, pol, margin_bytes_per_s)
     kp = make_pool(pool, layout)
     ctx = c_void_p()
     _check(lib().oc_context_create(device, ctypes.byref(kp), ctypes.byref(opts), max_prefix_tokens,
@@ -261,14 +269,28 @@ def oc_pipeline_run(ctx, requests: Sequence[Request], num_layers: int):
             objs = (c_void_p * co.shape[0])(*[co.ctypes.data + j * row for j in range(co.shape[0])])
             keep.append(objs)
         creqs[i] = c_request(r.prefix_tokens, r.suffix_tokens, ctypes.pointer(bt), objs,
-                             _ptr(r.device_payload), _ptr(r.q), _ptr(r.k_new), _ptr(r.v_new), _ptr(r.out))
+                             _ptr(r.device_payload), _ptr(r.q), _ptr(r.k_new), _ptr(r.v_new), _ptr(r.out),
+                             r.layer_compute_s)
         per = [(c_double * num_layers)() for _ in range(4)]
         arrays.append(per)
-        stats[i] = c_request_stats(0.0, *per)
+        stats[i] = c_request_stats(0.0, *per, 0.0)
     _check(lib().oc_pipeline_run(ctx, creqs, n, stats))
     out = []
     for i in range(n):
         p = arrays[i]
         out.append({"ttft_ms": stats[i].ttft_ms, "produced_ms": list(p[0]), "landed_ms": list(p[1]),
-                    "ingested_ms": list(p[2]), "done_ms": list(p[3])})
+                    "ingested_ms": list(p[2]), "done_ms": list(p[3]), "rate_bytes_per_s": stats[i].rate_bytes_per_s})
     return out
+
+
+def oc_bandwidth_allocate(policy, layer_bytes, layer_compute_s, budget_bytes_per_s: float,
+                          margin_bytes_per_s: float = 0.0):
+    """Per-request rates (bytes/s) under a shared budget; `policy` is a name
+    of ALLOC_POLICIES or its number."""
+    pol = ALLOC_POLICIES.get(policy, -1) if isinstance(policy, str) else int(policy)
+    n = len(layer_bytes)
+    s = (c_double * n)(*layer_bytes)
+    c = (c_double * n)(*layer_compute_s) if layer_compute_s is not None else None
+    out = (c_double * n)()
+    _check(lib().oc_bandwidth_allocate(pol, n, s, c, budget_bytes_per_s, margin_bytes_per_s, out))
+    return list(out)

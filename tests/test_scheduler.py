@@ -1,6 +1,8 @@
 """Bandwidth allocation under a shared cap (Section 3.6, eqs. (4)-(7)): the
 oracle's allocators against the paper's per-request allocation table, brute
-force and the optimality conditions."""
+force and the optimality conditions; then the library's allocator against
+the oracle (host code, no GPU)."""
+import ctypes
 import math
 import random
 from itertools import groupby
@@ -111,3 +113,49 @@ def test_zero_stall_rates_fit_means_no_stall():
     r = model.alloc_stall_opt(100.0, s, c)
     assert r == [10.0, 5.0] and model.total_stall(s, c, r) == 0.0
     assert model.per_layer_stall(10.0, 5.0, 1.0) == pytest.approx(1.0)
+
+
+# ---------------------------------------------------------------------------
+# the library's allocator (host code) against the oracle
+# ---------------------------------------------------------------------------
+
+POLICIES = ["equal", "kv_prop", "bw_prop", "stall_opt", "cal_stall_opt"]
+
+
+def lib_alloc(policy, B, s, c, delta):
+    import paper_2605_22850_amd as oc
+    return np.array(oc.oc_bandwidth_allocate(policy, s, c, B, delta))
+
+
+def test_library_reproduces_the_paper_allocation_table():
+    for name, B, s, c, want in paper_workloads():
+        got = np.array([lib_alloc(p, B, s, c, 5 * GBPS) for p in POLICIES]).T / GBPS
+        np.testing.assert_allclose(got, want, atol=0.011, err_msg=f"workload {name}")
+
+
+def test_library_matches_oracle_on_random_sets():
+    rng = random.Random(17)
+    for _ in range(300):
+        n = rng.randint(1, 16)
+        s = [rng.uniform(1e5, 5e8) for _ in range(n)]
+        c = [rng.uniform(1e-4, 0.3) for _ in range(n)]
+        rstar = [a / b for a, b in zip(s, c)]
+        B = rng.uniform(0.05, 1.5) * sum(rstar)
+        delta = rng.choice([0.0, 5 * GBPS, 0.1 * B])
+        want = oracle_all(B, s, c, delta)
+        got = np.array([lib_alloc(p, B, s, c, delta) for p in POLICIES]).T
+        np.testing.assert_allclose(got, want, rtol=1e-9, atol=1e-6 * B)
+
+
+def test_library_allocator_rejects_bad_input():
+    import paper_2605_22850_amd as oc
+    from paper_2605_22850_amd import _lib as L
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_bandwidth_allocate("stall_opt", [1.0, 2.0], [0.0, 1.0], 1.0, 0.0)
+    assert e.value.status == L.OC_EINVAL
+    with pytest.raises(oc.OcError):
+        oc.oc_bandwidth_allocate("stall_opt", [1.0], [1.0], -1.0, 0.0)
+    with pytest.raises(oc.OcError):
+        oc.oc_bandwidth_allocate("no_such_policy", [1.0], [1.0], 1.0, 0.0)
+    out = (ctypes.c_double * 1)()
+    assert oc.lib().oc_bandwidth_allocate(0, 0, None, None, 1.0, 0.0, out) == L.OC_EINVAL

@@ -16,6 +16,8 @@
 #include <chrono>
 #include <condition_variable>
 #include <cstring>
+#include <deque>
+#include <queue>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -56,6 +58,7 @@ struct RunShared {
     bool abort = false;           // driver -> producer: stop now
     int producer_status = OC_OK;  // producer -> driver
     std::string producer_msg;
+    std::deque<int64_t> reported; // rate producer -> driver: items complete in a pinned slot
 };
 
 struct Item {
@@ -72,6 +75,11 @@ static int fill_defaults(oc_pipeline_opts &o) {
     if (o.producer_threads > 64) return fail(OC_EINVAL, "producer_threads must be <= 64");
     if (o.mode < OC_MODE_HBM_RESIDENT || o.mode > OC_MODE_PRODUCER) return fail(OC_EINVAL, "unknown mode");
     if (o.rate_bytes_per_s < 0) return fail(OC_EINVAL, "negative rate");
+    if (o.alloc_policy < OC_ALLOC_FIFO || o.alloc_policy > OC_ALLOC_CAL_STALL_OPT)
+        return fail(OC_EINVAL, "unknown allocation policy");
+    if (o.alloc_policy != OC_ALLOC_FIFO && !(o.rate_bytes_per_s > 0))
+        return fail(OC_EINVAL, "an allocation policy needs a positive budget (rate_bytes_per_s)");
+    if (o.margin_bytes_per_s < 0) return fail(OC_EINVAL, "negative margin");
     return OC_OK;
 }
 
@@ -236,6 +244,235 @@ struct Producer {
     }
 };
 
+// ---- per-request rates (allocation policies) --------------------------------
+// Each request is paced by its own clock at its allocated rate for the whole
+// run -- one scheduling epoch: a request that finishes early does not pass
+// its rate on.  The dispatcher hands out payload pieces by weighted deficit
+// round robin (a quantum proportional to the rate per round) to the copy
+// threads, which copy each piece once its release time has come.  A request
+// starts its next layer only when a staging slot is free; its layers are
+// reported to the driver in layer order, and the driver lands whichever
+// layer is reported first, so a slow request does not hold up a fast one.
+struct RateProducer {
+    Context *c;
+    RunShared *sh;
+    const oc_request *reqs;
+    int32_t n_reqs, L;
+    int64_t S;
+    Clock::time_point t0;
+    std::vector<double> rate;                // bytes/s per request
+    std::vector<double> *produced_ms;        // per item k = layer * n_reqs + request
+    std::vector<hipEvent_t> *landed;         // per item
+
+    struct Piece {
+        double release_s;
+        int64_t item, j0, j1;
+        int slot;
+    };
+    struct Later {
+        bool operator()(const Piece &a, const Piece &b) const { return a.release_s > b.release_s; }
+    };
+    // lock order: wmu may be held while taking sh->mu, never the reverse
+    std::mutex wmu;
+    std::condition_variable wcv;
+    std::priority_queue<Piece, std::vector<Piece>, Later> heap;
+    bool stop = false;
+    std::vector<int64_t> pieces_left;        // per item
+    std::vector<char> complete;              // per item
+    std::vector<int32_t> next_report;        // per request: the layer to report next
+    std::vector<int> slot_of;                // per item; written before the item is reported
+
+    struct FreeSlot {
+        int slot;
+        int64_t after_item;                  // its DMA must have landed before reuse (-1: none)
+    };
+    std::deque<FreeSlot> free_slots;         // guarded by sh->mu
+
+    double now_s() const { return std::chrono::duration<double>(Clock::now() - t0).count(); }
+    int64_t item_of(int32_t layer, int32_t r) const { return (int64_t)layer * n_reqs + r; }
+
+    bool aborted() {
+        std::lock_guard<std::mutex> g(sh->mu);
+        return sh->abort;
+    }
+    void set_error(int st, const char *msg) {
+        std::lock_guard<std::mutex> g(sh->mu);
+        if (sh->producer_status == OC_OK) {
+            sh->producer_status = st;
+            sh->producer_msg = msg;
+        }
+        sh->cv.notify_all();
+    }
+
+    // called with wmu held: hand every finished layer of request r, in layer order, to the driver
+    void report_ready(int32_t r) {
+        std::lock_guard<std::mutex> g(sh->mu);
+        while (next_report[r] < L && complete[item_of(next_report[r], r)]) {
+            const int64_t k = item_of(next_report[r], r);
+            (*produced_ms)[k] = std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
+            sh->reported.push_back(k);
+            ++next_report[r];
+        }
+        sh->cv.notify_all();
+    }
+
+    // a free slot whose previous DMA has landed, or -1
+    int acquire_slot() {
+        std::lock_guard<std::mutex> g(sh->mu);
+        for (auto it = free_slots.begin(); it != free_slots.end(); ++it) {
+            if (it->after_item >= 0 && hipEventQuery((*landed)[it->after_item]) != hipSuccess) continue;
+            const int s = it->slot;
+            free_slots.erase(it);
+            return s;
+        }
+        return -1;
+    }
+
+    void worker() {
+        for (;;) {
+            Piece pc;
+            {
+                std::unique_lock<std::mutex> lk(wmu);
+                for (;;) {
+                    if (stop) return;
+                    if (!heap.empty()) {
+                        const double wait = heap.top().release_s - now_s();
+                        if (wait <= 0.0) {
+                            pc = heap.top();
+                            heap.pop();
+                            break;
+                        }
+                        wcv.wait_for(lk, std::chrono::duration<double>(std::min(wait, 0.001)));
+                    } else {
+                        wcv.wait(lk);
+                    }
+                }
+            }
+            const int32_t layer = (int32_t)(pc.item / n_reqs), r = (int32_t)(pc.item % n_reqs);
+            unsigned char *dst = static_cast<unsigned char *>(c->slots[pc.slot].pinned);
+            for (int64_t j = pc.j0; j < pc.j1; ++j) {
+                const unsigned char *obj = static_cast<const unsigned char *>(reqs[r].chunk_objects[j]);
+                std::memcpy(dst + j * S, obj + (int64_t)layer * S, (size_t)S);
+            }
+            std::lock_guard<std::mutex> g(wmu);
+            if (--pieces_left[pc.item] == 0) {
+                complete[pc.item] = 1;
+                report_ready(r);
+            }
+            wcv.notify_all();
+        }
+    }
+
+    void run() {
+        const int64_t n_items = (int64_t)n_reqs * L;
+        const int64_t cpp = std::max<int64_t>(1, c->opts.piece_bytes / S);     // chunks per piece
+        pieces_left.assign(n_items, 0);
+        complete.assign(n_items, 0);
+        next_report.assign(n_reqs, 0);
+        slot_of.assign(n_items, -1);
+        {
+            std::lock_guard<std::mutex> g(sh->mu);
+            for (int s = 0; s < (int)c->slots.size(); ++s) free_slots.push_back({s, -1});
+        }
+        std::vector<int64_t> N(n_reqs), npieces(n_reqs), piece(n_reqs, 0);
+        std::vector<int32_t> layer(n_reqs, 0);
+        std::vector<double> cum(n_reqs, 0.0), deficit(n_reqs, 0.0), quantum(n_reqs, 0.0);
+        double max_rate = 0.0;
+        for (int32_t r = 0; r < n_reqs; ++r) max_rate = std::max(max_rate, rate[r]);
+        {
+            std::lock_guard<std::mutex> g(wmu);
+            for (int32_t r = 0; r < n_reqs; ++r) {
+                N[r] = reqs[r].prefix_tokens / c->pool.layout.chunk_tokens;
+                npieces[r] = (N[r] + cpp - 1) / cpp;
+                quantum[r] = max_rate > 0 ? (double)(cpp * S) * rate[r] / max_rate : 0.0;
+                for (int32_t l = 0; l < L; ++l) pieces_left[item_of(l, r)] = npieces[r];
+                if (N[r] == 0) {            // nothing to deliver: every layer is ready now
+                    for (int32_t l = 0; l < L; ++l) complete[item_of(l, r)] = 1;
+                    layer[r] = L;
+                    report_ready(r);
+                }
+            }
+        }
+        const int nw = c->opts.producer_threads;
+        std::vector<std::thread> pool;
+        for (int i = 0; i < nw; ++i) pool.emplace_back([this] { worker(); });
+        const double lookahead_s = 0.004;   // hand out pieces due within this window
+        bool failed = false;
+        for (;;) {
+            if (aborted()) {
+                failed = true;
+                break;
+            }
+            bool all_done = true, progress = false;
+            for (int32_t r = 0; r < n_reqs; ++r) {
+                if (layer[r] >= L) continue;
+                all_done = false;
+                if (c->opts.fault != OC_FAULT_NONE && layer[r] == c->opts.fault_layer && piece[r] == 0) {
+                    if (c->opts.fault == OC_FAULT_ABORT) {
+                        set_error(OC_EABORT, "producer aborted (injected fault)");
+                    } else {      // injected stall: deliver nothing more until the driver gives up
+                        std::unique_lock<std::mutex> lk(sh->mu);
+                        sh->cv.wait(lk, [&] { return sh->abort; });
+                    }
+                    failed = true;
+                    break;
+                }
+                deficit[r] = std::min(deficit[r] + quantum[r], 2.0 * (double)(cpp * S));
+                while (layer[r] < L) {
+                    const int64_t j0 = piece[r] * cpp, j1 = std::min(N[r], j0 + cpp);
+                    const double bytes = (double)(j1 - j0) * S;
+                    if (deficit[r] < bytes) break;
+                    const double release = (cum[r] + bytes) / rate[r];
+                    if (release > now_s() + lookahead_s) break;
+                    const int64_t k = item_of(layer[r], r);
+                    if (piece[r] == 0) {
+                        const int s = acquire_slot();
+                        if (s < 0) break;
+                        slot_of[k] = s;
+                    }
+                    {
+                        std::lock_guard<std::mutex> g(wmu);
+                        heap.push({release, k, j0, j1, slot_of[k]});
+                    }
+                    wcv.notify_all();
+                    cum[r] += bytes;
+                    deficit[r] -= bytes;
+                    progress = true;
+                    if (++piece[r] == npieces[r]) {
+                        ++layer[r];
+                        piece[r] = 0;
+                    }
+                }
+            }
+            if (failed || all_done) break;
+            if (!progress) {     // wait for a slot to come back or the next release window
+                std::unique_lock<std::mutex> lk(sh->mu);
+                sh->cv.wait_for(lk, std::chrono::microseconds(250));
+            }
+        }
+        // let the copies already handed out finish, unless the run is stopped
+        if (!failed) {
+            for (;;) {
+                std::unique_lock<std::mutex> lk(wmu);
+                const bool finished = wcv.wait_for(lk, std::chrono::milliseconds(1), [&] {
+                    if (!heap.empty()) return false;
+                    for (int64_t k = 0; k < n_items; ++k)
+                        if (pieces_left[k] > 0) return false;
+                    return true;
+                });
+                lk.unlock();
+                if (finished || aborted()) break;
+            }
+        }
+        {
+            std::lock_guard<std::mutex> g(wmu);
+            stop = true;
+        }
+        wcv.notify_all();
+        for (auto &t : pool) t.join();
+    }
+};
+
 static int validate_requests(Context *c, const oc_request *reqs, int32_t n) {
     const oc_layout &l = c->pool.layout;
     const int mode = c->opts.mode;
@@ -325,15 +562,49 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     OC_HIP(hipStreamWaitEvent(c->copy, c->caller_done, 0));
     OC_HIP(hipStreamWaitEvent(c->compute, c->caller_done, 0));
 
+    // per-request rates under the shared budget (allocation policies)
+    const bool by_rate = mode == OC_MODE_PRODUCER && c->opts.alloc_policy != OC_ALLOC_FIFO;
+    std::vector<double> req_rate(n_reqs, 0.0);
+    if (by_rate) {
+        std::vector<double> s_i, c_i;
+        std::vector<int32_t> who;
+        for (int32_t r = 0; r < n_reqs; ++r)
+            if (reqs[r].prefix_tokens > 0) {
+                who.push_back(r);
+                s_i.push_back((double)reqs[r].prefix_tokens * (double)b_tok);
+                c_i.push_back(reqs[r].layer_compute_s);
+            }
+        if (!who.empty()) {
+            std::vector<double> out(who.size());
+            const int rc = oc_bandwidth_allocate(c->opts.alloc_policy, (int32_t)who.size(), s_i.data(), c_i.data(),
+                                                 c->opts.rate_bytes_per_s, c->opts.margin_bytes_per_s, out.data());
+            if (rc) return rc;
+            for (size_t i = 0; i < who.size(); ++i) req_rate[who[i]] = out[i];
+        }
+    }
+
     RunShared sh;
     Producer prod{};
+    RateProducer rprod{};
     std::thread producer_thread;
     const hipStream_t first = mode == OC_MODE_HBM_RESIDENT ? c->compute : c->copy;
     OC_HIP(hipEventRecord(ev_start, first));
     if (mode != OC_MODE_HBM_RESIDENT) OC_HIP(hipStreamWaitEvent(c->compute, ev_start, 0));
     const Clock::time_point t0 = Clock::now();
 
-    if (mode == OC_MODE_PRODUCER) {
+    if (by_rate) {
+        rprod.c = c;
+        rprod.sh = &sh;
+        rprod.reqs = reqs;
+        rprod.n_reqs = n_reqs;
+        rprod.L = L;
+        rprod.S = S;
+        rprod.t0 = t0;
+        rprod.rate = req_rate;
+        rprod.produced_ms = &produced;
+        rprod.landed = &landed;
+        producer_thread = std::thread([&rprod] { rprod.run(); });
+    } else if (mode == OC_MODE_PRODUCER) {
         prod.c = c;
         prod.sh = &sh;
         prod.reqs = reqs;
@@ -349,13 +620,56 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
 
     int status = OC_OK;
     std::string msg;
-    for (int64_t k = 0; k < n_items && status == OC_OK; ++k) {
+    for (int64_t step = 0; step < n_items && status == OC_OK; ++step) {
+        int64_t k = step;
+        if (by_rate) {     // the next layer any request has ready, in the order they became ready
+            std::unique_lock<std::mutex> lk(sh.mu);
+            const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
+            const bool ok = sh.cv.wait_until(lk, deadline, [&] { return !sh.reported.empty() || sh.producer_status != OC_OK; });
+            if (sh.producer_status != OC_OK) {
+                status = sh.producer_status;
+                msg = sh.producer_msg;
+                break;
+            }
+            if (!ok) {
+                status = OC_ETIMEOUT;
+                msg = "no layer arrived within " + std::to_string(c->opts.timeout_ms) + " ms";
+                break;
+            }
+            k = sh.reported.front();
+            sh.reported.pop_front();
+        }
         const Item it = items[k];
         const oc_request &r = reqs[it.req];
         const int64_t layer_bytes = r.prefix_tokens * b_tok;
         const int64_t N = r.prefix_tokens / l.chunk_tokens;
         const void *payload = nullptr;
-        if (mode == OC_MODE_PRODUCER) {
+        if (by_rate) {
+            if (layer_bytes > 0) {
+                const int slot = rprod.slot_of[k];
+                Slot &s = c->slots[slot];
+                hipError_t e = hipMemcpyAsync(s.device, s.pinned, (size_t)layer_bytes, hipMemcpyHostToDevice, c->copy);
+                if (e == hipSuccess) e = hipEventRecord(landed[k], c->copy);
+                {
+                    std::lock_guard<std::mutex> g(sh.mu);
+                    rprod.free_slots.push_back({slot, k});   // reusable once this DMA has landed
+                }
+                sh.cv.notify_all();
+                if (e != hipSuccess) {
+                    status = hip_fail(e, "landing a layer payload");
+                    msg = oc_last_error();
+                    break;
+                }
+                payload = s.device;
+            } else {
+                hipError_t e = hipEventRecord(landed[k], c->copy);
+                if (e != hipSuccess) {
+                    status = hip_fail(e, "hipEventRecord");
+                    msg = oc_last_error();
+                    break;
+                }
+            }
+        } else if (mode == OC_MODE_PRODUCER) {
             std::unique_lock<std::mutex> lk(sh.mu);
             const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
             const bool ok = sh.cv.wait_until(lk, deadline, [&] { return sh.ready > k || sh.producer_status != OC_OK; });
@@ -414,7 +728,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 a.n_kv = l.num_kv_heads;
                 a.d = l.head_dim;
                 a.Ps = l.page_size;
-                e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy, k > 0);
+                e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy, step > 0);
             }
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
             if (e == hipSuccess) e = hipStreamWaitEvent(c->compute, ingested[k], 0);
@@ -488,6 +802,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             if (st.landed_ms) st.landed_ms[it.layer] = mode == OC_MODE_HBM_RESIDENT ? 0.0 : ev_ms(ev_start, landed[k]);
             if (st.ingested_ms) st.ingested_ms[it.layer] = ev_ms(ev_start, ingested[k]);
             if (st.done_ms) st.done_ms[it.layer] = t_done;
+            st.rate_bytes_per_s = req_rate[it.req];
         }
     }
     c->last_ms = last;

@@ -124,6 +124,76 @@ def test_batch_of_requests_sharing_pool_and_rate():
     assert last >= 0.95 * total / rate * 1e3
 
 
+def _rate_set():
+    # three requests, per-layer bytes 256 KiB / 512 KiB / 1 MiB, distinct compute windows
+    rs = RequestSet(4, 4, 2, 64, [512, 1024, 2048], [16, 16, 16], 512, seed=7).upload(with_payload=True)
+    for req, c in zip(rs.reqs, (0.001, 0.020, 0.005)):
+        req.layer_compute_s = c
+    return rs
+
+
+def test_allocation_policies_deliver_at_their_rates():
+    import paper_2605_22850_amd as oc
+    print("[pipeline] allocation policies", flush=True)
+    rs = _rate_set()
+    want_pool = rs.expected_pool()
+    fill = np.int16(np.uint16(SENTINEL).view(np.int16))
+    rs.d_pool.fill_(fill)
+    _run(rs, oc.OC_MODE_PRODUCER)                       # one shared stream (FIFO)
+    ref = _outs(rs)
+    for l in range(rs.L):
+        for r in range(3):
+            assert_attention_close(ref[r][l], rs.expected_out(r, l), f"request {r} layer {l}")
+    B = 200e6
+    s = [tp * 2 * rs.nkv * rs.d * 2 for tp in rs.prefix]
+    c = [req.layer_compute_s for req in rs.reqs]
+    for policy in ("equal", "kv_prop", "bw_prop", "stall_opt", "cal_stall_opt"):
+        rs.d_pool.fill_(fill)
+        for req in rs.reqs:
+            req.out.zero_()
+        stats = _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=B, alloc_policy=policy,
+                     margin_bytes_per_s=20e6, slots=6)
+        assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want_pool), policy
+        assert all(np.array_equal(a, b) for a, b in zip(_outs(rs), ref)), policy
+        want = oc.oc_bandwidth_allocate(policy, s, c, B, 20e6)
+        for r, st in enumerate(stats):
+            assert st["rate_bytes_per_s"] == pytest.approx(want[r], rel=1e-12)
+            # request r's last layer cannot be complete before its clock allows,
+            # and its own pacing, not the other requests, decides when it is
+            t_pace = rs.L * s[r] / want[r] * 1e3
+            got = st["produced_ms"][rs.L - 1]
+            print(f"  {policy:14s} request {r}: rate {want[r] / 1e6:7.2f} MB/s, last layer produced at "
+                  f"{got:7.2f} ms (pacing {t_pace:7.2f} ms)", flush=True)
+            assert t_pace * 0.99 <= got <= t_pace * 1.25 + 5.0, (policy, r)
+
+
+def test_slow_request_does_not_hold_up_a_fast_one():
+    # under Equal with a tiny and a large request, the tiny one finishes first
+    import paper_2605_22850_amd as oc
+    print("[pipeline] per-request progress", flush=True)
+    rs = RequestSet(4, 4, 2, 64, [4096, 256], [8, 8], 512, seed=8).upload(with_payload=True)
+    stats = _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=100e6, alloc_policy="equal", slots=2)
+    assert stats[1]["ttft_ms"] < 0.25 * stats[0]["ttft_ms"]
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
+
+
+def test_allocation_policy_validation():
+    import paper_2605_22850_amd as oc
+    print("[pipeline] policy validation", flush=True)
+    rs = _rate_set()
+    with pytest.raises(oc.OcError) as e:
+        rs.context(oc.OC_MODE_PRODUCER, alloc_policy="stall_opt")           # no budget
+    assert "budget" in str(e.value)
+    with pytest.raises(oc.OcError):
+        rs.context(oc.OC_MODE_PRODUCER, rate_bytes_per_s=1e8, alloc_policy=9)
+    rs.reqs[1].layer_compute_s = 0.0
+    with pytest.raises(oc.OcError) as e:
+        _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=1e8, alloc_policy="stall_opt")
+    assert "compute" in str(e.value)
+    # policies that need no compute windows run without them
+    _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=1e9, alloc_policy="kv_prop")
+
+
 def test_pacing_and_timestamps():
     import paper_2605_22850_amd as oc
     print("[pipeline] pacing", flush=True)

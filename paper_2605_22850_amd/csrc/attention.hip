@@ -47,6 +47,10 @@ constexpr int TILE_ROWS = WAVES * WAVE_ROWS;
 constexpr int THREADS = WAVES * 64;
 constexpr int TARGET_WGS = 256;   // one workgroup per CU
 constexpr float RESCALE_SLACK = 8.0f;   // log2 units the running max may lag
+#ifndef OC_LOOKAHEAD
+#define OC_LOOKAHEAD 4
+#endif
+constexpr int LOOKAHEAD = OC_LOOKAHEAD;   // MFMAs an operand read runs ahead of its use
 
 struct KParams {
     const uint16_t *q;
@@ -96,13 +100,27 @@ __device__ inline int v_swz(int r) {
 
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-typedef __attribute__((address_space(1))) const void *gbl_ptr_t;
 
-// one 16-byte global -> LDS copy per lane; the wavefront's 64 lanes fill 1 KiB
-// of LDS starting at `lds_chunk`, lane i at byte 16*i
-__device__ inline void dma16(const uint16_t *src, uint16_t *lds_chunk) {
-    __builtin_amdgcn_global_load_lds((gbl_ptr_t)src, (lds_ptr_t)lds_chunk, 16, 0, 0);
+// one 16-byte global -> LDS copy per lane from `base` (wave-uniform) plus the
+// lane's byte offset; the wavefront's 64 lanes fill 1 KiB of LDS starting at
+// `lds_chunk`, lane i at byte 16*i.  Issued as inline
+// assembly on purpose: the compiler treats every outstanding global->LDS copy
+// as a possible writer of any LDS address, and would make each operand read
+// of the current tile wait (vmcnt(0)) for the copies of the blocks still in
+// flight, which serialises the prefetch.  The kernel orders these copies
+// itself: wait_vmcnt before the per-block barrier, which is the only point
+// where a tile becomes readable, and a buffer is refilled only after every
+// wavefront has passed the barrier that follows its last read.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"   // m0 is written here and read by nothing else in these kernels
+__device__ inline void dma16(const void *base, uint32_t lane_off, uint16_t *lds_chunk) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)(lds_ptr_t)lds_chunk;   // LDS byte address, wave-uniform
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(lane_off), "s"(base), "s"(m0)
+                 : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 template <int N>
 __device__ inline void wait_vmcnt() {
@@ -110,6 +128,118 @@ __device__ inline void wait_vmcnt() {
     if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+}
+
+// Per-wavefront running state of the online softmax for its 32 query rows.
+template <int D>
+struct WaveState {
+    f32x16 o[D / 32];    // O^T: 32 dims x 32 rows per tile, fp32
+    f32x16 s[2];         // scores of the current block, one 32-key half each
+    bf16x8 p[2][2];      // P of the last softmaxed block as the PV operand: [half][8-key group]
+    float m, l;          // running maximum (log2 units) and sum of this lane's row
+};
+
+// Matrix phase of a wavefront: O^T += V^T P for the previous block (PV:
+// 16 MFMAs at d = 128, each V^T fragment from two transposing LDS reads),
+// then S^T = K Q^T for the current block (S: 16 MFMAs, K fragments from the
+// swizzled tile, the two 32-key halves alternating so that consecutive MFMAs
+// are independent).  Written as one flat sequence whose operand reads run
+// LOOKAHEAD MFMAs ahead (with PV, the first LOOKAHEAD come preloaded, see
+// prefetch_vt); a scheduling fence after every MFMA keeps that order (left
+// alone, the compiler hoists every read to the top and runs out of VGPRs).
+// V^T fragment n of a PV pass (n = 8-key group * D/32 + dim tile)
+template <int D>
+__device__ __forceinline__ bf16x8 load_vt(const uint16_t *V, const int (&voff)[D / 32], int n) {
+    constexpr int NET = D / 32;
+    const int et = n % NET, g4 = n / NET;     // g4 = 2*half + key group
+    const uint16_t *vp = V + voff[et] + ((g4 >> 1) * 32 + (g4 & 1) * 16) * D;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)vp);
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vp + 4 * D));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// The first LOOKAHEAD V^T fragments of a PV pass, read ahead of the barrier
+// that opens the matrix phase (the V tile of the previous block is already
+// readable there), so the phase starts without waiting on LDS.
+template <int D>
+__device__ __forceinline__ void prefetch_vt(const uint16_t *V, const int (&voff)[D / 32], bf16x8 (&pre)[LOOKAHEAD]) {
+#pragma unroll
+    for (int n = 0; n < LOOKAHEAD; ++n) pre[n] = load_vt<D>(V, voff, n);
+}
+
+template <int D, bool PV, bool S>
+__device__ __forceinline__ void matrix_phase(WaveState<D> &w, const uint16_t *V, const int (&voff)[D / 32],
+                                             const uint16_t *K, const bf16x8 (&qop)[D / 16], int krow, int half,
+                                             const bf16x8 (&pre)[LOOKAHEAD]) {
+    constexpr int NET = D / 32, NDS = D / 16;
+    constexpr int NPV = PV ? 4 * NET : 0;
+    constexpr int N = NPV + (S ? 2 * NDS : 0);
+    static_assert(!PV || NPV >= LOOKAHEAD, "prefetched fragments must all be V^T fragments");
+    auto load = [&](int n) -> bf16x8 {
+        if (n < NPV) return load_vt<D>(V, voff, n);
+        const int n2 = n - NPV, ds = n2 >> 1, kt = n2 & 1;
+        return *reinterpret_cast<const bf16x8 *>(&K[k_lds<D>(kt * 32 + krow, ds * 2 + half)]);
+    };
+    bf16x8 f[N];
+#pragma unroll
+    for (int n = 0; n < LOOKAHEAD && n < N; ++n) f[n] = PV ? pre[n] : load(n);
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+        if (n + LOOKAHEAD < N) f[n + LOOKAHEAD] = load(n + LOOKAHEAD);
+        if (n < NPV) {
+            const int et = n % NET, g4 = n / NET;
+            w.o[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[n], w.p[g4 >> 1][g4 & 1], w.o[et], 0, 0, 0);
+        } else {
+            const int n2 = n - NPV, ds = n2 >> 1, kt = n2 & 1;
+            w.s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[n], qop[ds], ds == 0 ? f32x16{} : w.s[kt], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// Softmax phase of a wavefront for one block: the block maximum (one lane
+// swap between the half-waves), the lazy raise of the running maximum (O and
+// l rescaled only when the block maximum exceeds it by more than
+// 2^RESCALE_SLACK), then P = 2^(s*scale*log2(e) - m) as bf16 and the row sums
+// of that rounded P.
+template <int D>
+__device__ __forceinline__ void softmax_phase(WaveState<D> &w, float scale_log2) {
+    float mx[2] = {-__builtin_inff(), -__builtin_inff()};   // two partial maxima
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i2 = 0; i2 < 16; ++i2) mx[i2 & 1] = fmaxf(mx[i2 & 1], w.s[kt][i2]);
+    const float mblk = half_swap_max(fmaxf(mx[0], mx[1])) * scale_log2;
+    if (__any(mblk > w.m + RESCALE_SLACK)) {
+        const float m_new = fmaxf(w.m, mblk);
+        const float alpha = __builtin_amdgcn_exp2f(w.m - (m_new == -__builtin_inff() ? 0.f : m_new));
+        w.m = m_new;
+        w.l *= alpha;
+#pragma unroll
+        for (int et = 0; et < D / 32; ++et) w.o[et] *= alpha;
+    }
+    const float m_use = w.m == -__builtin_inff() ? 0.f : w.m;
+    // row sums of the rounded P (the values the PV product uses), two bf16
+    // pairs per dot instruction, two partial sums
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+    float lsum[2] = {0.f, 0.f};
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            f32x8 pv;
+#pragma unroll
+            for (int i2 = 0; i2 < 8; ++i2)
+                pv[i2] = __builtin_amdgcn_exp2f(fmaf(w.s[kt][hf * 8 + i2], scale_log2, -m_use));
+            const bf16x8 pp = __builtin_convertvector(pv, bf16x8);
+            w.p[kt][hf] = pp;
+            lsum[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pp, pp, 0, 1), ones, lsum[0], false);
+            lsum[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pp, pp, 2, 3), ones, lsum[1], false);
+            lsum[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pp, pp, 4, 5), ones, lsum[0], false);
+            lsum[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pp, pp, 6, 7), ones, lsum[1], false);
+        }
+    w.l += lsum[0] + lsum[1];
 }
 
 template <int D>
@@ -120,7 +250,9 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     constexpr int KROWS = 512 / D;                 // K rows per chunk
     constexpr int CPP = D / 32;                    // chunks per page (K and V alike)
     constexpr int NDMA = 2 * CPW;                  // DMA instructions per wavefront per block
-    constexpr int NBUF = 3;
+    // buffers: the current block, the previous one (its V is read in this
+    // block's phase B), and two blocks whose copies are in flight
+    constexpr int NBUF = 4;
     static_assert(CPW >= 1 && CHUNKS % WAVES == 0, "tile does not divide");
     extern __shared__ __align__(1024) uint16_t lds[];   // [NBUF][K tile, V tile]
 
@@ -130,27 +262,24 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
 
     // XCD-aware decode: workgroup w runs on XCD w % 8; all row tiles of one
     // (KV head, split) group get consecutive slots on the same XCD
-    const int w = blockIdx.x;
-    const int xcd = w & 7, local = w >> 3;
+    const int wg = blockIdx.x;
+    const int xcd = wg & 7, local = wg >> 3;
     const int gamma = (local / p.m_tiles) * 8 + xcd;
     if (gamma >= p.n_groups) return;
     const int mt = local % p.m_tiles;
     const int g = gamma / p.n_split, split = gamma - g * p.n_split;
 
-    int tok[QB];
-    bool row_ok[QB];
-    bf16x8 qop[QB][D / 16];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + qb * 32 + col;
-        row_ok[qb] = row < p.rows;
-        tok[qb] = row_ok[qb] ? (int)(row / p.grp) : 0;
-        const int head = g * p.grp + (row_ok[qb] ? (int)(row % p.grp) : 0);
-        const uint16_t *qr = p.q + ((int64_t)tok[qb] * p.nq + head) * D + half * 8;
+    const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + col;
+    const bool row_ok = row < p.rows;
+    const int tok = row_ok ? (int)(row / p.grp) : 0;
+    bf16x8 qop[D / 16];
+    {
+        const int head = g * p.grp + (row_ok ? (int)(row % p.grp) : 0);
+        const uint16_t *qr = p.q + ((int64_t)tok * p.nq + head) * D + half * 8;
 #pragma unroll
         for (int ds = 0; ds < D / 16; ++ds) {
-            u32x4 v = row_ok[qb] ? *reinterpret_cast<const u32x4 *>(qr + ds * 16) : u32x4{0, 0, 0, 0};
-            qop[qb][ds] = __builtin_bit_cast(bf16x8, v);
+            u32x4 v = row_ok ? *reinterpret_cast<const u32x4 *>(qr + ds * 16) : u32x4{0, 0, 0, 0};
+            qop[ds] = __builtin_bit_cast(bf16x8, v);
         }
     }
 
@@ -187,46 +316,47 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
             pid[u] = v < n_pre_pages ? pages_c[v] : 0;
         }
     };
+    // per-lane parts of the copy addresses (bytes), fixed for the whole loop:
+    // chunk u of a wavefront covers key rows rr[u] + [0, KROWS) of its page
+    uint32_t klane[CPW], vlane[CPW];
+    int rr[CPW];
+#pragma unroll
+    for (int u = 0; u < CPW; ++u) {
+        const unsigned q = (unsigned)(u * WAVES + wave);
+        const int r = (int)(q % CPP) * KROWS + lane / (D / 8);   // key row within the page
+        const int ck = (lane % (D / 8)) ^ (r & (D / 8 - 1));
+        const int cv = (lane % (D / 8)) ^ v_swz<D>(r);
+        rr[u] = r;
+        klane[u] = (uint32_t)(r * D + ck * 8) * 2;
+        vlane[u] = (uint32_t)(r * D + cv * 8) * 2;
+    }
     auto issue_block = [&](int64_t b, int buf, const int32_t (&pid)[CPW]) {
         uint16_t *kt_lds = lds + buf * 2 * TILE;
         uint16_t *vt_lds = kt_lds + TILE;
 #pragma unroll
         for (int u = 0; u < CPW; ++u) {
             const int q = u * WAVES + wave;                   // chunk index, uniform per wavefront
-            const int pg = q / CPP;                           // its page within the block
-            const int r = (q % CPP) * KROWS + lane / (D / 8); // key row within the page
-            const int ck = (lane % (D / 8)) ^ (r & (D / 8 - 1));
-            const int cv = (lane % (D / 8)) ^ v_swz<D>(r);
-            const int64_t v = b * 4 + pg;                     // page of the key sequence
-            const uint16_t *krow, *vrow;
+            const int64_t v = b * 4 + q / CPP;                // page of the key sequence
             if (v < n_pre_pages) {
-                const int64_t blk = ((int64_t)pid[u] * nkv + g) * head_block + r * D;
-                krow = pool_k + blk;
-                vrow = pool_v + blk;
+                const int64_t blk = ((int64_t)pid[u] * nkv + g) * head_block;
+                dma16(pool_k + blk, klane[u], kt_lds + q * 512);
+                dma16(pool_v + blk, vlane[u], vt_lds + q * 512);
             } else {
                 // suffix token; rows past the last one repeat it (finite, and masked)
-                int64_t T = (v - n_pre_pages) * PAGE + r;
+                int64_t T = (v - n_pre_pages) * PAGE + rr[u];
                 if (T > Ts - 1) T = Ts - 1;
-                const int64_t row = (T * nkv + g) * D;
-                krow = k_new + row;
-                vrow = v_new + row;
+                const uint32_t rw = (uint32_t)((T * nkv + g) * D - rr[u] * D) * 2;
+                dma16(k_new, rw + klane[u], kt_lds + q * 512);
+                dma16(v_new, rw + vlane[u], vt_lds + q * 512);
             }
-            dma16(krow + ck * 8, kt_lds + q * 512);
-            dma16(vrow + cv * 8, vt_lds + q * 512);
         }
     };
 
-    f32x16 oacc[QB][D / 32];
+    WaveState<D> w;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int et = 0; et < D / 32; ++et) oacc[qb][et] = f32x16{};
-    float m_run[QB], l_run[QB];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        m_run[qb] = -__builtin_inff();
-        l_run[qb] = 0.f;
-    }
+    for (int et = 0; et < D / 32; ++et) w.o[et] = f32x16{};
+    w.m = -__builtin_inff();
+    w.l = 0.f;
     const int krow = key_perm(col);
     // Transposing V reads: in each 16-lane group, source lane 4j+q names the
     // four dims [4q, 4q+4) of key row j; output lane i then holds dim i of
@@ -243,6 +373,30 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
         }
     }
 
+    // Mask of one block: keys [0, pe) of the block are prefix keys, suffix
+    // keys start at ps, and a row sees suffix key k (block position) when
+    // k - ps <= its token.  Branch-free bitwise select of the score or -inf
+    // (a short-circuit form was compiled into divergent branches that
+    // dropped the kept value).
+    // (The limits are shifted by this half-wave's key offset so that each
+    // comparison is against a constant: no per-lane key index stays live.)
+    auto mask_block = [&](int64_t b) {
+        const int sh = 8 * half;
+        const int pe = (int)(p.Tp - b * KB) - sh;
+        const int ps = (int)(p.n_pre_pages * PAGE - b * KB) - sh;
+        const int lim = tok + ps;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int i2 = 0; i2 < 16; ++i2) {
+                const int kin = kt * 32 + (i2 < 8 ? i2 : 8 + i2);   // key in the block, less 8*half
+                const uint32_t keep = 0u - (uint32_t)((kin < pe) | ((kin >= ps) & (kin <= lim)));
+                w.s[kt][i2] = __uint_as_float((__float_as_uint(w.s[kt][i2]) & keep) | (0xff800000u & ~keep));
+            }
+    };
+    // Q operands are in registers before the key loop starts (a wait the
+    // compiler sees, so it places none of its own inside the loop)
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     const int nb = (int)(b1 > b0 ? b1 - b0 : 0);
     int32_t pid[CPW];
     if (nb > 0) {
@@ -254,162 +408,111 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
         issue_block(b0 + 1, 1, pid);
     }
     if (nb > 2) load_pids(b0 + 2, pid);
-    for (int i = 0; i < nb; ++i) {
-        const int64_t b = b0 + i;
-        const int buf = i % NBUF;
-        // this block's copies are done (the next block's may still fly),
-        // and every wavefront is past the block that last used buffer i+2
-        if (i + 1 < nb) wait_vmcnt<NDMA>();
+    // Ping-pong schedule.  Each wavefront alternates a matrix phase (PV of
+    // block j-1, S of block j) and a softmax phase (block j); wavefronts 4-7
+    // (the second wavefront of every SIMD) run the same sequence one phase
+    // later than wavefronts 0-3, so on every SIMD one wavefront's MFMAs run
+    // beside the other's softmax.  A workgroup barrier ends every phase.
+    // Block j's tile becomes readable at phase 2j: its copies were started
+    // at phase 2j-4 and each wavefront waits for its own before the barrier;
+    // the copy of block j+2 then goes into the buffer of block j-2, whose
+    // last reads (wavefronts 4-7's PV of block j-2) ended with phase 2j-1.
+    const bool first = (wave >> 2) == 0;
+    auto tile_k = [&](int j) -> const uint16_t * { return lds + (j % NBUF) * 2 * TILE; };
+    auto tile_v = [&](int j) -> const uint16_t * { return lds + (j % NBUF) * 2 * TILE + TILE; };
+    // phase 2j: block j's tile becomes readable, block j+2's copy starts
+    auto open_block = [&](int j) {
+        if (j + 1 < nb) wait_vmcnt<NDMA>();
         else wait_vmcnt<0>();
         lds_barrier();
-        if (i + 2 < nb) issue_block(b + 2, (i + 2) % NBUF, pid);
-        if (i + 3 < nb) load_pids(b + 3, pid);
-        const uint16_t *K = lds + buf * 2 * TILE;
-        uint16_t *V = const_cast<uint16_t *>(K) + TILE;
-
-        const bool edge = (b + 1) * 4 > full_pre_pages;   // block holds a partial page or suffix keys
-        if (edge && b * 4 <= full_pre_pages && full_pre_pages < p.n_pre_pages) {
+        if (j + 2 < nb) issue_block(b0 + j + 2, (j + 2) % NBUF, pid);
+        if (j + 3 < nb) load_pids(b0 + j + 3, pid);
+        const int64_t b = b0 + j;
+        if (j < nb && (b + 1) * 4 > full_pre_pages && b * 4 <= full_pre_pages && full_pre_pages < p.n_pre_pages) {
             // last, partial prefix page: its slots past Tp may hold anything;
-            // zero them so masked keys contribute exactly nothing
+            // zero them so masked keys contribute exactly nothing (the V
+            // tile is first read after the next barrier)
+            uint16_t *V = lds + (j % NBUF) * 2 * TILE + TILE;
             const int pg = (int)(full_pre_pages - b * 4), k0 = (int)(p.Tp % PAGE);
             for (int idx = tid; idx < D * (PAGE - k0); idx += THREADS) V[(pg * PAGE + k0) * D + idx] = 0;
+        }
+    };
+    auto softmax_block = [&](int j) {
+        const int64_t b = b0 + j;
+        if ((b + 1) * 4 > full_pre_pages) mask_block(b);   // partial page or suffix keys
+        softmax_phase<D>(w, p.scale_log2);
+    };
+    // Each group runs its own copy of the loop (one straight path each, so
+    // the accumulators keep their registers); both execute the same barriers.
+    if (nb > 0) {
+        bf16x8 pre[LOOKAHEAD];
+        if (first) {
+            open_block(0);
+            matrix_phase<D, false, true>(w, nullptr, voff, tile_k(0), qop, krow, half, pre);
             lds_barrier();
-        }
-
-        // S^T = K Q^T for both 32-key halves of the block, issued back to back
-        // so the MFMAs of the second half run while the first half's softmax
-        // executes on the vector ALU
-        f32x16 sacc[QB][2];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            bf16x8 kf[D / 16];
-#pragma unroll
-            for (int ds = 0; ds < D / 16; ++ds)
-                kf[ds] = *reinterpret_cast<const bf16x8 *>(&K[k_lds<D>(kt * 32 + krow, ds * 2 + half)]);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-                sacc[qb][kt] = f32x16{};
-#pragma unroll
-                for (int ds = 0; ds < D / 16; ++ds)
-                    sacc[qb][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ds], qop[qb][ds], sacc[qb][kt], 0, 0, 0);
+            softmax_block(0);
+            for (int j = 1; j < nb; ++j) {
+                prefetch_vt<D>(tile_v(j - 1), voff, pre);
+                open_block(j);
+                matrix_phase<D, true, true>(w, tile_v(j - 1), voff, tile_k(j), qop, krow, half, pre);
+                lds_barrier();
+                softmax_block(j);
             }
-        }
-
-        if (edge) {
-            // keys [0, pe) of the block are prefix keys; suffix keys start at ps;
-            // a row sees suffix key (block position k) when k - ps <= its token
-            const int pe = (int)(p.Tp - b * KB);
-            const int ps = (int)(p.n_pre_pages * PAGE - b * KB);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-                const int lim = tok[qb] + ps;
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int i2 = 0; i2 < 16; ++i2) {
-                        const int kin = kt * 32 + (i2 < 8 ? i2 : 8 + i2) + 8 * half;
-                        // branch-free: bitwise predicate, then a bitwise select of
-                        // the score or -inf (a short-circuit form was compiled into
-                        // divergent branches that dropped the kept value)
-                        const uint32_t keep = 0u - (uint32_t)((kin < pe) | ((kin >= ps) & (kin <= lim)));
-                        sacc[qb][kt][i2] = __uint_as_float((__float_as_uint(sacc[qb][kt][i2]) & keep) |
-                                                           (0xff800000u & ~keep));
-                    }
+            prefetch_vt<D>(tile_v(nb - 1), voff, pre);
+            open_block(nb);
+            matrix_phase<D, true, false>(w, tile_v(nb - 1), voff, nullptr, qop, krow, half, pre);
+            lds_barrier();
+        } else {
+            open_block(0);
+            lds_barrier();
+            matrix_phase<D, false, true>(w, nullptr, voff, tile_k(0), qop, krow, half, pre);
+            for (int j = 1; j < nb; ++j) {
+                open_block(j);
+                softmax_block(j - 1);
+                prefetch_vt<D>(tile_v(j - 1), voff, pre);
+                lds_barrier();
+                matrix_phase<D, true, true>(w, tile_v(j - 1), voff, tile_k(j), qop, krow, half, pre);
             }
-        }
-
-        // online softmax per 32-key half, one query column per lane; the
-        // running maximum is raised (and O rescaled) only when it lags the
-        // half's maximum by more than 2^RESCALE_SLACK
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            float m_use[QB];
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-                float mx = -__builtin_inff();
-#pragma unroll
-                for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, sacc[qb][kt][i2]);
-                const float mblk = half_swap_max(mx) * p.scale_log2;
-                if (__any(mblk > m_run[qb] + RESCALE_SLACK)) {
-                    const float m_new = fmaxf(m_run[qb], mblk);
-                    const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - (m_new == -__builtin_inff() ? 0.f : m_new));
-                    m_run[qb] = m_new;
-                    l_run[qb] *= alpha;
-#pragma unroll
-                    for (int et = 0; et < D / 32; ++et) oacc[qb][et] *= alpha;
-                }
-                m_use[qb] = m_run[qb] == -__builtin_inff() ? 0.f : m_run[qb];
-            }
-            // P = 2^(s*scale - m) as bf16, eight keys per MFMA operand; O^T += V^T P
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-                bf16x8 pf[QB];
-#pragma unroll
-                for (int qb = 0; qb < QB; ++qb) {
-                    f32x8 pv;
-                    float lsum = 0.f;
-#pragma unroll
-                    for (int i2 = 0; i2 < 8; ++i2) {
-                        const float e = __builtin_amdgcn_exp2f(fmaf(sacc[qb][kt][hf * 8 + i2], p.scale_log2, -m_use[qb]));
-                        lsum += e;
-                        pv[i2] = e;
-                    }
-                    l_run[qb] += lsum;
-                    pf[qb] = __builtin_convertvector(pv, bf16x8);
-                }
-#pragma unroll
-                for (int et = 0; et < D / 32; ++et) {
-                    const uint16_t *vp = V + voff[et] + (kt * 32 + hf * 16) * D;
-                    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)vp);
-                    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vp + 4 * D));
-                    const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-                    for (int qb = 0; qb < QB; ++qb)
-                        oacc[qb][et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[qb], oacc[qb][et], 0, 0, 0);
-                }
-            }
+            open_block(nb);
+            softmax_block(nb - 1);
+            prefetch_vt<D>(tile_v(nb - 1), voff, pre);
+            lds_barrier();
+            matrix_phase<D, true, false>(w, tile_v(nb - 1), voff, nullptr, qop, krow, half, pre);
         }
     }
 
+    const float l_tot = half_swap_sum(w.l);
+    if (!row_ok) return;
+    if (p.n_split == 1) {
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        const int head = g * p.grp + (int)(row % p.grp);
+        uint16_t *orow = p.out + ((int64_t)tok * p.nq + head) * D;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const float l_tot = half_swap_sum(l_run[qb]);
-        if (!row_ok[qb]) continue;
-        const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + qb * 32 + col;
-        if (p.n_split == 1) {
-            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            const int head = g * p.grp + (int)(row % p.grp);
-            uint16_t *orow = p.out + ((int64_t)tok[qb] * p.nq + head) * D;
+        for (int et = 0; et < D / 32; ++et)
 #pragma unroll
-            for (int et = 0; et < D / 32; ++et)
-#pragma unroll
-                for (int vq = 0; vq < 4; ++vq) {
-                    f32x4 o4 = {oacc[qb][et][vq * 4 + 0], oacc[qb][et][vq * 4 + 1], oacc[qb][et][vq * 4 + 2],
-                                oacc[qb][et][vq * 4 + 3]};
-                    *reinterpret_cast<bf16x4 *>(orow + et * 32 + vq * 8 + half * 4) =
-                        __builtin_convertvector(o4 * inv, bf16x4);
-                }
-        } else {
-            const int64_t prow = ((int64_t)split * p.nkv + g) * p.rows_pad + row;
-            float *orow = p.o_part + prow * D;
-#pragma unroll
-            for (int et = 0; et < D / 32; ++et)
-#pragma unroll
-                for (int vq = 0; vq < 4; ++vq) {
-                    f32x4 o4 = {oacc[qb][et][vq * 4 + 0], oacc[qb][et][vq * 4 + 1], oacc[qb][et][vq * 4 + 2],
-                                oacc[qb][et][vq * 4 + 3]};
-                    *reinterpret_cast<f32x4 *>(orow + et * 32 + vq * 8 + half * 4) = o4;
-                }
-            if (half == 0) {
-                p.ml_part[prow * 2 + 0] = m_run[qb];
-                p.ml_part[prow * 2 + 1] = l_tot;
+            for (int vq = 0; vq < 4; ++vq) {
+                f32x4 o4 = {w.o[et][vq * 4 + 0], w.o[et][vq * 4 + 1], w.o[et][vq * 4 + 2], w.o[et][vq * 4 + 3]};
+                *reinterpret_cast<bf16x4 *>(orow + et * 32 + vq * 8 + half * 4) = __builtin_convertvector(o4 * inv, bf16x4);
             }
+    } else {
+        const int64_t prow = ((int64_t)split * p.nkv + g) * p.rows_pad + row;
+        float *orow = p.o_part + prow * D;
+#pragma unroll
+        for (int et = 0; et < D / 32; ++et)
+#pragma unroll
+            for (int vq = 0; vq < 4; ++vq) {
+                f32x4 o4 = {w.o[et][vq * 4 + 0], w.o[et][vq * 4 + 1], w.o[et][vq * 4 + 2], w.o[et][vq * 4 + 3]};
+                *reinterpret_cast<f32x4 *>(orow + et * 32 + vq * 8 + half * 4) = o4;
+            }
+        if (half == 0) {
+            p.ml_part[prow * 2 + 0] = w.m;
+            p.ml_part[prow * 2 + 1] = l_tot;
         }
     }
 }
 
 template <int D>
-constexpr size_t attn_lds_bytes() { return (size_t)3 * 2 * KB * D * 2; }
+constexpr size_t attn_lds_bytes() { return (size_t)4 * 2 * KB * D * 2; }
 
 // Merge the splits of each row: weights 2^(m_s - M), normalised by the
 // matching sum of l_s; bf16 out.

@@ -326,7 +326,7 @@ def run_bench(args):
                    "step": "device-staged pipeline: per layer ingest (copy stream) then attention (compute "
                            "stream), all layers"},
         "roofline": {"bound": "hbm", "kernel": "ingest (kv_ingest_rows_kernel beside the attention; "
-                     "kv_ingest_kernel for a step's first layer)", "achieved": round(value, 2),
+                     "kv_ingest_src_kernel for a step's first layer)", "achieved": round(value, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "traffic_source": traffic_src,
                      "bytes_per_launch": per_launch_bytes, "launches": n_ingest,
@@ -399,6 +399,7 @@ def profile_summary(paths, workload, warmup, steps):
     b = 2 * wl.num_kv_heads * wl.head_dim * 2
     out = []
     counters = {}
+    attn_counters = []
     for path in paths:
         c = sqlite3.connect(path)
         has_pmc = c.execute("select count(*) from counters_collection").fetchone()[0] > 0
@@ -441,16 +442,34 @@ def profile_summary(paths, workload, warmup, steps):
                 e = by_disp.setdefault(disp, {"name": name, "start": st, "end": en, "c": {}})
                 e["c"][cn] = e["c"].get(cn, 0.0) + val
             disp = sorted(by_disp.values(), key=lambda e: e["start"])
+            att = [e for e in disp if "attn_fwd_kernel" in e["name"]][lo:hi]
+            if att and any("MfmaUtil" in e["c"] for e in att):
+                attn_counters.append((os.path.basename(path), att))
             ing = [e for e in disp if "kv_ingest" in e["name"]]
             first_ing = ing[0]["start"] if ing else float("inf")
             cal = [e for e in disp if "copyBuffer" in e["name"] and e["start"] < first_ing
                    and e["end"] - e["start"] > 20000]
             sel = ing[lo:hi]
-            for cn in sorted({k for e in sel for k in e["c"]}):
+            for cn in sorted({k for e in sel for k in e["c"]} & {"FETCH_SIZE", "WRITE_SIZE"}):
                 counters[cn] = {"ingest_kib": float(np.mean([e["c"][cn] for e in sel])),
                                 "calib_kib": float(sum(e["c"].get(cn, 0.0) for e in cal)),
                                 "calib_dispatches": len(cal), "ingest_dispatches": len(sel),
                                 "db": os.path.basename(path)}
+    for db, att in attn_counters:
+        # derived counters as rocprofv3 reports them (percent of the kernel's GPU time)
+        flops = attn_flops(wl.num_q_heads, wl.head_dim, wl.prefix_tokens[0], wl.suffix_tokens[0])
+        out.append(f"### Attention counters (`{db}`, {len(att)} timed-step `attn_fwd_kernel` dispatches)\n")
+        out.append("| counter | mean per dispatch |\n|---|---|")
+        for cn in sorted({k for e in att for k in e["c"]}):
+            vals = [e["c"][cn] for e in att if cn in e["c"]]
+            out.append(f"| {cn} | {np.mean(vals):.4g} |")
+        mops = [e["c"]["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for e in att if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in e["c"]]
+        if mops:
+            out.append("")
+            out.append(f"MFMA bf16 flops per dispatch (MOPS x 512): {np.mean(mops) * 512:.4g}; algorithmic "
+                       f"flops per layer (unmasked pairs): {flops:.4g}; ratio {np.mean(mops) * 512 / flops:.3f} "
+                       f"(masked pairs of the causal diagonal and padding rows are computed and discarded).")
+        out.append("")
     if counters:
         nbytes = 2.0 * sum(wl.prefix_tokens) * b / len(wl.prefix_tokens)
         out.append("### HBM byte counters (ingest, timed-step launches)\n")

@@ -7,13 +7,15 @@
 // of a chunk token-major ([K|V][token][head][dim]), the pool holds them per
 // (page, head) block ([slot][dim]).  Two launch shapes:
 //  - alone on the GPU (the single-layer entry point, the first layer of a
-//    run): pieces numbered by (page of the prefix, head), then K/V, slot and
-//    16-byte column, two per thread, 256 pieces apart, so a wavefront writes
-//    1 KiB of one block contiguously and many short wavefronts stream;
-//  - beside the attention kernel of an earlier layer, where one ingest
-//    wavefront per SIMD fits: a thread takes 8 slots x one 16-byte column of
-//    one (page, head) block and moves its K rows, then its V rows (8 loads in
-//    flight, one page lookup per 256 bytes moved).
+//    run): one piece per thread in payload order, so every wavefront reads
+//    1 KiB of the payload contiguously and writes four 256-byte rows, and
+//    many short wavefronts keep the most bytes in flight;
+//  - beside the attention kernel of an earlier layer, where only a couple of
+//    ingest wavefronts per SIMD fit: a thread takes 8 slots x one 16-byte
+//    column of one (page, head) block and moves its K rows, then its V rows
+//    (8 loads in flight, one page lookup per 256 bytes moved).
+// The gather (pool -> payload, the inverse) numbers pieces by destination
+// block, two per thread.
 #include "common.hpp"
 
 namespace oc {
@@ -80,11 +82,6 @@ __device__ inline void copy_pieces(const IngestArgs &a, uint16_t *payload_out, i
         if (ok[i]) *reinterpret_cast<u32x4 *>(FORWARD ? a.pool_k + keep[i] : payload_out + keep[i]) = r[i];
 }
 
-template <int U, bool POW2>
-__global__ __launch_bounds__(kThreads, 8) void kv_ingest_kernel(IngestArgs a, int64_t n_units) {
-    copy_pieces<U, POW2, true>(a, nullptr, n_units);
-}
-
 // 8 slots x one 16-byte column of one (page, head) block, K then V.
 __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs a, int64_t n_rows8) {
     const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -131,6 +128,47 @@ __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs 
     }
 }
 
+// One 16-byte piece per thread, pieces numbered in payload order
+// ([chunk][K|V][token][head][16-byte column]): every wavefront reads 1 KiB of
+// the payload contiguously and writes 256-byte rows into the (page, head)
+// blocks.  Many short wavefronts keep the most bytes in flight.
+template <bool POW2>
+__global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, int64_t n_pieces) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= n_pieces) return;
+    int c, h, t, kv;
+    int64_t j;
+    if (POW2) {
+        c = (int)(e & (a.d8 - 1));
+        h = (int)((e >> a.lg_d8) & (a.n_kv - 1));
+        t = (int)((e >> (a.lg_d8 + a.lg_nkv)) & (a.G - 1));
+        kv = (int)((e >> (a.lg_d8 + a.lg_nkv + a.lg_g)) & 1);
+        j = e >> (a.lg_d8 + a.lg_nkv + a.lg_g + 1);
+    } else {
+        int64_t r = e / a.d8;
+        c = (int)(e - r * a.d8);
+        int64_t r2 = r / a.n_kv;
+        h = (int)(r - r2 * a.n_kv);
+        int64_t r3 = r2 / a.G;
+        t = (int)(r2 - r3 * a.G);
+        j = r3 >> 1;
+        kv = (int)(r3 & 1);
+    }
+    const int64_t T = j * a.G + t;
+    int64_t q, slot;
+    if (POW2) {
+        q = T >> a.lg_ps;
+        slot = T & (a.Ps - 1);
+    } else {
+        q = T / a.Ps;
+        slot = T - q * a.Ps;
+    }
+    const int64_t page = a.pages[q];
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(a.staging + e * 8);
+    *reinterpret_cast<u32x4 *>(a.pool_k + kv * a.region + ((page * a.n_kv + h) * a.Ps + slot) * (int64_t)a.d + c * 8) =
+        v;
+}
+
 template <bool POW2>
 __global__ __launch_bounds__(kThreads, 8) void kv_gather_kernel(IngestArgs a, uint16_t *payload, int64_t n_units) {
     copy_pieces<2, POW2, false>(a, payload, n_units);
@@ -155,14 +193,6 @@ static bool prepare(IngestArgs &a) {
     return p2;
 }
 
-template <int U>
-static void launch_u(const IngestArgs &a, bool p2, int64_t n_units, hipStream_t s) {
-    const int64_t n = n_units * 2 * a.Ps * a.d8;
-    const dim3 grid((unsigned)((n + kThreads * U - 1) / (kThreads * U)));
-    if (p2) hipLaunchKernelGGL((kv_ingest_kernel<U, true>), grid, dim3(kThreads), 0, s, a, n_units);
-    else hipLaunchKernelGGL((kv_ingest_kernel<U, false>), grid, dim3(kThreads), 0, s, a, n_units);
-}
-
 hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool beside_compute) {
     if (n_pages_used == 0) return hipSuccess;
     const bool p2 = prepare(a);
@@ -172,8 +202,12 @@ hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool
         hipLaunchKernelGGL(kv_ingest_rows_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
                            s, a, n);
     } else {
-        launch_u<2>(a, p2, n_units, s);
+        const int64_t n = a.num_tokens * 2 * a.n_kv * a.d8;   // 16-byte pieces of the payload
+        const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
+        if (p2) hipLaunchKernelGGL(kv_ingest_src_kernel<true>, grid, dim3(kThreads), 0, s, a, n);
+        else hipLaunchKernelGGL(kv_ingest_src_kernel<false>, grid, dim3(kThreads), 0, s, a, n);
     }
+    (void)n_units;
     return hipGetLastError();
 }
 

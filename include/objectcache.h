@@ -34,7 +34,7 @@
 extern "C" {
 #endif
 
-#define OC_ABI_VERSION 1
+#define OC_ABI_VERSION 2
 
 typedef enum {
     OC_OK = 0,
@@ -113,6 +113,19 @@ int oc_block_table_check(const int32_t *host_pages, int64_t num_entries, int64_t
 int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_table,
                        oc_kv_pool *kv_pool, int32_t layer, void *stream);
 
+/* Chunkwise ingest (the delivery mode of eq. (2) below the threshold, where
+ * whole chunk objects arrive instead of layer payloads): scatter every layer
+ * of num_chunks consecutive chunk objects of a request into the pool.
+ * objects->data holds the objects back to back as stored (each L*S bytes:
+ * layer 0's KV_L2TD slice, then layer 1's, ...); they are chunks
+ * first_chunk .. first_chunk+num_chunks-1 of the request's prefix, so their
+ * tokens are first_chunk*G .. and the block table must cover them
+ * (block_table->num_tokens >= (first_chunk+num_chunks)*G).  The pool result
+ * equals oc_kv_layer_ingest of every layer payload.  Same alignment and
+ * shape requirements as oc_kv_layer_ingest; asynchronous on `stream`. */
+int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc_block_table *block_table,
+                        oc_kv_pool *kv_pool, void *stream);
+
 /* Inverse of the ingest: read the prefix of `layer` out of the pool into a
  * staging-layout device buffer (the layout a chunk object's layer slice has;
  * the write-back direction).  Same requirements as oc_kv_layer_ingest. */
@@ -154,6 +167,12 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
  * allocation policy each request gets its own rate for the run (one
  * scheduling epoch) and the producer dispatches their payload pieces by
  * weighted deficit round robin (Section 3.6 and its appendix pseudocode).
+ * A request delivered chunkwise (eq. (2)) instead receives its whole chunk
+ * objects in prefix order, as many per staging slot as fit; each group is
+ * landed and ingested with oc_kv_chunks_ingest, and its L layers' attention
+ * runs once the last group is in.  Chunkwise requests are delivered before
+ * the layerwise ones share the rate; they take OC_ALLOC_FIFO only (the
+ * allocation policies schedule layerwise requests, Section 3.4).
  * ------------------------------------------------------------------------- */
 
 /* Per-request bandwidth under a shared cap (Section 3.6; the baselines of the
@@ -191,6 +210,16 @@ typedef enum {
     OC_FAULT_ABORT = 2         /* producer gives up at fault_layer (tests error paths)      */
 } oc_fault;
 
+/* Delivery of a request's cached prefix (eq. (2), Section 3.4).  The
+ * storage layout is always chunkwise; the delivery order is the choice. */
+typedef enum {
+    OC_DELIVERY_LAYERWISE = 0, /* per-layer payloads; layer l computes while l+1 lands  */
+    OC_DELIVERY_CHUNKWISE = 1, /* whole chunk objects in prefix order; compute starts
+                                  after the last one is in (the chunkwise baseline)      */
+    OC_DELIVERY_AUTO = 2       /* eq. (2) per request: chunkwise when W = N*L*S is
+                                  below theta_bytes, layerwise otherwise                 */
+} oc_delivery;
+
 typedef struct {
     int32_t mode;              /* oc_mode                                                  */
     double rate_bytes_per_s;   /* producer pacing; 0 = as fast as memcpy goes              */
@@ -202,6 +231,8 @@ typedef struct {
     int32_t fault_layer;       /* layer at which the fault triggers                        */
     int32_t alloc_policy;      /* oc_alloc_policy (PRODUCER mode); budget = rate_bytes_per_s */
     double margin_bytes_per_s; /* delta of OC_ALLOC_CAL_STALL_OPT                          */
+    int32_t delivery;          /* oc_delivery, PRODUCER mode only (other modes: layerwise) */
+    double theta_bytes;        /* Theta of OC_DELIVERY_AUTO                                */
 } oc_pipeline_opts;
 
 /* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */
@@ -222,7 +253,9 @@ typedef struct {
 } oc_request;
 
 /* Per-request timings (milliseconds from the start of the run, all on one
- * clock).  Arrays, when non-NULL, are caller-owned with num_layers entries. */
+ * clock).  Arrays, when non-NULL, are caller-owned with num_layers entries.
+ * For a request delivered chunkwise, produced/landed/ingested of every layer
+ * are those of its last chunk group (the time every layer became usable). */
 typedef struct {
     double ttft_ms;            /* start -> this request's last layer done          */
     double *produced_ms;       /* host: layer payload fully in its pinned slot     */
@@ -230,6 +263,7 @@ typedef struct {
     double *ingested_ms;       /* device: ingest kernel finished                   */
     double *done_ms;           /* device: attention finished                       */
     double rate_bytes_per_s;   /* the request's allocated rate (0 under FIFO)      */
+    int32_t delivery;          /* the delivery the request got (oc_delivery)       */
 } oc_request_stats;
 
 /* Create a context on `device` for one pool.  Allocates the streams, events,

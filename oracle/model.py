@@ -5,6 +5,8 @@ Closed forms written from the paper:
     S = 2*G*n_kv*d*p;
   * eq. (2): size-threshold mode dispatch on W = N*L*S;
   * eq. (3): layerwise-prefetch TTFT  X_0 + sum_{l<L-1} max(X_{l+1}, C_l) + C_{L-1};
+  * Section 3.5: the chunkwise baseline waits for all transfers first,
+    sum X_l + sum C_l;
   * Section 5.3: overlap requirement B_req = D_l / t_l with
     D_l = 2*n_kv*d*p*(P*r);
   * Section 3.6, eq. (4): per-layer stall and the zero-stall rate r* = s/c;
@@ -47,6 +49,14 @@ def layerwise_ttft(X: Sequence[float], C: Sequence[float]) -> float:
     for l in range(L - 1):
         t += max(X[l + 1], C[l])
     return t + C[L - 1]
+
+
+def chunkwise_ttft(X: Sequence[float], C: Sequence[float]) -> float:
+    """Section 3.5's chunkwise baseline: compute waits for the whole cached
+    prefix, so every transfer comes before every layer's compute."""
+    if len(X) != len(C) or not X:
+        raise ValueError("X and C need one entry per layer")
+    return float(sum(X)) + float(sum(C))
 
 
 def required_bandwidth(context: int, hit: float, n_kv: int, d: int, t_layer_s: float,

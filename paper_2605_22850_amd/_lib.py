@@ -22,9 +22,11 @@ OC_OK, OC_EINVAL, OC_ESHAPE, OC_EALIGN, OC_ERANGE, OC_EHIP, OC_ETIMEOUT, OC_ENOM
 OC_MODE_HBM_RESIDENT, OC_MODE_DEVICE_STAGED, OC_MODE_PRODUCER = 0, 1, 2
 OC_FAULT_NONE, OC_FAULT_STALL, OC_FAULT_ABORT = 0, 1, 2
 ALLOC_POLICIES = {"fifo": 0, "equal": 1, "kv_prop": 2, "bw_prop": 3, "stall_opt": 4, "cal_stall_opt": 5}
+DELIVERIES = {"layerwise": 0, "chunkwise": 1, "auto": 2}
 
 EXPORTS = [
-    "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather",
+    "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest",
+    "oc_kv_layer_gather",
     "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
     "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate",
 ]
@@ -58,7 +60,7 @@ class c_pipeline_opts(ctypes.Structure):
     _fields_ = [("mode", c_int32), ("rate_bytes_per_s", c_double), ("piece_bytes", c_int64),
                 ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
                 ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
-                ("margin_bytes_per_s", c_double)]
+                ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double)]
 
 
 class c_request(ctypes.Structure):
@@ -70,7 +72,7 @@ class c_request(ctypes.Structure):
 class c_request_stats(ctypes.Structure):
     _fields_ = [("ttft_ms", c_double), ("produced_ms", POINTER(c_double)), ("landed_ms", POINTER(c_double)),
                 ("ingested_ms", POINTER(c_double)), ("done_ms", POINTER(c_double)),
-                ("rate_bytes_per_s", c_double)]
+                ("rate_bytes_per_s", c_double), ("delivery", c_int32)]
 
 
 _lib = None
@@ -87,6 +89,8 @@ def lib():
         L.oc_block_table_check.argtypes = [c_void_p, c_int64, c_int64, c_int64, c_int32]
         L.oc_kv_layer_ingest.argtypes = [POINTER(c_staging), POINTER(c_block_table), POINTER(c_kv_pool), c_int32,
                                          c_void_p]
+        L.oc_kv_chunks_ingest.argtypes = [POINTER(c_staging), c_int64, POINTER(c_block_table), POINTER(c_kv_pool),
+                                          c_void_p]
         L.oc_kv_layer_gather.argtypes = [POINTER(c_block_table), POINTER(c_kv_pool), c_int32, c_void_p, c_int64,
                                          c_int64, c_void_p]
         L.oc_attention_workspace_bytes.argtypes = [POINTER(c_layout), c_int64, c_int64]
@@ -106,8 +110,8 @@ def lib():
             L.oc_context_destroy.restype = None
         L.oc_bandwidth_allocate.argtypes = [c_int32, c_int32, POINTER(c_double), POINTER(c_double), c_double, c_double,
                                             POINTER(c_double)]
-        for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_layer_gather", "oc_suffix_prefill_layer",
-                     "oc_bandwidth_allocate"):
+        for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest", "oc_kv_layer_gather",
+                     "oc_suffix_prefill_layer", "oc_bandwidth_allocate"):
             getattr(L, name).restype = c_int
         _lib = L
     return _lib
@@ -184,6 +188,16 @@ def oc_kv_layer_ingest(staging, num_chunks: int, pages, num_tokens: int, pool, l
     _check(lib().oc_kv_layer_ingest(ctypes.byref(st), ctypes.byref(bt), ctypes.byref(kp), layer, _stream(stream)))
 
 
+def oc_kv_chunks_ingest(objects, num_chunks: int, first_chunk: int, pages, num_tokens: int, pool, layout: Layout,
+                        stream=None) -> None:
+    """Whole chunk objects (device, num_chunks * L * S bytes back to back) -> every layer of the pool."""
+    st = c_staging(_ptr(objects), num_chunks, layout.slice_bytes)
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_kv_chunks_ingest(ctypes.byref(st), first_chunk, ctypes.byref(bt), ctypes.byref(kp),
+                                     _stream(stream)))
+
+
 def oc_kv_layer_gather(pages, num_tokens: int, pool, layout: Layout, layer: int, staging_out, num_chunks: int,
                        stream=None) -> None:
     bt = make_table(pages, num_tokens)
@@ -231,10 +245,12 @@ class Request:
 def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, max_suffix_tokens: int,
                       rate_bytes_per_s: float = 0.0, piece_bytes: int = 0, slots: int = 0,
                       producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
-                      fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0):
+                      fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0,
+                      delivery="layerwise", theta_bytes: float = 0.0):
     pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
+    dv = DELIVERIES[delivery] if isinstance(delivery, str) else int(delivery)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
-                           fault_layer, pol, margin_bytes_per_s)
+                           fault_layer, pol, margin_bytes_per_s, dv, theta_bytes)
     kp = make_pool(pool, layout)
     ctx = c_void_p()
     _check(lib().oc_context_create(device, ctypes.byref(kp), ctypes.byref(opts), max_prefix_tokens,
@@ -273,13 +289,14 @@ def oc_pipeline_run(ctx, requests: Sequence[Request], num_layers: int):
                              r.layer_compute_s)
         per = [(c_double * num_layers)() for _ in range(4)]
         arrays.append(per)
-        stats[i] = c_request_stats(0.0, *per, 0.0)
+        stats[i] = c_request_stats(0.0, *per, 0.0, 0)
     _check(lib().oc_pipeline_run(ctx, creqs, n, stats))
     out = []
     for i in range(n):
         p = arrays[i]
         out.append({"ttft_ms": stats[i].ttft_ms, "produced_ms": list(p[0]), "landed_ms": list(p[1]),
-                    "ingested_ms": list(p[2]), "done_ms": list(p[3]), "rate_bytes_per_s": stats[i].rate_bytes_per_s})
+                    "ingested_ms": list(p[2]), "done_ms": list(p[3]), "rate_bytes_per_s": stats[i].rate_bytes_per_s,
+                    "delivery": {v: k for k, v in DELIVERIES.items()}[stats[i].delivery]})
     return out
 
 

@@ -59,6 +59,21 @@ static IngestArgs ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, 
     return a;
 }
 
+IngestArgs chunks_ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, const void *objects,
+                              int64_t first_chunk, int64_t num_chunks) {
+    const oc_layout &l = pool->layout;
+    IngestArgs a = ingest_args(pool, bt, 0, objects);
+    const int64_t slice = 2LL * l.chunk_tokens * l.num_kv_heads * l.head_dim;   // elements of S
+    const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+    a.num_tokens = num_chunks * l.chunk_tokens;
+    a.token0 = first_chunk * l.chunk_tokens;
+    a.chunk_stride = (int64_t)l.num_layers * slice;
+    a.n_layers = l.num_layers;
+    a.layer_step_staging = slice;
+    a.layer_step_pool = 2 * l.num_pages * block;
+    return a;
+}
+
 static int check_staging_shape(const oc_layout &l, const oc_block_table *bt, int64_t num_chunks,
                                int64_t slice_bytes) {
     const int64_t S = 2LL * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
@@ -115,6 +130,29 @@ int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_ta
     IngestArgs a = ingest_args(kv_pool, block_table, layer, staging->data);
     const int64_t n_pages = (block_table->num_tokens + l.page_size - 1) / l.page_size;
     OC_HIP(launch_ingest(a, n_pages, static_cast<hipStream_t>(stream), false));
+    return OC_OK;
+}
+
+int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc_block_table *block_table,
+                        oc_kv_pool *kv_pool, void *stream) {
+    clear_error();
+    if (!objects || !kv_pool) return fail(OC_EINVAL, "objects and kv_pool must not be NULL");
+    int rc = check_layout(kv_pool->layout);
+    if (rc) return rc;
+    const oc_layout &l = kv_pool->layout;
+    if ((rc = check_table(block_table, l))) return rc;
+    const int64_t S = 2LL * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
+    if (objects->per_layer_chunk_bytes != S)
+        return fail(OC_ESHAPE, "per_layer_chunk_bytes must equal 2*G*n_kv*d*2 = " + std::to_string(S));
+    if (first_chunk < 0 || objects->num_chunks < 0) return fail(OC_EINVAL, "negative first_chunk or num_chunks");
+    if ((first_chunk + objects->num_chunks) * l.chunk_tokens > block_table->num_tokens)
+        return fail(OC_ERANGE, "chunks past the end of the block table's prefix");
+    if (objects->num_chunks == 0) return OC_OK;
+    if (!objects->data || !kv_pool->base) return fail(OC_EINVAL, "NULL data or pool base");
+    if (!aligned(objects->data, 16) || !aligned(kv_pool->base, 16))
+        return fail(OC_EALIGN, "object data and pool base must be 16-byte aligned");
+    IngestArgs a = chunks_ingest_args(kv_pool, block_table, objects->data, first_chunk, objects->num_chunks);
+    OC_HIP(launch_chunks_ingest(a, static_cast<hipStream_t>(stream)));
     return OC_OK;
 }
 

@@ -27,12 +27,19 @@ inline bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintp
 
 // ---- ingest / gather ------------------------------------------------------
 struct IngestArgs {
-    const uint16_t *staging;   // one layer payload [N][2][G][n_kv][d]
+    const uint16_t *staging;   // chunk slices [N][2][G][n_kv][d], chunk_stride apart
     uint16_t *pool_k;          // pool + ((layer*2+0)*P) * n_kv * Ps * d
     uint16_t *pool_v;          // pool + ((layer*2+1)*P) * n_kv * Ps * d
     const int32_t *pages;
-    int64_t num_tokens;        // T_p
+    int64_t num_tokens;        // tokens in the staging (N * G)
     int32_t G, n_kv, d, Ps;
+    // optional (0 = one layer payload): elements from one chunk's slice to the
+    // next (a layer payload: 2*G*n_kv*d; whole chunk objects: L times that),
+    // the first staged token's index in the prefix, and for whole chunk
+    // objects the layer count with the per-layer steps in staging and pool
+    int64_t chunk_stride, token0;
+    int32_t n_layers;
+    int64_t layer_step_staging, layer_step_pool;
     // filled by the launcher
     int64_t region;            // pool_v - pool_k, elements
     int32_t d8, lg_d8, lg_ps, lg_nkv, lg_g;
@@ -40,6 +47,12 @@ struct IngestArgs {
 // beside_compute: launched to run next to the attention kernel (more bytes in
 // flight per thread) rather than alone on the GPU
 hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool beside_compute);
+// every layer of whole chunk objects (n_layers, layer steps and token0 set)
+hipError_t launch_chunks_ingest(IngestArgs a, hipStream_t s);
+// arguments for chunks first_chunk .. first_chunk+num_chunks-1 of a request,
+// stored back to back as whole objects at `objects`
+IngestArgs chunks_ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, const void *objects,
+                              int64_t first_chunk, int64_t num_chunks);
 hipError_t launch_gather(IngestArgs a, uint16_t *staging_out, int64_t n_pages_used, hipStream_t s);
 
 // ---- attention --------------------------------------------------------------

@@ -106,12 +106,12 @@ __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs 
         // the 8 tokens sit in one chunk, one payload row apart
         const int64_t j = T0 / G, t0 = T0 - j * G;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) src[i] = (j * 2 * G + t0 + i) * D + col;
+        for (int i = 0; i < 8; ++i) src[i] = j * a.chunk_stride + (t0 + i) * D + col;
     } else {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int64_t T = T0 + i, j = T / G;
-            src[i] = (j * 2 * G + (T - j * G)) * D + col;
+            src[i] = j * a.chunk_stride + (T - j * G) * D + col;
         }
     }
     u32x4 r[8];
@@ -132,10 +132,12 @@ __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs 
 // ([chunk][K|V][token][head][16-byte column]): every wavefront reads 1 KiB of
 // the payload contiguously and writes 256-byte rows into the (page, head)
 // blocks.  Many short wavefronts keep the most bytes in flight.
+// For whole chunk objects blockIdx.y is the layer.
 template <bool POW2>
 __global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, int64_t n_pieces) {
     const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (e >= n_pieces) return;
+    const int64_t slice_pieces = 2LL * a.G * a.n_kv * a.d8;   // 16-byte pieces per chunk slice
     int c, h, t, kv;
     int64_t j;
     if (POW2) {
@@ -154,7 +156,7 @@ __global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, i
         j = r3 >> 1;
         kv = (int)(r3 & 1);
     }
-    const int64_t T = j * a.G + t;
+    const int64_t T = a.token0 + j * a.G + t;
     int64_t q, slot;
     if (POW2) {
         q = T >> a.lg_ps;
@@ -164,9 +166,10 @@ __global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, i
         slot = T - q * a.Ps;
     }
     const int64_t page = a.pages[q];
-    const u32x4 v = *reinterpret_cast<const u32x4 *>(a.staging + e * 8);
-    *reinterpret_cast<u32x4 *>(a.pool_k + kv * a.region + ((page * a.n_kv + h) * a.Ps + slot) * (int64_t)a.d + c * 8) =
-        v;
+    const uint16_t *src = a.staging + blockIdx.y * a.layer_step_staging + j * a.chunk_stride + (e - j * slice_pieces) * 8;
+    uint16_t *pool = a.pool_k + blockIdx.y * a.layer_step_pool + kv * a.region;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(src);
+    *reinterpret_cast<u32x4 *>(pool + ((page * a.n_kv + h) * a.Ps + slot) * (int64_t)a.d + c * 8) = v;
 }
 
 template <bool POW2>
@@ -181,8 +184,11 @@ static int lg(int64_t x) {
     return r;
 }
 
-// Fills the derived fields; returns whether the shift decode applies.
+// Fills the derived fields and the defaults of a single layer payload;
+// returns whether the shift decode applies.
 static bool prepare(IngestArgs &a) {
+    if (a.chunk_stride == 0) a.chunk_stride = 2LL * a.G * a.n_kv * a.d;
+    if (a.n_layers == 0) a.n_layers = 1;
     a.d8 = a.d / 8;
     a.region = (int64_t)(a.pool_v - a.pool_k);
     const bool p2 = pow2(a.d8) && pow2(a.Ps) && pow2(a.n_kv) && pow2(a.G);
@@ -197,7 +203,7 @@ hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool
     if (n_pages_used == 0) return hipSuccess;
     const bool p2 = prepare(a);
     const int64_t n_units = n_pages_used * a.n_kv;
-    if (beside_compute) {
+    if (beside_compute && a.token0 == 0) {
         const int64_t n = n_pages_used * a.n_kv * (a.Ps / 8) * a.d8;
         hipLaunchKernelGGL(kv_ingest_rows_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
                            s, a, n);
@@ -208,6 +214,16 @@ hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool
         else hipLaunchKernelGGL(kv_ingest_src_kernel<false>, grid, dim3(kThreads), 0, s, a, n);
     }
     (void)n_units;
+    return hipGetLastError();
+}
+
+hipError_t launch_chunks_ingest(IngestArgs a, hipStream_t s) {
+    if (a.num_tokens == 0) return hipSuccess;
+    const bool p2 = prepare(a);
+    const int64_t n = a.num_tokens * 2 * a.n_kv * a.d8;   // 16-byte pieces of one layer
+    const dim3 grid((unsigned)((n + kThreads - 1) / kThreads), (unsigned)a.n_layers);
+    if (p2) hipLaunchKernelGGL(kv_ingest_src_kernel<true>, grid, dim3(kThreads), 0, s, a, n);
+    else hipLaunchKernelGGL(kv_ingest_src_kernel<false>, grid, dim3(kThreads), 0, s, a, n);
     return hipGetLastError();
 }
 

@@ -61,9 +61,14 @@ struct RunShared {
     std::deque<int64_t> reported; // rate producer -> driver: items complete in a pinned slot
 };
 
+// A unit of delivery: one layer payload of a request (layerwise), or a
+// group of whole chunk objects j0..j1-1 of a request (chunkwise, layer 0 for
+// the fault injection).
 struct Item {
     int32_t layer;
     int32_t req;
+    bool chunks = false;
+    int64_t j0 = 0, j1 = 0;
 };
 
 static int fill_defaults(oc_pipeline_opts &o) {
@@ -80,6 +85,10 @@ static int fill_defaults(oc_pipeline_opts &o) {
     if (o.alloc_policy != OC_ALLOC_FIFO && !(o.rate_bytes_per_s > 0))
         return fail(OC_EINVAL, "an allocation policy needs a positive budget (rate_bytes_per_s)");
     if (o.margin_bytes_per_s < 0) return fail(OC_EINVAL, "negative margin");
+    if (o.delivery < OC_DELIVERY_LAYERWISE || o.delivery > OC_DELIVERY_AUTO) return fail(OC_EINVAL, "unknown delivery");
+    if (o.theta_bytes < 0) return fail(OC_EINVAL, "negative theta_bytes");
+    if (o.delivery == OC_DELIVERY_CHUNKWISE && o.alloc_policy != OC_ALLOC_FIFO)
+        return fail(OC_EINVAL, "allocation policies schedule layerwise requests; chunkwise delivery needs OC_ALLOC_FIFO");
     return OC_OK;
 }
 
@@ -143,9 +152,14 @@ struct Producer {
             const Item it = (*items)[item];
             const oc_request &r = reqs[it.req];
             const int64_t N = r.prefix_tokens / c->pool.layout.chunk_tokens;
-            const int64_t j0 = p * cpp, j1 = std::min(N, j0 + cpp);
+            // layerwise: layer `it.layer` of every chunk, S bytes each;
+            // chunkwise: whole objects it.j0..it.j1-1, L*S bytes each
+            const int64_t unit = it.chunks ? (int64_t)L * S : S;
+            const int64_t first = it.chunks ? it.j0 : 0, last = it.chunks ? it.j1 : N;
+            const int64_t src_off = it.chunks ? 0 : (int64_t)it.layer * S;
+            const int64_t j0 = first + p * cpp, j1 = std::min(last, j0 + cpp);
             if (rate > 0) {
-                const double t_release = (cum + (double)j1 * S) / rate;
+                const double t_release = (cum + (double)(j1 - first) * unit) / rate;
                 const auto when = t0 + std::chrono::duration_cast<Clock::duration>(std::chrono::duration<double>(t_release));
                 // sleep most of the way, then spin for a microsecond-accurate release
                 for (;;) {
@@ -158,7 +172,7 @@ struct Producer {
             unsigned char *dst = static_cast<unsigned char *>(c->slots[item % c->slots.size()].pinned);
             for (int64_t j = j0; j < j1; ++j) {
                 const unsigned char *obj = static_cast<const unsigned char *>(r.chunk_objects[j]);
-                std::memcpy(dst + j * S, obj + (int64_t)it.layer * S, (size_t)S);
+                std::memcpy(dst + (j - first) * unit, obj + src_off, (size_t)unit);
             }
             {
                 std::lock_guard<std::mutex> g(wmu);
@@ -211,10 +225,11 @@ struct Producer {
             }
             if (aborted()) break;
             const oc_request &r = reqs[it.req];
-            const int64_t N = r.prefix_tokens / c->pool.layout.chunk_tokens;
+            const int64_t N = it.chunks ? it.j1 - it.j0 : r.prefix_tokens / c->pool.layout.chunk_tokens;
+            const int64_t unit = it.chunks ? (int64_t)L * S : S;
             {
                 std::lock_guard<std::mutex> g(wmu);
-                chunks_per_piece = std::max<int64_t>(1, c->opts.piece_bytes / S);
+                chunks_per_piece = std::max<int64_t>(1, c->opts.piece_bytes / unit);
                 n_pieces = (N + chunks_per_piece - 1) / chunks_per_piece;
                 next_piece = 0;
                 pieces_done = 0;
@@ -227,7 +242,7 @@ struct Producer {
                 wcv.wait(lk, [&] { return pieces_done == n_pieces; });
                 cur_item = -1;
             }
-            cum += (double)N * S;
+            cum += (double)N * unit;
             (*produced_ms)[k] = std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
             {
                 std::lock_guard<std::mutex> g(sh->mu);
@@ -534,13 +549,51 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         c->ws_bytes = ws_need;
     }
 
+    // delivery of each request (eq. (2)); only the producer has an order to choose
+    std::vector<int32_t> deliv(n_reqs, OC_DELIVERY_LAYERWISE);
+    const int64_t obj_bytes = (int64_t)L * S;     // one whole chunk object
+    int n_cw = 0;
+    if (mode == OC_MODE_PRODUCER)
+        for (int32_t r = 0; r < n_reqs; ++r) {
+            const int64_t N = reqs[r].prefix_tokens / l.chunk_tokens;
+            const double W = (double)N * (double)obj_bytes;
+            if (N > 0 && (c->opts.delivery == OC_DELIVERY_CHUNKWISE ||
+                          (c->opts.delivery == OC_DELIVERY_AUTO && W < c->opts.theta_bytes))) {
+                deliv[r] = OC_DELIVERY_CHUNKWISE;
+                ++n_cw;
+            }
+        }
+    if (n_cw > 0 && c->opts.alloc_policy != OC_ALLOC_FIFO)
+        return fail(OC_EINVAL, "a request falls on the chunkwise side of theta_bytes, and allocation policies "
+                               "schedule layerwise requests only (use OC_ALLOC_FIFO)");
+    if (n_cw > 0 && (int64_t)c->slot_bytes < obj_bytes)
+        return fail(OC_EINVAL, "staging slots hold less than one chunk object: create the context with a "
+                               "chunkwise-capable delivery");
+
+    // items: every chunkwise request's object groups (as many whole objects as
+    // a slot holds), then the layerwise requests layer-major, request-minor
     std::vector<Item> items;
+    std::vector<int64_t> last_group(n_reqs, -1), item_of((size_t)n_reqs * L, -1);
+    const int64_t per_group = n_cw > 0 ? (int64_t)c->slot_bytes / obj_bytes : 1;
+    for (int32_t r = 0; r < n_reqs; ++r) {
+        if (deliv[r] != OC_DELIVERY_CHUNKWISE) continue;
+        const int64_t N = reqs[r].prefix_tokens / l.chunk_tokens;
+        for (int64_t j0 = 0; j0 < N; j0 += per_group) {
+            items.push_back({0, r, true, j0, std::min(N, j0 + per_group)});
+            last_group[r] = (int64_t)items.size() - 1;
+        }
+    }
     for (int32_t layer = 0; layer < L; ++layer)
-        for (int32_t r = 0; r < n_reqs; ++r) items.push_back({layer, r});
+        for (int32_t r = 0; r < n_reqs; ++r)
+            if (deliv[r] == OC_DELIVERY_LAYERWISE) {
+                item_of[(size_t)r * L + layer] = (int64_t)items.size();
+                items.push_back({layer, r});
+            }
     const int64_t n_items = (int64_t)items.size();
 
-    // events: start + landed/ingested/done per item
-    const size_t n_ev = 1 + 3 * (size_t)n_items;
+    // events: start, landed/ingested per item, done per (request, layer)
+    const size_t n_done = (size_t)n_reqs * L;
+    const size_t n_ev = 1 + 2 * (size_t)n_items + n_done;
     while (c->events.size() < n_ev) {
         hipEvent_t e;
         OC_HIP(hipEventCreate(&e));
@@ -549,8 +602,28 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     hipEvent_t ev_start = c->events[0];
     std::vector<hipEvent_t> landed(c->events.begin() + 1, c->events.begin() + 1 + n_items);
     std::vector<hipEvent_t> ingested(c->events.begin() + 1 + n_items, c->events.begin() + 1 + 2 * n_items);
-    std::vector<hipEvent_t> done(c->events.begin() + 1 + 2 * n_items, c->events.begin() + 1 + 3 * n_items);
+    std::vector<hipEvent_t> done(c->events.begin() + 1 + 2 * n_items, c->events.begin() + 1 + 2 * n_items + n_done);
     std::vector<double> produced(n_items, -1.0);
+
+    // one layer's attention of one request on `st`
+    auto enqueue_attention = [&](const oc_request &r, int32_t layer, hipStream_t st) -> hipError_t {
+        AttnPlan p;
+        plan_attention(l, r.prefix_tokens, r.suffix_tokens, &p);
+        AttnArgs a{};
+        const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+        const uint16_t *base = static_cast<const uint16_t *>(c->pool.base);
+        const int64_t q_stride = r.suffix_tokens * l.num_q_heads * l.head_dim;
+        const int64_t kv_stride = r.suffix_tokens * l.num_kv_heads * l.head_dim;
+        a.q = static_cast<const uint16_t *>(r.q) + layer * q_stride;
+        a.k_new = static_cast<const uint16_t *>(r.k_new) + layer * kv_stride;
+        a.v_new = static_cast<const uint16_t *>(r.v_new) + layer * kv_stride;
+        a.out = static_cast<uint16_t *>(r.out) + layer * q_stride;
+        a.pool_k = base + ((int64_t)layer * 2 + 0) * l.num_pages * block;
+        a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
+        a.pages = r.block_table->pages;
+        a.ws = static_cast<unsigned char *>(c->ws);
+        return launch_attention(p, a, st);
+    };
 
     OC_HIP(hipSetDevice(c->device));
     OC_HIP(hipStreamSynchronize(c->copy));
@@ -644,6 +717,53 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         const int64_t layer_bytes = r.prefix_tokens * b_tok;
         const int64_t N = r.prefix_tokens / l.chunk_tokens;
         const void *payload = nullptr;
+        if (it.chunks) {
+            // a group of whole chunk objects: land it, ingest every layer of
+            // it; after the request's last group, all its layers compute
+            {
+                std::unique_lock<std::mutex> lk(sh.mu);
+                const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
+                const bool ok = sh.cv.wait_until(lk, deadline, [&] { return sh.ready > k || sh.producer_status != OC_OK; });
+                if (sh.producer_status != OC_OK) {
+                    status = sh.producer_status;
+                    msg = sh.producer_msg;
+                    break;
+                }
+                if (!ok) {
+                    status = OC_ETIMEOUT;
+                    msg = "chunks " + std::to_string(it.j0) + ".." + std::to_string(it.j1 - 1) + " of request " +
+                          std::to_string(it.req) + " did not arrive within " + std::to_string(c->opts.timeout_ms) +
+                          " ms";
+                    break;
+                }
+            }
+            Slot &s = c->slots[k % c->slots.size()];
+            hipError_t e = hipMemcpyAsync(s.device, s.pinned, (size_t)((it.j1 - it.j0) * obj_bytes),
+                                          hipMemcpyHostToDevice, c->copy);
+            if (e == hipSuccess) e = hipEventRecord(landed[k], c->copy);
+            {
+                std::lock_guard<std::mutex> g(sh.mu);
+                sh.landed_recorded = k + 1;
+            }
+            sh.cv.notify_all();
+            if (e == hipSuccess)
+                e = launch_chunks_ingest(chunks_ingest_args(&c->pool, r.block_table, s.device, it.j0, it.j1 - it.j0),
+                                         c->copy);
+            if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
+            if (e == hipSuccess && k == last_group[it.req]) {
+                e = hipStreamWaitEvent(c->compute, ingested[k], 0);
+                for (int32_t layer = 0; layer < L && e == hipSuccess; ++layer) {
+                    e = enqueue_attention(r, layer, c->compute);
+                    if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + layer], c->compute);
+                }
+            }
+            if (e != hipSuccess) {
+                status = hip_fail(e, "enqueueing a chunk group");
+                msg = oc_last_error();
+                break;
+            }
+            continue;
+        }
         if (by_rate) {
             if (layer_bytes > 0) {
                 const int slot = rprod.slot_of[k];
@@ -736,25 +856,8 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             e = hipEventRecord(landed[k], c->compute);
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->compute);
         }
-        if (e == hipSuccess) {
-            AttnPlan p;
-            plan_attention(l, r.prefix_tokens, r.suffix_tokens, &p);
-            AttnArgs a{};
-            const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
-            const uint16_t *base = static_cast<const uint16_t *>(c->pool.base);
-            const int64_t q_stride = r.suffix_tokens * l.num_q_heads * l.head_dim;
-            const int64_t kv_stride = r.suffix_tokens * l.num_kv_heads * l.head_dim;
-            a.q = static_cast<const uint16_t *>(r.q) + it.layer * q_stride;
-            a.k_new = static_cast<const uint16_t *>(r.k_new) + it.layer * kv_stride;
-            a.v_new = static_cast<const uint16_t *>(r.v_new) + it.layer * kv_stride;
-            a.out = static_cast<uint16_t *>(r.out) + it.layer * q_stride;
-            a.pool_k = base + ((int64_t)it.layer * 2 + 0) * l.num_pages * block;
-            a.pool_v = base + ((int64_t)it.layer * 2 + 1) * l.num_pages * block;
-            a.pages = r.block_table->pages;
-            a.ws = static_cast<unsigned char *>(c->ws);
-            e = launch_attention(p, a, attn_stream);
-        }
-        if (e == hipSuccess) e = hipEventRecord(done[k], attn_stream);
+        if (e == hipSuccess) e = enqueue_attention(r, it.layer, attn_stream);
+        if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + it.layer], attn_stream);
         if (e != hipSuccess) {
             status = hip_fail(e, "enqueueing a layer");
             msg = oc_last_error();
@@ -791,20 +894,22 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     if (e2 != hipSuccess) return hip_fail(e2, "draining the compute stream");
 
     double last = 0.0;
-    for (int64_t k = 0; k < n_items; ++k) {
-        const Item it = items[k];
-        const double t_done = ev_ms(ev_start, done[k]);
-        last = std::max(last, t_done);
-        if (stats) {
-            oc_request_stats &st = stats[it.req];
-            if (it.layer == L - 1) st.ttft_ms = t_done;
-            if (st.produced_ms) st.produced_ms[it.layer] = produced[k];
-            if (st.landed_ms) st.landed_ms[it.layer] = mode == OC_MODE_HBM_RESIDENT ? 0.0 : ev_ms(ev_start, landed[k]);
-            if (st.ingested_ms) st.ingested_ms[it.layer] = ev_ms(ev_start, ingested[k]);
-            if (st.done_ms) st.done_ms[it.layer] = t_done;
-            st.rate_bytes_per_s = req_rate[it.req];
+    for (int32_t r = 0; r < n_reqs; ++r)
+        for (int32_t layer = 0; layer < L; ++layer) {
+            const double t_done = ev_ms(ev_start, done[(size_t)r * L + layer]);
+            last = std::max(last, t_done);
+            if (!stats) continue;
+            // a chunkwise request's layers all became usable with its last group
+            const int64_t k = deliv[r] == OC_DELIVERY_CHUNKWISE ? last_group[r] : item_of[(size_t)r * L + layer];
+            oc_request_stats &st = stats[r];
+            if (layer == L - 1) st.ttft_ms = t_done;
+            if (st.produced_ms) st.produced_ms[layer] = produced[k];
+            if (st.landed_ms) st.landed_ms[layer] = mode == OC_MODE_HBM_RESIDENT ? 0.0 : ev_ms(ev_start, landed[k]);
+            if (st.ingested_ms) st.ingested_ms[layer] = ev_ms(ev_start, ingested[k]);
+            if (st.done_ms) st.done_ms[layer] = t_done;
+            st.rate_bytes_per_s = req_rate[r];
+            st.delivery = deliv[r];
         }
-    }
     c->last_ms = last;
     return OC_OK;
 }
@@ -837,6 +942,11 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
     c->max_prefix = max_prefix_tokens;
     c->max_suffix = max_suffix_tokens;
     c->slot_bytes = (size_t)max_prefix_tokens * 2 * l.num_kv_heads * l.head_dim * 2;
+    if (c->opts.delivery != OC_DELIVERY_LAYERWISE && max_prefix_tokens > 0) {
+        // a slot must hold at least one whole chunk object (L*S bytes)
+        const size_t obj = (size_t)l.num_layers * 2 * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
+        c->slot_bytes = std::max(c->slot_bytes, obj);
+    }
     if (hipSetDevice(device) != hipSuccess) {
         delete c;
         return fail(OC_EHIP, "hipSetDevice failed");

@@ -137,7 +137,7 @@ class RequestSet:
 
     def chunk_rows(self, r):
         # one row per chunk object: the object's L slices back to back
-        return self.objs[r].reshape(self.objs[r].shape[0], -1)
+        return self.objs[r].reshape(self.objs[r].shape[0], self.L * self.slice_elems)
 
     def pool_shape(self):
         return oracle.pool_shape(self.L, self.P, self.nkv, self.Ps, self.d)

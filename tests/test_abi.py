@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert oc.oc_abi_version() == 1
+    assert oc.oc_abi_version() == 2
 
 
 def _layout(**kw):
@@ -71,6 +71,33 @@ def test_ingest_validation():
     # nothing to do is not an error
     assert _ingest(lay, num_chunks=0, table_entries=0, num_tokens=0) == L.OC_OK
     assert oc.lib().oc_kv_layer_ingest(None, None, None, 0, None) == L.OC_EINVAL
+
+
+def _chunks(layout, num_chunks=4, first_chunk=0, slice_bytes=None, table_entries=16, num_tokens=256, data=FAKE,
+            base=FAKE):
+    if slice_bytes is None:
+        slice_bytes = 2 * layout.chunk_tokens * layout.num_kv_heads * layout.head_dim * 2
+    st = L.c_staging(data, num_chunks, slice_bytes)
+    bt = L.c_block_table(FAKE, table_entries, num_tokens)
+    kp = L.c_kv_pool(base, layout)
+    return oc.lib().oc_kv_chunks_ingest(ctypes.byref(st), first_chunk, ctypes.byref(bt), ctypes.byref(kp), None)
+
+
+def test_chunks_ingest_validation():
+    lay = _layout()
+    assert _chunks(lay, slice_bytes=1000) == L.OC_ESHAPE
+    assert _chunks(lay, first_chunk=-1) == L.OC_EINVAL
+    assert _chunks(lay, num_chunks=-1) == L.OC_EINVAL
+    # chunks 13..16 of a 16-chunk (256-token) prefix run past its end
+    assert _chunks(lay, first_chunk=13) == L.OC_ERANGE
+    assert b"past the end" in oc.lib().oc_last_error()
+    assert _chunks(lay, table_entries=15) == L.OC_ERANGE
+    assert _chunks(lay, data=FAKE + 8) == L.OC_EALIGN
+    assert _chunks(lay, base=FAKE + 2) == L.OC_EALIGN
+    assert _chunks(_layout(num_q_heads=3)) == L.OC_ESHAPE
+    # no objects is not an error, wherever they would start
+    assert _chunks(lay, num_chunks=0, first_chunk=16) == L.OC_OK
+    assert oc.lib().oc_kv_chunks_ingest(None, 0, None, None, None) == L.OC_EINVAL
 
 
 def test_attention_validation():

@@ -1,6 +1,7 @@
 """Paper arithmetic: eq. (1) sizes, the element counts of the aggregation
 table, eq. (3) and the overlap requirement of Section 5.3 against the numbers
 the paper prints."""
+import numpy as np
 import pytest
 
 import kvgen
@@ -69,6 +70,22 @@ def test_eq3_limits():
     X, C = [3, 1, 4, 1, 5], [2, 7, 1, 8, 2]
     t = model.layerwise_ttft(X, C)
     assert t >= sum(X) and t >= sum(C)
+
+
+def test_chunkwise_baseline_against_eq3():
+    # one layer: nothing to overlap, both orders take transfer then compute
+    assert model.chunkwise_ttft([2.0], [3.0]) == model.layerwise_ttft([2.0], [3.0]) == 5.0
+    # no compute: both are the transfer time (eq. (3) telescopes to sum X)
+    X = [3.0, 1.0, 4.0, 1.0, 5.0]
+    assert model.layerwise_ttft(X, [0.0] * 5) == pytest.approx(model.chunkwise_ttft(X, [0.0] * 5))
+    # with compute, layerwise overlap saves exactly the hidden part:
+    # chunkwise - layerwise = sum_{l<L-1} min(X_{l+1}, C_l)
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        L = int(rng.integers(1, 12))
+        X, C = list(rng.uniform(0, 5, L)), list(rng.uniform(0, 5, L))
+        saved = sum(min(X[l + 1], C[l]) for l in range(L - 1))
+        assert model.chunkwise_ttft(X, C) - model.layerwise_ttft(X, C) == pytest.approx(saved)
 
 
 def test_eq2_mode_dispatch():

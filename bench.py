@@ -22,6 +22,8 @@ Reported (one JSON line on stdout):
                  capped at 12.5 GB/s (100 Gbps), mean and std over trials
                  after the first
   added_ttft_ms  capped producer minus HBM-resident, beside the eq. (3) floor
+  delivery_sweep layerwise against chunkwise delivery at several producer
+                 rates, beside eq. (3) and the chunkwise closed form
   cpu_baseline   the CPU oracle on a bounded sample, on this host
 
 ``--profile-summary DB...`` turns rocprofv3 output of this script into the
@@ -221,7 +223,42 @@ def ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev):
                "arrival_floor_ms": round(L * layer_bytes / args.cap * 1e3, 3)}
     res["gates"] = {"device_staged_over_hbm": round((ttft["device_staged"][0] - ttft["hbm_resident"][0]) /
                                                     ttft["hbm_resident"][0], 4)}
+    if not args.no_producer and args.sweep_rates:
+        res["delivery_sweep"] = delivery_sweep(oc, wl, layout, pool, reqs, args, ttft["device_staged"][0] / L)
     return ttft, res
+
+
+def chunkwise_floor(X, C):
+    # Section 3.5's chunkwise baseline: every transfer, then every layer's compute
+    return sum(X) + sum(C)
+
+
+def delivery_sweep(oc, wl, layout, pool, reqs, args, c_layer_ms):
+    """Layerwise against chunkwise delivery over a range of producer rates
+    (Section 5's bandwidth sensitivity), each beside its model: eq. (3) for
+    layerwise, all transfers then all compute for chunkwise, X_l = layer bytes
+    / rate, C_l = the measured device-staged time per layer."""
+    L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
+    layer_bytes = sum(wl.prefix_tokens) * b
+    trials = max(2, args.trials // 2)
+    out = []
+    for gbs in [float(x) for x in args.sweep_rates.split(",")]:
+        rate = gbs * 1e9
+        if rate > 0 and L * layer_bytes / rate > args.sweep_max_s:
+            out.append({"rate_GBps": gbs, "skipped": f"over {args.sweep_max_s} s per trial"})
+            continue
+        row = {"rate_GBps": gbs if rate > 0 else "uncapped"}
+        for name in ("layerwise", "chunkwise"):
+            runs = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=rate,
+                            delivery=name)
+            row[f"{name}_ms"] = mean_std(x[0] for x in runs[1:])
+        if rate > 0:
+            X, C = [layer_bytes / rate * 1e3] * L, [c_layer_ms] * L
+            row["eq3_floor_ms"] = round(layerwise_floor(X, C), 3)
+            row["chunkwise_floor_ms"] = round(chunkwise_floor(X, C), 3)
+        out.append(row)
+        log(f"[bench] {wl.name} delivery sweep {gbs} GB/s done")
+    return out
 
 
 def cpu_baseline(wl, objs_all, tables, budget_s):
@@ -504,6 +541,9 @@ def main():
     ap.add_argument("--no-producer", action="store_true", help="skip the producer TTFT modes")
     ap.add_argument("--isolated-passes", type=int, default=2, help="passes of the isolated ingest leg (0: skip)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--sweep-rates", default="1.25,12.5,50,0",
+                    help="producer rates (GB/s, 0 = uncapped) of the layerwise/chunkwise sweep; empty: skip")
+    ap.add_argument("--sweep-max-s", type=float, default=2.0, help="skip sweep rates whose payload takes longer")
     ap.add_argument("--second-workload", default="8b-4k",
                     help="workload whose TTFT legs are reported beside the main one ('' to skip)")
     ap.add_argument("--copy-calibration", action="store_true",

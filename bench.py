@@ -24,6 +24,8 @@ Reported (one JSON line on stdout):
   added_ttft_ms  capped producer minus HBM-resident, beside the eq. (3) floor
   delivery_sweep layerwise against chunkwise delivery at several producer
                  rates, beside eq. (3) and the chunkwise closed form
+  policy_sweep   (--policy-sweep) every bandwidth allocation policy under the
+                 shared cap: per-request TTFT and rate beside eq. (3)
   cpu_baseline   the CPU oracle on a bounded sample, on this host
 
 ``--profile-summary DB...`` turns rocprofv3 output of this script into the
@@ -261,6 +263,103 @@ def delivery_sweep(oc, wl, layout, pool, reqs, args, c_layer_ms):
     return out
 
 
+POLICIES = ["fifo", "equal", "kv_prop", "bw_prop", "stall_opt", "cal_stall_opt"]
+
+
+def policy_sweep(oc, wl, layout, pool, reqs, args, hbm):
+    """Every bandwidth allocation policy on the workload's requests under one
+    shared cap (Section 3.6 and the multi-tenant evaluation): per-request TTFT
+    and allocated rate, the eq. (3) prediction at that rate, and the added
+    TTFT over an uncapped run (the paper's comparison metric).  Compute
+    windows c_i are the measured per-layer attention times of each request."""
+    L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
+    R = len(reqs)
+    trials = max(2, args.trials // 2)
+    c_ms = [float(np.mean([st[r]["done_ms"][l] - st[r]["ingested_ms"][l] for _, st in hbm[1:] for l in range(L)]))
+            for r in range(R)]
+    for r, req in enumerate(reqs):
+        req.layer_compute_s = c_ms[r] / 1e3
+    s_bytes = [wl.prefix_tokens[r] * b for r in range(R)]
+    unc = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=0.0)
+    base = [float(np.mean([st[r]["ttft_ms"] for _, st in unc[1:]])) for r in range(R)]
+    out = {"cap_GBps": args.cap / 1e9, "margin_GBps": args.policy_margin / 1e9,
+           "layer_bytes": s_bytes, "compute_ms_per_layer": [round(c, 4) for c in c_ms],
+           "uncapped_ttft_ms": [round(t, 3) for t in base], "policies": {}}
+    log(f"[bench] policy sweep: uncapped baseline done")
+    for pol in POLICIES:
+        runs = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=args.cap,
+                        alloc_policy=pol, margin_bytes_per_s=args.policy_margin)
+        ttft = [float(np.mean([st[r]["ttft_ms"] for _, st in runs[1:]])) for r in range(R)]
+        rates = [runs[-1][1][r]["rate_bytes_per_s"] for r in range(R)]
+        row = {"ttft_ms": [round(t, 3) for t in ttft], "mean_ttft_ms": round(float(np.mean(ttft)), 3),
+               "max_ttft_ms": round(max(ttft), 3),
+               "added_ttft_ms": round(float(np.mean([t - u for t, u in zip(ttft, base)])), 3)}
+        if pol != "fifo":
+            row["rate_GBps"] = [round(x / 1e9, 4) for x in rates]
+            # eq. (3) per request at its own rate for the whole run
+            row["eq3_ms"] = [round(layerwise_floor([s_bytes[r] / rates[r] * 1e3] * L, [c_ms[r]] * L), 3)
+                             if rates[r] > 0 else None for r in range(R)]
+        out["policies"][pol] = row
+        log(f"[bench] policy sweep: {pol} done")
+    eq = out["policies"]["equal"]["added_ttft_ms"]
+    for pol in ("stall_opt", "cal_stall_opt"):
+        a = out["policies"][pol]["added_ttft_ms"]
+        out[f"equal_over_{pol}"] = round(eq / a, 3) if a > 0 else None
+    return out
+
+
+def scheduler_workloads(args):
+    """The multi-tenant bandwidth-allocation evaluation: Workloads A/B/C (the
+    paper's request cells, cached tokens and A100 compute windows scaled down
+    together), every policy under the workload's cap with the per-layer
+    compute windows emulated, against an uncapped run.  Reports per-request
+    TTFT, allocated rates, eq. (3) per request, and the added TTFT ratio of
+    Equal to (Calibrated) Stall-opt -- the paper's headline comparison."""
+    # every request computes on a stream of its own; with HIP's default of 4
+    # hardware queues per process the streams would share queues and one
+    # request's window would hold up the others (must be set before HIP starts)
+    os.environ["GPU_MAX_HW_QUEUES"] = "16"
+    import torch
+    import kvgen
+    import paper_2605_22850_amd as oc
+    torch.cuda.set_device(0)
+    out = {}
+    for name in args.scheduler_workloads.split(","):
+        wl, windows, cap = kvgen.scheduler_workload(name, scale=args.scheduler_scale)
+        layout, pool, reqs, _, _ = setup(wl)
+        L, b, R = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2, wl.n_requests
+        for req, w in zip(reqs, windows):
+            req.layer_compute_s = w
+        s_bytes = [t * b for t in wl.prefix_tokens]
+        trials = max(2, args.trials // 2)
+        kw = dict(emulate_compute=True, slots=2 * R, piece_bytes=1 << 20)
+        unc = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=0.0, **kw)
+        base = [float(np.mean([st[r]["ttft_ms"] for _, st in unc[1:]])) for r in range(R)]
+        res = {"cap_Gbps": cap * 8 / 1e9, "scale": args.scheduler_scale, "cached_tokens": wl.prefix_tokens,
+               "window_ms": [round(w * 1e3, 3) for w in windows], "uncapped_ttft_ms": [round(t, 2) for t in base],
+               "policies": {}}
+        for pol in POLICIES[1:]:
+            runs = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=cap,
+                            alloc_policy=pol, margin_bytes_per_s=args.policy_margin, **kw)
+            ttft = [float(np.mean([st[r]["ttft_ms"] for _, st in runs[1:]])) for r in range(R)]
+            rates = [runs[-1][1][r]["rate_bytes_per_s"] for r in range(R)]
+            res["policies"][pol] = {
+                "rate_Gbps": [round(x * 8 / 1e9, 2) for x in rates],
+                "ttft_ms": [round(t, 2) for t in ttft],
+                "eq3_ms": [round(layerwise_floor([s_bytes[r] / rates[r] * 1e3] * L, [windows[r] * 1e3] * L), 2)
+                           for r in range(R)],
+                "added_ttft_ms": round(float(sum(t - u for t, u in zip(ttft, base))), 2)}
+            log(f"[bench] scheduler workload {name}: {pol} done")
+        eq = res["policies"]["equal"]["added_ttft_ms"]
+        for pol in ("stall_opt", "cal_stall_opt"):
+            a = res["policies"][pol]["added_ttft_ms"]
+            res[f"equal_over_{pol}"] = round(eq / a, 3) if a > 0 else None
+        out[name] = res
+        del pool, reqs
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl, objs_all, tables, budget_s):
     """The CPU oracle, as it stands, on a bounded sample of the same workload."""
     import oracle
@@ -397,6 +496,8 @@ def run_bench(args):
     }
     line["ttft_ms"], res = ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev)
     line.update(res)
+    if args.policy_sweep:
+        line["policy_sweep"] = policy_sweep(oc, wl, layout, pool, reqs, args, hbm)
     if args.second_workload and args.second_workload != wl.name:
         wl2 = kvgen.workload(args.second_workload)
         del hbm, dev
@@ -544,6 +645,14 @@ def main():
     ap.add_argument("--sweep-rates", default="1.25,12.5,50,0",
                     help="producer rates (GB/s, 0 = uncapped) of the layerwise/chunkwise sweep; empty: skip")
     ap.add_argument("--sweep-max-s", type=float, default=2.0, help="skip sweep rates whose payload takes longer")
+    ap.add_argument("--policy-sweep", action="store_true",
+                    help="run every bandwidth allocation policy under the cap (meant for --workload batch8)")
+    ap.add_argument("--scheduler-workloads", default="",
+                    help="run the multi-tenant scheduler evaluation on these workloads (e.g. A,B,C) instead")
+    ap.add_argument("--scheduler-scale", type=int, default=4,
+                    help="divide the scheduler workloads' cached tokens and compute windows by this")
+    ap.add_argument("--policy-margin", type=float, default=0.625e9,
+                    help="Calibrated Stall-opt margin, bytes/s (0.625e9 = 5 Gbps)")
     ap.add_argument("--second-workload", default="8b-4k",
                     help="workload whose TTFT legs are reported beside the main one ('' to skip)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -556,9 +665,15 @@ def main():
         print(profile_summary(args.profile_summary, args.workload, args.warmup, args.steps))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the path has no cross-GPU part (DESIGN.md describes how it would "
-              "shard); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the path has no cross-GPU part in this build; run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
+    if args.scheduler_workloads:
+        res = scheduler_workloads(args)
+        print(json.dumps({"metric": "added TTFT by bandwidth allocation policy (scheduler workloads)",
+                          "unit": "ms", "higher_is_better": False, "data": "synthetic", "n_gpus": 1,
+                          "scheduler_workloads": res}), flush=True)
+        return
     run_bench(args)
 
 

@@ -233,6 +233,14 @@ typedef struct {
     double margin_bytes_per_s; /* delta of OC_ALLOC_CAL_STALL_OPT                          */
     int32_t delivery;          /* oc_delivery, PRODUCER mode only (other modes: layerwise) */
     double theta_bytes;        /* Theta of OC_DELIVERY_AUTO                                */
+    int32_t emulate_compute;   /* nonzero: each request computes on a stream of its own,
+                                  and after each layer's attention that stream is held
+                                  for the request's layer_compute_s -- a stand-in for the
+                                  rest of the model's per-layer compute, so eq. (3)'s
+                                  window C_l can be set; windows of different requests
+                                  overlap (at most 10 s per layer) as long as their
+                                  streams get hardware queues of their own
+                                  (GPU_MAX_HW_QUEUES >= requests + 2)                      */
 } oc_pipeline_opts;
 
 /* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */
@@ -249,7 +257,8 @@ typedef struct {
     const void *v_new;                    /* device [L][T_s][n_kv][d]                      */
     void *out;                            /* device [L][T_s][n_q][d]                       */
     double layer_compute_s;               /* c_i for the allocation policies (seconds per
-                                             layer); ignored under OC_ALLOC_FIFO            */
+                                             layer), and the emulated window with
+                                             emulate_compute; otherwise ignored             */
 } oc_request;
 
 /* Per-request timings (milliseconds from the start of the run, all on one

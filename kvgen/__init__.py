@@ -226,3 +226,40 @@ def workload(name: str, seed: Optional[int] = None) -> Workload:
 
 
 WORKLOADS = ["tiny", "8b-4k", "8b-64k", "batch8", "70b-32k"]
+
+
+# ---------------------------------------------------------------------------
+# the multi-tenant scheduler workloads (Section 5's bandwidth-allocation
+# evaluation): requests are cells of the appendix table "Per-layer compute
+# time and required transfer throughput" (Llama 3.1 8B on A100, L = 32,
+# 4096 B per token per layer): (context, hit rate) -> cached tokens and the
+# measured per-layer compute time in ms.  Workloads A and B hold the 16K and
+# 64K cells at 50 % and 87.5 % under 80 and 50 Gbps caps; C adds the 32K
+# cells under 50 Gbps.  `scale` divides cached tokens and compute windows
+# alike, so every request keeps its transfer/compute ratio at the same caps.
+# ---------------------------------------------------------------------------
+
+SCHEDULER_CELLS = {
+    (16384, 0.5): (8192, 29.87), (16384, 0.875): (14336, 8.80),
+    (32768, 0.5): (16384, 80.91), (32768, 0.875): (28672, 23.85),
+    (65536, 0.5): (32768, 271.02), (65536, 0.875): (57344, 75.75),
+}
+SCHEDULER_WORKLOADS = {
+    "A": (10.0e9, [(16384, 0.5), (16384, 0.875), (65536, 0.5), (65536, 0.875)]),
+    "B": (6.25e9, [(16384, 0.5), (16384, 0.875), (65536, 0.5), (65536, 0.875)]),
+    "C": (6.25e9, [(16384, 0.5), (16384, 0.875), (32768, 0.5), (32768, 0.875), (65536, 0.5), (65536, 0.875)]),
+}
+
+
+def scheduler_workload(name: str, scale: int = 4, suffix: int = 128, seed: int = 6):
+    """Workload `name` of the scheduler evaluation on the Llama-3-8B shape:
+    (Workload, per-request compute window in seconds per layer, cap in bytes/s)."""
+    cap, cells = SCHEDULER_WORKLOADS[name]
+    tps = [SCHEDULER_CELLS[c][0] // scale for c in cells]
+    windows = [SCHEDULER_CELLS[c][1] / scale / 1e3 for c in cells]
+    need = sum(-(-t // 16) for t in tps)
+    wl = Workload(name=f"sched-{name}", num_layers=32, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                  page_size=16, chunk_tokens=16, prefix_tokens=tps, suffix_tokens=[suffix] * len(tps),
+                  pool_pages=4 * need, seed=seed, rate_bytes_per_s=cap,
+                  description=f"scheduler workload {name}: cells {cells}, cached tokens and windows / {scale}")
+    return wl, windows, cap

@@ -60,7 +60,8 @@ class c_pipeline_opts(ctypes.Structure):
     _fields_ = [("mode", c_int32), ("rate_bytes_per_s", c_double), ("piece_bytes", c_int64),
                 ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
                 ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
-                ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double)]
+                ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double),
+                ("emulate_compute", c_int32)]
 
 
 class c_request(ctypes.Structure):
@@ -246,11 +247,11 @@ def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, m
                       rate_bytes_per_s: float = 0.0, piece_bytes: int = 0, slots: int = 0,
                       producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
                       fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0,
-                      delivery="layerwise", theta_bytes: float = 0.0):
+                      delivery="layerwise", theta_bytes: float = 0.0, emulate_compute: bool = False):
     pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
     dv = DELIVERIES[delivery] if isinstance(delivery, str) else int(delivery)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
-                           fault_layer, pol, margin_bytes_per_s, dv, theta_bytes)
+                           fault_layer, pol, margin_bytes_per_s, dv, theta_bytes, int(bool(emulate_compute)))
     kp = make_pool(pool, layout)
     ctx = c_void_p()
     _check(lib().oc_context_create(device, ctypes.byref(kp), ctypes.byref(opts), max_prefix_tokens,

@@ -55,6 +55,11 @@ IngestArgs chunks_ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, 
                               int64_t first_chunk, int64_t num_chunks);
 hipError_t launch_gather(IngestArgs a, uint16_t *staging_out, int64_t n_pages_used, hipStream_t s);
 
+// ---- emulated compute window ---------------------------------------------------
+// holds stream `s` for `seconds` (at most OC_MAX_WINDOW_S, checked by callers)
+hipError_t launch_compute_window(double seconds, hipStream_t s);
+constexpr double OC_MAX_WINDOW_S = 10.0;
+
 // ---- attention --------------------------------------------------------------
 struct AttnPlan {
     int64_t Tp, Ts;

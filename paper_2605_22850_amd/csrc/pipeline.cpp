@@ -41,6 +41,7 @@ struct Context {
     int64_t max_prefix = 0, max_suffix = 0;
     size_t slot_bytes = 0;
     hipStream_t copy = nullptr, compute = nullptr;
+    std::vector<hipStream_t> req_streams;   // per-request compute streams (emulated compute windows)
     std::vector<Slot> slots;
     void *ws = nullptr;
     size_t ws_bytes = 0;
@@ -96,6 +97,7 @@ static void release(Context *c) {
     if (!c) return;
     if (c->copy) hipStreamSynchronize(c->copy);
     if (c->compute) hipStreamSynchronize(c->compute);
+    for (auto st : c->req_streams) hipStreamSynchronize(st);
     for (auto &s : c->slots) {
         if (s.pinned) hipHostFree(s.pinned);
         if (s.device) hipFree(s.device);
@@ -105,6 +107,7 @@ static void release(Context *c) {
     if (c->ws) hipFree(c->ws);
     if (c->copy) hipStreamDestroy(c->copy);
     if (c->compute) hipStreamDestroy(c->compute);
+    for (auto st : c->req_streams) hipStreamDestroy(st);
     delete c;
 }
 
@@ -263,8 +266,11 @@ struct Producer {
 // Each request is paced by its own clock at its allocated rate for the whole
 // run -- one scheduling epoch: a request that finishes early does not pass
 // its rate on.  The dispatcher hands out payload pieces by weighted deficit
-// round robin (a quantum proportional to the rate per round) to the copy
-// threads, which copy each piece once its release time has come.  A request
+// round robin to the copy threads, which copy each piece once its release
+// time has come.  A request's credit grows with elapsed time at its rate (the
+// weight), not by a fixed amount per round: rounds are uneven in length, and
+// a per-round quantum would hold a slow request below its rate whenever its
+// share of a round is smaller than the round's length times its rate.  A request
 // starts its next layer only when a staging slot is free; its layers are
 // reported to the driver in layer order, and the driver lands whichever
 // layer is reported first, so a slow request does not hold up a fast one.
@@ -391,15 +397,16 @@ struct RateProducer {
         }
         std::vector<int64_t> N(n_reqs), npieces(n_reqs), piece(n_reqs, 0);
         std::vector<int32_t> layer(n_reqs, 0);
-        std::vector<double> cum(n_reqs, 0.0), deficit(n_reqs, 0.0), quantum(n_reqs, 0.0);
-        double max_rate = 0.0;
-        for (int32_t r = 0; r < n_reqs; ++r) max_rate = std::max(max_rate, rate[r]);
+        const double lookahead_s = 0.004;   // hand out pieces due within this window
+        // credit cap: two pieces beyond what the look-ahead window releases
+        std::vector<double> cum(n_reqs, 0.0), deficit(n_reqs, 0.0), credit_cap(n_reqs, 0.0);
         {
             std::lock_guard<std::mutex> g(wmu);
             for (int32_t r = 0; r < n_reqs; ++r) {
                 N[r] = reqs[r].prefix_tokens / c->pool.layout.chunk_tokens;
                 npieces[r] = (N[r] + cpp - 1) / cpp;
-                quantum[r] = max_rate > 0 ? (double)(cpp * S) * rate[r] / max_rate : 0.0;
+                credit_cap[r] = 2.0 * (double)(cpp * S) + rate[r] * lookahead_s;
+                deficit[r] = credit_cap[r];
                 for (int32_t l = 0; l < L; ++l) pieces_left[item_of(l, r)] = npieces[r];
                 if (N[r] == 0) {            // nothing to deliver: every layer is ready now
                     for (int32_t l = 0; l < L; ++l) complete[item_of(l, r)] = 1;
@@ -411,9 +418,11 @@ struct RateProducer {
         const int nw = c->opts.producer_threads;
         std::vector<std::thread> pool;
         for (int i = 0; i < nw; ++i) pool.emplace_back([this] { worker(); });
-        const double lookahead_s = 0.004;   // hand out pieces due within this window
         bool failed = false;
+        double last_round = now_s();
         for (;;) {
+            const double round_start = now_s(), dt = round_start - last_round;
+            last_round = round_start;
             if (aborted()) {
                 failed = true;
                 break;
@@ -432,7 +441,7 @@ struct RateProducer {
                     failed = true;
                     break;
                 }
-                deficit[r] = std::min(deficit[r] + quantum[r], 2.0 * (double)(cpp * S));
+                deficit[r] = std::min(deficit[r] + rate[r] * dt, credit_cap[r]);
                 while (layer[r] < L) {
                     const int64_t j0 = piece[r] * cpp, j1 = std::min(N[r], j0 + cpp);
                     const double bytes = (double)(j1 - j0) * S;
@@ -563,6 +572,18 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 ++n_cw;
             }
         }
+    const bool emu = c->opts.emulate_compute != 0;
+    if (emu)
+        for (int32_t r = 0; r < n_reqs; ++r)
+            if (!(reqs[r].layer_compute_s >= 0.0) || reqs[r].layer_compute_s > OC_MAX_WINDOW_S)
+                return fail(OC_EINVAL, "emulated compute window must be in [0, 10] seconds");
+    // the stream each request's attention (and emulated window) runs on
+    while (emu && (int32_t)c->req_streams.size() < n_reqs) {
+        hipStream_t st;
+        OC_HIP(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));   // default priority
+        c->req_streams.push_back(st);
+    }
+    auto stream_of = [&](int32_t r) { return emu ? c->req_streams[r] : c->compute; };
     if (n_cw > 0 && c->opts.alloc_policy != OC_ALLOC_FIFO)
         return fail(OC_EINVAL, "a request falls on the chunkwise side of theta_bytes, and allocation policies "
                                "schedule layerwise requests only (use OC_ALLOC_FIFO)");
@@ -634,6 +655,8 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     OC_HIP(hipEventRecord(c->caller_done, nullptr));
     OC_HIP(hipStreamWaitEvent(c->copy, c->caller_done, 0));
     OC_HIP(hipStreamWaitEvent(c->compute, c->caller_done, 0));
+    if (emu)
+        for (int32_t r = 0; r < n_reqs; ++r) OC_HIP(hipStreamWaitEvent(c->req_streams[r], c->caller_done, 0));
 
     // per-request rates under the shared budget (allocation policies)
     const bool by_rate = mode == OC_MODE_PRODUCER && c->opts.alloc_policy != OC_ALLOC_FIFO;
@@ -663,6 +686,8 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     const hipStream_t first = mode == OC_MODE_HBM_RESIDENT ? c->compute : c->copy;
     OC_HIP(hipEventRecord(ev_start, first));
     if (mode != OC_MODE_HBM_RESIDENT) OC_HIP(hipStreamWaitEvent(c->compute, ev_start, 0));
+    if (emu)
+        for (int32_t r = 0; r < n_reqs; ++r) OC_HIP(hipStreamWaitEvent(c->req_streams[r], ev_start, 0));
     const Clock::time_point t0 = Clock::now();
 
     if (by_rate) {
@@ -751,10 +776,12 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                                          c->copy);
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
             if (e == hipSuccess && k == last_group[it.req]) {
-                e = hipStreamWaitEvent(c->compute, ingested[k], 0);
+                const hipStream_t cs = stream_of(it.req);
+                e = hipStreamWaitEvent(cs, ingested[k], 0);
                 for (int32_t layer = 0; layer < L && e == hipSuccess; ++layer) {
-                    e = enqueue_attention(r, layer, c->compute);
-                    if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + layer], c->compute);
+                    e = enqueue_attention(r, layer, cs);
+                    if (e == hipSuccess && emu) e = launch_compute_window(r.layer_compute_s, cs);
+                    if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + layer], cs);
                 }
             }
             if (e != hipSuccess) {
@@ -831,7 +858,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             }
         }
         hipError_t e = hipSuccess;
-        hipStream_t attn_stream = c->compute;
+        hipStream_t attn_stream = stream_of(it.req);
         if (mode != OC_MODE_HBM_RESIDENT) {
             if (N > 0) {
                 oc_kv_pool pool = c->pool;
@@ -851,12 +878,13 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy, step > 0);
             }
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
-            if (e == hipSuccess) e = hipStreamWaitEvent(c->compute, ingested[k], 0);
+            if (e == hipSuccess) e = hipStreamWaitEvent(attn_stream, ingested[k], 0);
         } else {
-            e = hipEventRecord(landed[k], c->compute);
-            if (e == hipSuccess) e = hipEventRecord(ingested[k], c->compute);
+            e = hipEventRecord(landed[k], attn_stream);
+            if (e == hipSuccess) e = hipEventRecord(ingested[k], attn_stream);
         }
         if (e == hipSuccess) e = enqueue_attention(r, it.layer, attn_stream);
+        if (e == hipSuccess && emu) e = launch_compute_window(r.layer_compute_s, attn_stream);
         if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + it.layer], attn_stream);
         if (e != hipSuccess) {
             status = hip_fail(e, "enqueueing a layer");
@@ -889,6 +917,10 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     }
     hipError_t e1 = hipStreamSynchronize(c->copy);
     hipError_t e2 = hipStreamSynchronize(c->compute);
+    for (int32_t r = 0; emu && r < n_reqs; ++r) {
+        const hipError_t e3 = hipStreamSynchronize(c->req_streams[r]);
+        if (e2 == hipSuccess) e2 = e3;
+    }
     if (status != OC_OK) return fail(status, msg);
     if (e1 != hipSuccess) return hip_fail(e1, "draining the copy stream");
     if (e2 != hipSuccess) return hip_fail(e2, "draining the compute stream");

@@ -265,3 +265,38 @@ def test_llama8b_4k_capped_pipeline():
     for l in (0, 31):
         assert_attention_close(out[l][rows], rs.expected_out(0, l, rows=rows), f"layer {l}")
     print(f"  ttft {st['ttft_ms']:.1f} ms (arrival floor {total / 12.5e9 * 1e3:.1f} ms)", flush=True)
+
+
+def test_emulated_compute_windows_follow_eq3():
+    # a stand-in for the rest of the model's per-layer compute: with a window
+    # C per layer and a transfer X per layer the run takes eq. (3)'s
+    # X_0 + sum max(X, C) + C; two requests' windows overlap on their own
+    # streams; the data path is unchanged
+    import oracle.model as model
+    import paper_2605_22850_amd as oc
+    print("[pipeline] emulated compute windows", flush=True)
+    rs = RequestSet(4, 4, 2, 64, [256], [16], 64, seed=4).upload(with_payload=True)
+    want = rs.expected_pool()
+    rs.reqs[0].layer_compute_s = 0.005
+    st = _run(rs, oc.OC_MODE_DEVICE_STAGED, emulate_compute=True)[0]
+    assert 4 * 5.0 <= st["ttft_ms"] <= 4 * 5.0 + 4.0, st["ttft_ms"]
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want)
+    for l in range(rs.L):
+        assert_attention_close(from_dev(rs.reqs[0].out)[l], rs.expected_out(0, l), f"layer {l}")
+    # transfer-bound then compute-bound, against eq. (3)
+    layer_bytes = 256 * 2 * 2 * 64 * 2
+    for x_ms, c_ms in ((8.0, 3.0), (2.0, 6.0)):
+        rs.reqs[0].layer_compute_s = c_ms / 1e3
+        st = _run(rs, oc.OC_MODE_PRODUCER, emulate_compute=True, rate_bytes_per_s=layer_bytes / (x_ms / 1e3),
+                  piece_bytes=4096)[0]
+        want_ms = model.layerwise_ttft([x_ms] * 4, [c_ms] * 4)
+        assert want_ms * 0.97 <= st["ttft_ms"] <= want_ms * 1.15 + 1.0, (x_ms, c_ms, st["ttft_ms"], want_ms)
+    # two requests' windows overlap
+    rs2 = RequestSet(4, 4, 2, 64, [256, 128], [16, 8], 64, seed=5).upload(with_payload=True)
+    for r in rs2.reqs:
+        r.layer_compute_s = 0.005
+    stats = _run(rs2, oc.OC_MODE_DEVICE_STAGED, emulate_compute=True)
+    assert max(s["ttft_ms"] for s in stats) <= 4 * 5.0 + 6.0, [s["ttft_ms"] for s in stats]
+    rs2.reqs[0].layer_compute_s = 11.0
+    with pytest.raises(oc.OcError):
+        _run(rs2, oc.OC_MODE_DEVICE_STAGED, emulate_compute=True)

@@ -48,6 +48,10 @@ def _load():
         lib.oco_ingest_layer.restype = ctypes.c_int
         lib.oco_gather_layer.argtypes = [P, I64, I32, P, I64, I64, I32, I32, I32, I32, P]
         lib.oco_gather_layer.restype = ctypes.c_int
+        lib.oco_append_suffix.argtypes = [P, P, I64, I32, I32, I32, P, I64, I64, P, I64, I32]
+        lib.oco_append_suffix.restype = ctypes.c_int
+        lib.oco_gather_chunks.argtypes = [P, I64, I32, P, I64, I64, I64, I32, I32, I32, I32, P]
+        lib.oco_gather_chunks.restype = ctypes.c_int
         lib.oco_attention.argtypes = [P, P, P, P, P, I64, I64, I32, I32, I32, P, I64, P, I32]
         lib.oco_attention.restype = ctypes.c_int
         _lib = lib
@@ -121,6 +125,39 @@ def gather_layer(pool: np.ndarray, layer: int, table: np.ndarray, n_chunks: int,
     out = np.empty(n_chunks * 2 * G * n_kv * d, dtype=np.uint16)
     rc = lib.oco_gather_layer(_ptr(pool), pool.shape[2], layer, _ptr(table), table.size, n_chunks,
                               G, n_kv, d, Ps, _ptr(out))
+    if rc != 0:
+        raise ValueError("block table entry out of range or too short")
+    return out
+
+
+def append_suffix(k_new: np.ndarray, v_new: np.ndarray, token0: int, table: np.ndarray, pool: np.ndarray,
+                  layer: int, Ps: int) -> None:
+    """Write one layer's suffix K/V ([T_s][n_kv][d] each) into ``pool`` at
+    logical positions token0 .. token0+T_s-1, in place."""
+    lib = _load()
+    k_new, v_new = _u16(k_new), _u16(v_new)
+    if k_new.shape != v_new.shape or k_new.ndim != 3:
+        raise ValueError("k_new and v_new must both be [T_s][n_kv][d]")
+    Ts, n_kv, d = k_new.shape
+    table = np.ascontiguousarray(table, dtype=np.int32)
+    if not pool.flags["C_CONTIGUOUS"] or pool.dtype != np.uint16:
+        raise ValueError("pool must be contiguous uint16")
+    rc = lib.oco_append_suffix(_ptr(k_new), _ptr(v_new), Ts, n_kv, d, Ps, _ptr(table), table.size, token0,
+                               _ptr(pool), pool.shape[2], layer)
+    if rc != 0:
+        raise ValueError("block table entry out of range or too short")
+
+
+def gather_chunks(pool: np.ndarray, table: np.ndarray, first_chunk: int, n_chunks: int, G: int, n_kv: int,
+                  d: int, Ps: int) -> np.ndarray:
+    """Chunk objects first_chunk .. first_chunk+n_chunks-1 rebuilt from the pool,
+    all layers: uint16 [n_chunks][L*2*G*n_kv*d]."""
+    lib = _load()
+    table = np.ascontiguousarray(table, dtype=np.int32)
+    L = pool.shape[0]
+    out = np.empty((n_chunks, L * 2 * G * n_kv * d), dtype=np.uint16)
+    rc = lib.oco_gather_chunks(_ptr(pool), pool.shape[2], L, _ptr(table), table.size, first_chunk, n_chunks,
+                               G, n_kv, d, Ps, _ptr(out))
     if rc != 0:
         raise ValueError("block table entry out of range or too short")
     return out

@@ -12,7 +12,9 @@
  *     hidden dimension (head-major, then head dim) innermost (Section 3.3,
  *     KV_L2TD in Section 3.3; per-layer slice size S of eq. (1));
  *   - paged-pool scatter and gather, one element at a time, through the block
- *     table (the vLLM paged substrate the serving node builds on);
+ *     table (the vLLM paged substrate the serving node builds on), and the
+ *     write path: the suffix's K/V appended behind the prefix, and whole
+ *     chunk objects rebuilt from the pool for offload;
  *   - suffix-prefill GQA attention in float64 over the logical, un-paged keys:
  *     softmax of scaled dot products, each suffix token seeing every cached
  *     prefix token and the suffix tokens up to itself.
@@ -113,6 +115,55 @@ int oco_gather_layer(const uint16_t *pool, int64_t P, int32_t layer, const int32
                         staging[j * slice + l2td_index(0, m, t, h, e, G, n_kv, d)] =
                             pool[pool_index(layer, m, page, h, (int32_t)(T % Ps), e, P, n_kv, Ps, d)];
                     }
+    return 0;
+}
+
+/* Suffix append (the prefill node materialising the full KV state, Section 3
+ * opening): suffix token i of one layer, K and V given dense [T_s][n_kv][d],
+ * is written to logical position T = token0 + i, i.e. page table[T / Ps],
+ * slot T % Ps -- the same paging rule as the prefix.  Returns 0, or -1 when a
+ * table entry is missing or outside [0, P). */
+int oco_append_suffix(const uint16_t *k_new, const uint16_t *v_new, int64_t Ts, int32_t n_kv, int32_t d,
+                      int32_t Ps, const int32_t *table, int64_t table_len, int64_t token0, uint16_t *pool,
+                      int64_t P, int32_t layer) {
+    for (int32_t m = 0; m < 2; ++m)
+        for (int64_t i = 0; i < Ts; ++i)
+            for (int32_t h = 0; h < n_kv; ++h)
+                for (int32_t e = 0; e < d; ++e) {
+                    int64_t T = token0 + i;
+                    int64_t q = T / Ps;
+                    if (q >= table_len) return -1;
+                    int64_t page = table[q];
+                    if (page < 0 || page >= P) return -1;
+                    const uint16_t *src = m == 0 ? k_new : v_new;
+                    pool[pool_index(layer, m, page, h, (int32_t)(T % Ps), e, P, n_kv, Ps, d)] =
+                        src[(i * n_kv + h) * d + e];
+                }
+    return 0;
+}
+
+/* Offload (write-back of newly produced chunks, Section 3 opening): rebuild
+ * chunk objects first_chunk .. first_chunk+n_chunks-1 from the pool, every
+ * layer, in KV_L2TD order; object j is written at objects + j*L*2*G*n_kv*d.
+ * Returns 0, or -1 when a table entry is missing or outside [0, P). */
+int oco_gather_chunks(const uint16_t *pool, int64_t P, int32_t L, const int32_t *table, int64_t table_len,
+                      int64_t first_chunk, int64_t n_chunks, int32_t G, int32_t n_kv, int32_t d, int32_t Ps,
+                      uint16_t *objects) {
+    int64_t obj_elems = (int64_t)L * 2 * G * n_kv * d;
+    for (int64_t j = 0; j < n_chunks; ++j)
+        for (int32_t l = 0; l < L; ++l)
+            for (int32_t m = 0; m < 2; ++m)
+                for (int32_t t = 0; t < G; ++t)
+                    for (int32_t h = 0; h < n_kv; ++h)
+                        for (int32_t e = 0; e < d; ++e) {
+                            int64_t T = (first_chunk + j) * G + t;
+                            int64_t q = T / Ps;
+                            if (q >= table_len) return -1;
+                            int64_t page = table[q];
+                            if (page < 0 || page >= P) return -1;
+                            objects[j * obj_elems + l2td_index(l, m, t, h, e, G, n_kv, d)] =
+                                pool[pool_index(l, m, page, h, (int32_t)(T % Ps), e, P, n_kv, Ps, d)];
+                        }
     return 0;
 }
 

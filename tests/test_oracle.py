@@ -160,6 +160,86 @@ def test_ingest_rejects_out_of_range_page():
 
 
 # ---------------------------------------------------------------------------
+# write path: suffix append and chunk-object offload (Section 3 opening:
+# the prefill node materialises the full KV state; new chunks go back to
+# object storage)
+# ---------------------------------------------------------------------------
+
+def _no_sentinel(rng, shape):
+    x = rand_bf16(rng, shape)
+    x[x == SENTINEL] = 0
+    return x
+
+
+def test_append_puts_each_suffix_token_where_paging_says():
+    # prefix of 40 tokens: the suffix starts mid-page (page 2, slot 8)
+    L, nkv, d, Ps, P, layer, Tp, Ts = 2, 2, 8, 16, 12, 1, 40, 29
+    rng = np.random.default_rng(11)
+    k, v = _no_sentinel(rng, (Ts, nkv, d)), _no_sentinel(rng, (Ts, nkv, d))
+    table = rng.permutation(P)[:-(-(Tp + Ts) // Ps)].astype(np.int32)
+    pool = np.full(oracle.pool_shape(L, P, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+    oracle.append_suffix(k, v, Tp, table, pool, layer, Ps)
+    for i in range(Ts):
+        T = Tp + i
+        page, slot = table[T // Ps], T % Ps
+        for h in range(nkv):
+            assert np.array_equal(pool[layer, 0, page, h].reshape(Ps, d)[slot], k[i, h])
+            assert np.array_equal(pool[layer, 1, page, h].reshape(Ps, d)[slot], v[i, h])
+    # exactly the suffix rows were written: nothing of the prefix, no other layer
+    assert (pool != SENTINEL).sum() == 2 * Ts * nkv * d
+    assert (pool[0] == SENTINEL).all()
+    first = pool[layer, :, table[Tp // Ps]].reshape(2, nkv, Ps, d)
+    assert (first[:, :, :Tp % Ps] == SENTINEL).all()
+
+
+def test_append_rejects_a_table_too_short_for_the_suffix():
+    pool = np.zeros(oracle.pool_shape(1, 4, 1, 16, 8), dtype=np.uint16)
+    kv = np.zeros((9, 1, 8), np.uint16)
+    with pytest.raises(ValueError):       # tokens 8..16 need a second page
+        oracle.append_suffix(kv, kv, 8, np.array([2], np.int32), pool, 0, 16)
+
+
+@pytest.mark.parametrize("G,Ps", [(32, 16), (16, 16), (8, 16)])
+def test_chunk_gather_inverts_the_scatter_of_every_layer(G, Ps):
+    L, nkv, d, N, P = 3, 2, 8, 5, 24
+    rng = np.random.default_rng(G)
+    objs = np.stack([rand_bf16(rng, L * 2 * G * nkv * d) for _ in range(N)])
+    table = rng.permutation(P)[:-(-N * G // Ps)].astype(np.int32)
+    pool = np.zeros(oracle.pool_shape(L, P, nkv, Ps, d), dtype=np.uint16)
+    for layer in range(L):
+        staging = oracle.assemble_layer([o.view(np.uint8) for o in objs], 2 * G * nkv * d * 2, layer)
+        oracle.ingest_layer(staging, N, G, nkv, d, Ps, table, pool, layer)
+    assert np.array_equal(oracle.gather_chunks(pool, table, 0, N, G, nkv, d, Ps), objs)
+    assert np.array_equal(oracle.gather_chunks(pool, table, 1, 2, G, nkv, d, Ps), objs[1:3])
+    assert oracle.gather_chunks(pool, table, 2, 0, G, nkv, d, Ps).shape == (0, L * 2 * G * nkv * d)
+
+
+def test_append_then_offload_gives_the_suffix_chunk_objects():
+    # two prefix chunks, three suffix chunks of G tokens: after the append the
+    # pool holds the full KV state; offloading chunks 2..4 must give objects
+    # whose layer l is K then V of that chunk's suffix tokens (KV_L2TD),
+    # assembled here by plain concatenation
+    L, nkv, d, G, Ps, P = 2, 2, 8, 32, 16, 16
+    n_pre, n_suf = 2, 3
+    Tp, Ts = n_pre * G, n_suf * G
+    rng = np.random.default_rng(5)
+    pre = np.stack([rand_bf16(rng, L * 2 * G * nkv * d) for _ in range(n_pre)])
+    k = [rand_bf16(rng, (Ts, nkv, d)) for _ in range(L)]
+    v = [rand_bf16(rng, (Ts, nkv, d)) for _ in range(L)]
+    table = rng.permutation(P)[:(Tp + Ts) // Ps].astype(np.int32)
+    pool = np.zeros(oracle.pool_shape(L, P, nkv, Ps, d), dtype=np.uint16)
+    for layer in range(L):
+        staging = oracle.assemble_layer([o.view(np.uint8) for o in pre], 2 * G * nkv * d * 2, layer)
+        oracle.ingest_layer(staging, n_pre, G, nkv, d, Ps, table, pool, layer)
+        oracle.append_suffix(k[layer], v[layer], Tp, table, pool, layer, Ps)
+    want = np.stack([np.concatenate([np.concatenate([k[l][s * G:(s + 1) * G].ravel(),
+                                                     v[l][s * G:(s + 1) * G].ravel()]) for l in range(L)])
+                     for s in range(n_suf)])
+    assert np.array_equal(oracle.gather_chunks(pool, table, n_pre, n_suf, G, nkv, d, Ps), want)
+    assert np.array_equal(oracle.gather_chunks(pool, table, 0, n_pre, G, nkv, d, Ps), pre)
+
+
+# ---------------------------------------------------------------------------
 # attention
 # ---------------------------------------------------------------------------
 

@@ -16,6 +16,8 @@ Reported (one JSON line on stdout):
                  null when the kernel source has changed since
   ingest_isolated  the same kernel launched back to back with nothing beside
                  it (kernel capability, not the step)
+  write_path     offload gather of whole chunk objects, suffix append, and
+                 the ingest at 64- and 256-token chunks, each alone
   attention      attention TFLOP/s per layer (HBM-resident pass) against the
                  2.5 PFLOP/s bf16 dense MFMA peak
   ttft_ms        HBM-resident / device-staged / producer uncapped / producer
@@ -198,6 +200,81 @@ def isolated_ingest(oc, wl, layout, pool, reqs, passes):
             "launches": len(evs), "mean_launch_us": round(ms / len(evs) * 1e3, 3),
             "how": f"{passes} passes over all {wl.num_layers} layer payloads ({nbytes / len(evs) / 2**20:.0f} MiB "
                    f"read + written per launch), one stream, nothing beside it"}
+
+
+def _timed(s, evs, fn, nbytes):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    fn()
+    e1.record(s)
+    evs.append((e0, e1, nbytes))
+
+
+def _rate(evs, how):
+    ms = sum(e0.elapsed_time(e1) for e0, e1, _ in evs)
+    nbytes = sum(x for _, _, x in evs)
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"value": round(gbs, 2), "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "launches": len(evs),
+            "mean_launch_us": round(ms / len(evs) * 1e3, 3), "bytes_per_launch": nbytes / len(evs), "how": how}
+
+
+def write_path(oc, wl, layout, pool, reqs, passes):
+    """The write path and the other chunk sizes, each kernel back to back on
+    one stream with nothing beside it, per-launch HIP events:
+      offload_gather   every chunk object of each request rebuilt from the
+                       pool, all layers in one launch (read + write);
+      suffix_append    one layer's suffix K/V appended behind the prefix;
+      ingest_g64/g256  the layer ingest with the payload taken as chunks of
+                       64 / 256 tokens (the paper's other chunk sizes; the
+                       payload bytes are the same, only their order differs).
+    Leaves the pool in an unspecified state."""
+    import torch
+    L, nkv, d, Ps = wl.num_layers, wl.num_kv_heads, wl.head_dim, wl.page_size
+    b = 2 * nkv * d * 2
+    s = torch.cuda.Stream()
+    out = {}
+    with torch.cuda.stream(s):
+        evs = []
+        tp_max = max(wl.prefix_tokens)
+        objs = torch.empty(tp_max * b * L // 2, dtype=torch.int16, device="cuda")
+        for _ in range(passes):
+            for r, rq in enumerate(reqs):
+                tp = wl.prefix_tokens[r]
+                n = tp // wl.chunk_tokens
+                _timed(s, evs, lambda: oc.oc_kv_chunks_gather(rq.pages, tp, pool, layout, 0, n, objs, s),
+                       2.0 * tp * b * L)
+        s.synchronize()
+        del objs
+        out["offload_gather"] = _rate(evs, f"{passes} passes; per request one launch over all {L} layers of "
+                                           f"its chunk objects (read pool + write objects)")
+        # appending needs table room behind the prefix: a table of its own
+        tables = [torch.arange(-(-(tp + ts) // Ps), dtype=torch.int32, device="cuda")
+                  for tp, ts in zip(wl.prefix_tokens, wl.suffix_tokens)]
+        evs = []
+        for _ in range(passes):
+            for l in range(L):
+                for r, rq in enumerate(reqs):
+                    tp, ts = wl.prefix_tokens[r], wl.suffix_tokens[r]
+                    _timed(s, evs, lambda: oc.oc_kv_suffix_append(rq.k_new[l], rq.v_new[l], ts, tables[r], tp, pool,
+                                                                  layout, l, s), 2.0 * ts * b)
+        s.synchronize()
+        out["suffix_append"] = _rate(evs, f"{passes} passes over all {L} layers (read + write of the suffix K/V)")
+        for G in (64, 256):
+            if any(tp % G for tp in wl.prefix_tokens):
+                continue
+            lay = oc.Layout(L, wl.num_q_heads, nkv, d, Ps, G, wl.pool_pages)
+            evs = []
+            for _ in range(passes):
+                for l in range(L):
+                    for r, rq in enumerate(reqs):
+                        tp = wl.prefix_tokens[r]
+                        st = rq.device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]
+                        _timed(s, evs, lambda: oc.oc_kv_layer_ingest(st, tp // G, rq.pages, tp, pool, lay, l, s),
+                               2.0 * tp * b)
+            s.synchronize()
+            out[f"ingest_g{G}"] = _rate(evs, f"{passes} passes over all {L} layer payloads as {G}-token chunks")
+    return out
 
 
 def ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev):
@@ -511,6 +588,8 @@ def run_bench(args):
     if args.isolated_passes > 0:
         line["ingest_isolated"] = isolated_ingest(oc, wl, layout, pool, reqs, args.isolated_passes)
         log("[bench] isolated ingest done")
+        line["write_path"] = write_path(oc, wl, layout, pool, reqs, args.isolated_passes)
+        log("[bench] write path done")
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
         line["cpu_baseline"] = cpu_baseline(wl, objs_all, tables, args.cpu_budget)

@@ -34,7 +34,7 @@
 extern "C" {
 #endif
 
-#define OC_ABI_VERSION 2
+#define OC_ABI_VERSION 3
 
 typedef enum {
     OC_OK = 0,
@@ -132,6 +132,29 @@ int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc
 int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool,
                        int32_t layer, void *staging_out, int64_t num_chunks,
                        int64_t per_layer_chunk_bytes, void *stream);
+
+/* Offload gather (the write-back of chunks to object storage, Section 3
+ * opening, and the inverse of oc_kv_chunks_ingest): rebuild chunk objects
+ * first_chunk .. first_chunk+num_chunks-1 of a request from the pool, every
+ * layer.  objects_out (device, 16-byte aligned, caller-owned) receives them
+ * back to back, each L*S bytes in KV_L2TD order (layer 0's slice, then layer
+ * 1's, ...).  Their tokens must lie inside the table:
+ * (first_chunk+num_chunks)*G <= block_table->num_tokens -- to offload chunks
+ * that hold suffix tokens appended with oc_kv_suffix_append, pass a table
+ * whose num_tokens counts them.  num_chunks == 0 is not an error.
+ * Asynchronous on `stream`. */
+int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int64_t first_chunk,
+                        int64_t num_chunks, void *objects_out, void *stream);
+
+/* Suffix append (the prefill node materialising the full KV state, Section 3
+ * opening): write one layer's suffix K and V (device [suffix_tokens][n_kv][d]
+ * bfloat16 each, 16-byte aligned) into the pool behind the prefix: token i
+ * goes to logical position T_p + i (T_p = block_table->num_tokens), i.e. page
+ * pages[(T_p+i) / page_size], slot (T_p+i) % page_size.  The table must hold
+ * ceil((T_p+suffix_tokens)/page_size) entries.  Prefix slots are not
+ * touched.  suffix_tokens == 0 is not an error.  Asynchronous on `stream`. */
+int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tokens,
+                        const oc_block_table *block_table, oc_kv_pool *kv_pool, int32_t layer, void *stream);
 
 /* Bytes of device workspace oc_suffix_prefill_layer needs for these lengths
  * (at least 256; 0 means the layout or lengths are not supported). */
@@ -241,6 +264,11 @@ typedef struct {
                                   overlap (at most 10 s per layer) as long as their
                                   streams get hardware queues of their own
                                   (GPU_MAX_HW_QUEUES >= requests + 2)                      */
+    int32_t append_suffix;     /* nonzero: after each layer's attention, append that
+                                  layer's suffix K/V into the pool behind the prefix
+                                  (oc_kv_suffix_append), so the run leaves the full KV
+                                  state; every block table must then hold
+                                  ceil((T_p+T_s)/page_size) entries                       */
 } oc_pipeline_opts;
 
 /* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */

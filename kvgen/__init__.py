@@ -20,7 +20,7 @@ from __future__ import annotations
 
 import math
 import threading
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -226,6 +226,14 @@ def workload(name: str, seed: Optional[int] = None) -> Workload:
 
 
 WORKLOADS = ["tiny", "8b-4k", "8b-64k", "batch8", "70b-32k"]
+
+
+def with_chunk_tokens(wl: Workload, G: int) -> Workload:
+    """The same workload stored in chunks of G tokens (every prefix must be a
+    whole number of them); the name gains a "-g<G>" suffix."""
+    if any(t % G for t in wl.prefix_tokens):
+        raise ValueError(f"prefix lengths {wl.prefix_tokens} are not multiples of G={G}")
+    return replace(wl, name=f"{wl.name}-g{G}", chunk_tokens=G)
 
 
 # ---------------------------------------------------------------------------

@@ -26,7 +26,7 @@ DELIVERIES = {"layerwise": 0, "chunkwise": 1, "auto": 2}
 
 EXPORTS = [
     "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest",
-    "oc_kv_layer_gather",
+    "oc_kv_layer_gather", "oc_kv_chunks_gather", "oc_kv_suffix_append",
     "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
     "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate",
 ]
@@ -61,7 +61,7 @@ class c_pipeline_opts(ctypes.Structure):
                 ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
                 ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
                 ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double),
-                ("emulate_compute", c_int32)]
+                ("emulate_compute", c_int32), ("append_suffix", c_int32)]
 
 
 class c_request(ctypes.Structure):
@@ -94,6 +94,10 @@ def lib():
                                           c_void_p]
         L.oc_kv_layer_gather.argtypes = [POINTER(c_block_table), POINTER(c_kv_pool), c_int32, c_void_p, c_int64,
                                          c_int64, c_void_p]
+        L.oc_kv_chunks_gather.argtypes = [POINTER(c_block_table), POINTER(c_kv_pool), c_int64, c_int64, c_void_p,
+                                          c_void_p]
+        L.oc_kv_suffix_append.argtypes = [c_void_p, c_void_p, c_int64, POINTER(c_block_table), POINTER(c_kv_pool),
+                                          c_int32, c_void_p]
         L.oc_attention_workspace_bytes.argtypes = [POINTER(c_layout), c_int64, c_int64]
         L.oc_attention_workspace_bytes.restype = c_size_t
         L.oc_suffix_prefill_layer.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, POINTER(c_kv_pool),
@@ -112,7 +116,8 @@ def lib():
         L.oc_bandwidth_allocate.argtypes = [c_int32, c_int32, POINTER(c_double), POINTER(c_double), c_double, c_double,
                                             POINTER(c_double)]
         for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest", "oc_kv_layer_gather",
-                     "oc_suffix_prefill_layer", "oc_bandwidth_allocate"):
+                     "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_suffix_prefill_layer",
+                     "oc_bandwidth_allocate"):
             getattr(L, name).restype = c_int
         _lib = L
     return _lib
@@ -207,6 +212,24 @@ def oc_kv_layer_gather(pages, num_tokens: int, pool, layout: Layout, layer: int,
                                     layout.slice_bytes, _stream(stream)))
 
 
+def oc_kv_chunks_gather(pages, num_tokens: int, pool, layout: Layout, first_chunk: int, num_chunks: int,
+                        objects_out, stream=None) -> None:
+    """Pool -> chunk objects first_chunk .. first_chunk+num_chunks-1 (all layers) into device objects_out."""
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_kv_chunks_gather(ctypes.byref(bt), ctypes.byref(kp), first_chunk, num_chunks,
+                                     _ptr(objects_out), _stream(stream)))
+
+
+def oc_kv_suffix_append(k_new, v_new, suffix_tokens: int, pages, num_tokens: int, pool, layout: Layout,
+                        layer: int, stream=None) -> None:
+    """One layer's suffix K/V (device [Ts][nkv][d]) -> pool positions num_tokens .. num_tokens+Ts-1."""
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_kv_suffix_append(_ptr(k_new), _ptr(v_new), suffix_tokens, ctypes.byref(bt), ctypes.byref(kp),
+                                     layer, _stream(stream)))
+
+
 def oc_attention_workspace_bytes(layout: Layout, prefix_tokens: int, suffix_tokens: int) -> int:
     lay = layout.c()
     n = lib().oc_attention_workspace_bytes(ctypes.byref(lay), prefix_tokens, suffix_tokens)
@@ -247,11 +270,13 @@ def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, m
                       rate_bytes_per_s: float = 0.0, piece_bytes: int = 0, slots: int = 0,
                       producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
                       fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0,
-                      delivery="layerwise", theta_bytes: float = 0.0, emulate_compute: bool = False):
+                      delivery="layerwise", theta_bytes: float = 0.0, emulate_compute: bool = False,
+                      append_suffix: bool = False):
     pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
     dv = DELIVERIES[delivery] if isinstance(delivery, str) else int(delivery)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
-                           fault_layer, pol, margin_bytes_per_s, dv, theta_bytes, int(bool(emulate_compute)))
+                           fault_layer, pol, margin_bytes_per_s, dv, theta_bytes, int(bool(emulate_compute)),
+                           int(bool(append_suffix)))
     kp = make_pool(pool, layout)
     ctx = c_void_p()
     _check(lib().oc_context_create(device, ctypes.byref(kp), ctypes.byref(opts), max_prefix_tokens,

@@ -74,6 +74,36 @@ IngestArgs chunks_ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, 
     return a;
 }
 
+AppendArgs append_args(const oc_kv_pool *pool, const oc_block_table *bt, int32_t layer, const void *k_new,
+                       const void *v_new, int64_t suffix_tokens) {
+    const oc_layout &l = pool->layout;
+    const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
+    uint16_t *base = static_cast<uint16_t *>(pool->base);
+    AppendArgs a{};
+    a.k_new = static_cast<const uint16_t *>(k_new);
+    a.v_new = static_cast<const uint16_t *>(v_new);
+    a.pool_k = base + ((int64_t)layer * 2 + 0) * l.num_pages * block;
+    a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
+    a.pages = bt->pages;
+    a.num_tokens = suffix_tokens;
+    a.token0 = bt->num_tokens;
+    a.n_kv = l.num_kv_heads;
+    a.d = l.head_dim;
+    a.Ps = l.page_size;
+    return a;
+}
+
+// the table must also hold pages for suffix_tokens tokens behind the prefix
+int check_append_table(const oc_block_table *bt, const oc_layout &l, int64_t suffix_tokens) {
+    const int64_t need = (bt->num_tokens + suffix_tokens + l.page_size - 1) / l.page_size;
+    if (bt->num_entries < need)
+        return fail(OC_ERANGE, "block table needs " + std::to_string(need) +
+                                   " entries to hold the suffix behind the prefix");
+    if (need > l.num_pages) return fail(OC_ERANGE, "prefix and suffix need more pages than the pool has");
+    if (need > 0 && !bt->pages) return fail(OC_EINVAL, "block table pages pointer is NULL");
+    return OC_OK;
+}
+
 static int check_staging_shape(const oc_layout &l, const oc_block_table *bt, int64_t num_chunks,
                                int64_t slice_bytes) {
     const int64_t S = 2LL * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
@@ -171,8 +201,47 @@ int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_p
     if (!aligned(staging_out, 16) || !aligned(kv_pool->base, 16))
         return fail(OC_EALIGN, "staging and pool base must be 16-byte aligned");
     IngestArgs a = ingest_args(kv_pool, block_table, layer, nullptr);
-    const int64_t n_pages = (block_table->num_tokens + l.page_size - 1) / l.page_size;
-    OC_HIP(launch_gather(a, static_cast<uint16_t *>(staging_out), n_pages, static_cast<hipStream_t>(stream)));
+    OC_HIP(launch_gather(a, static_cast<uint16_t *>(staging_out), static_cast<hipStream_t>(stream)));
+    return OC_OK;
+}
+
+int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int64_t first_chunk,
+                        int64_t num_chunks, void *objects_out, void *stream) {
+    clear_error();
+    if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
+    int rc = check_layout(kv_pool->layout);
+    if (rc) return rc;
+    const oc_layout &l = kv_pool->layout;
+    if ((rc = check_table(block_table, l))) return rc;
+    if (first_chunk < 0 || num_chunks < 0) return fail(OC_EINVAL, "negative first_chunk or num_chunks");
+    if ((first_chunk + num_chunks) * l.chunk_tokens > block_table->num_tokens)
+        return fail(OC_ERANGE, "chunks past the end of the block table's tokens");
+    if (num_chunks == 0) return OC_OK;
+    if (!objects_out || !kv_pool->base) return fail(OC_EINVAL, "NULL objects_out or pool base");
+    if (!aligned(objects_out, 16) || !aligned(kv_pool->base, 16))
+        return fail(OC_EALIGN, "objects_out and pool base must be 16-byte aligned");
+    IngestArgs a = chunks_ingest_args(kv_pool, block_table, nullptr, first_chunk, num_chunks);
+    OC_HIP(launch_gather(a, static_cast<uint16_t *>(objects_out), static_cast<hipStream_t>(stream)));
+    return OC_OK;
+}
+
+int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tokens,
+                        const oc_block_table *block_table, oc_kv_pool *kv_pool, int32_t layer, void *stream) {
+    clear_error();
+    if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
+    int rc = check_layout(kv_pool->layout);
+    if (rc) return rc;
+    const oc_layout &l = kv_pool->layout;
+    if ((rc = check_table(block_table, l))) return rc;
+    if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
+    if (suffix_tokens < 0) return fail(OC_EINVAL, "negative suffix_tokens");
+    if ((rc = check_append_table(block_table, l, suffix_tokens))) return rc;
+    if (suffix_tokens == 0) return OC_OK;
+    if (!k_new || !v_new || !kv_pool->base) return fail(OC_EINVAL, "NULL k_new, v_new or pool base");
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(kv_pool->base, 16))
+        return fail(OC_EALIGN, "k_new, v_new and pool base must be 16-byte aligned");
+    AppendArgs a = append_args(kv_pool, block_table, layer, k_new, v_new, suffix_tokens);
+    OC_HIP(launch_append(a, static_cast<hipStream_t>(stream)));
     return OC_OK;
 }
 

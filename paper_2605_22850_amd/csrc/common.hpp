@@ -53,7 +53,27 @@ hipError_t launch_chunks_ingest(IngestArgs a, hipStream_t s);
 // stored back to back as whole objects at `objects`
 IngestArgs chunks_ingest_args(const oc_kv_pool *pool, const oc_block_table *bt, const void *objects,
                               int64_t first_chunk, int64_t num_chunks);
-hipError_t launch_gather(IngestArgs a, uint16_t *staging_out, int64_t n_pages_used, hipStream_t s);
+// the inverse direction, pool -> `out` laid out as the staging would be (a
+// layer payload, or whole chunk objects with n_layers and the steps set)
+hipError_t launch_gather(IngestArgs a, uint16_t *out, hipStream_t s);
+
+// ---- suffix append -------------------------------------------------------------
+struct AppendArgs {
+    const uint16_t *k_new, *v_new;   // [num_tokens][n_kv][d] each
+    uint16_t *pool_k, *pool_v;       // the layer's K and V regions
+    const int32_t *pages;
+    int64_t num_tokens, token0;      // suffix tokens, the first one's logical position
+    int32_t n_kv, d, Ps;
+    // filled by the launcher
+    int64_t region;
+    int32_t d8;
+};
+hipError_t launch_append(AppendArgs a, hipStream_t s);
+// OC_OK when bt also holds pages for suffix_tokens tokens behind its prefix
+int check_append_table(const oc_block_table *bt, const oc_layout &l, int64_t suffix_tokens);
+// arguments for appending `suffix_tokens` tokens of `layer` behind bt->num_tokens
+AppendArgs append_args(const oc_kv_pool *pool, const oc_block_table *bt, int32_t layer, const void *k_new,
+                       const void *v_new, int64_t suffix_tokens);
 
 // ---- emulated compute window ---------------------------------------------------
 // holds stream `s` for `seconds` (at most OC_MAX_WINDOW_S, checked by callers)

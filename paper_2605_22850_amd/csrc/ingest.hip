@@ -14,8 +14,9 @@
 //    ingest wavefronts per SIMD fit: a thread takes 8 slots x one 16-byte
 //    column of one (page, head) block and moves its K rows, then its V rows
 //    (8 loads in flight, one page lookup per 256 bytes moved).
-// The gather (pool -> payload, the inverse) numbers pieces by destination
-// block, two per thread.
+// The gather (pool -> payload or whole chunk objects, the offload direction)
+// numbers pieces the same way, reversed.  The suffix append writes the new
+// tokens' K/V rows behind the prefix through the same block table.
 #include "common.hpp"
 
 namespace oc {
@@ -23,64 +24,6 @@ namespace oc {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-
-// Piece p -> (payload offset, pool offset from the K region base).  With
-// POW2 every divisor (d/8, page size, KV heads, chunk size) is a power of two
-// and the decode is shifts and masks.
-template <bool POW2>
-__device__ inline bool piece_offsets(const IngestArgs &a, int64_t p, int64_t n_units, int64_t &pay, int64_t &pool) {
-    const int d = a.d, nkv = a.n_kv, Ps = a.Ps, G = a.G;
-    int64_t unit, q, T, j, t0;
-    int c, slot, kv, h;
-    if (POW2) {
-        c = (int)(p & (a.d8 - 1));
-        slot = (int)((p >> a.lg_d8) & (Ps - 1));
-        kv = (int)((p >> (a.lg_d8 + a.lg_ps)) & 1);
-        unit = p >> (a.lg_d8 + a.lg_ps + 1);
-        h = (int)(unit & (nkv - 1));
-        q = unit >> a.lg_nkv;
-        T = (q << a.lg_ps) + slot;
-        j = T >> a.lg_g;
-        t0 = T & (G - 1);
-    } else {
-        const int64_t unit_pieces = 2LL * Ps * a.d8;
-        unit = p / unit_pieces;
-        const int pi = (int)(p - unit * unit_pieces);
-        c = pi % a.d8;
-        slot = (pi / a.d8) % Ps;
-        kv = pi / (a.d8 * Ps);
-        q = unit / nkv;
-        h = (int)(unit - q * nkv);
-        T = q * Ps + slot;
-        j = T / G;
-        t0 = T - j * G;
-    }
-    if (unit >= n_units || T >= a.num_tokens) return false;
-    const int64_t D = (int64_t)nkv * d;
-    pay = ((j * 2 + kv) * G + t0) * D + (int64_t)h * d + c * 8;
-    const int64_t page = a.pages[q];
-    pool = kv * a.region + ((page * nkv + h) * Ps + slot) * (int64_t)d + c * 8;
-    return true;
-}
-
-// FORWARD: payload -> pool (ingest); otherwise pool -> payload (gather).
-template <int U, bool POW2, bool FORWARD>
-__device__ inline void copy_pieces(const IngestArgs &a, uint16_t *payload_out, int64_t n_units) {
-    const int64_t first = (int64_t)blockIdx.x * kThreads * U + threadIdx.x;
-    u32x4 r[U];
-    int64_t keep[U];   // the offset the store needs: pool (ingest) or payload (gather)
-    bool ok[U];
-#pragma unroll
-    for (int i = 0; i < U; ++i) {
-        int64_t pay = 0, pool = 0;
-        ok[i] = piece_offsets<POW2>(a, first + (int64_t)i * kThreads, n_units, pay, pool);
-        if (ok[i]) r[i] = *reinterpret_cast<const u32x4 *>(FORWARD ? a.staging + pay : a.pool_k + pool);
-        keep[i] = FORWARD ? pool : pay;
-    }
-#pragma unroll
-    for (int i = 0; i < U; ++i)
-        if (ok[i]) *reinterpret_cast<u32x4 *>(FORWARD ? a.pool_k + keep[i] : payload_out + keep[i]) = r[i];
-}
 
 // 8 slots x one 16-byte column of one (page, head) block, K then V.
 __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs a, int64_t n_rows8) {
@@ -128,15 +71,13 @@ __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs 
     }
 }
 
-// One 16-byte piece per thread, pieces numbered in payload order
-// ([chunk][K|V][token][head][16-byte column]): every wavefront reads 1 KiB of
-// the payload contiguously and writes 256-byte rows into the (page, head)
-// blocks.  Many short wavefronts keep the most bytes in flight.
-// For whole chunk objects blockIdx.y is the layer.
+// Piece e of a payload numbered in payload order ([chunk][K|V][token][head]
+// [16-byte column]) -> its element offsets in the staging (from `staging`)
+// and in the pool (from `pool_k`), both including the layer step of
+// blockIdx.y.  With POW2 every divisor (d/8, KV heads, chunk size, page size)
+// is a power of two and the decode is shifts and masks.
 template <bool POW2>
-__global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, int64_t n_pieces) {
-    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (e >= n_pieces) return;
+__device__ inline void src_order_piece(const IngestArgs &a, int64_t e, int64_t &stage, int64_t &pool) {
     const int64_t slice_pieces = 2LL * a.G * a.n_kv * a.d8;   // 16-byte pieces per chunk slice
     int c, h, t, kv;
     int64_t j;
@@ -166,15 +107,54 @@ __global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, i
         slot = T - q * a.Ps;
     }
     const int64_t page = a.pages[q];
-    const uint16_t *src = a.staging + blockIdx.y * a.layer_step_staging + j * a.chunk_stride + (e - j * slice_pieces) * 8;
-    uint16_t *pool = a.pool_k + blockIdx.y * a.layer_step_pool + kv * a.region;
-    const u32x4 v = *reinterpret_cast<const u32x4 *>(src);
-    *reinterpret_cast<u32x4 *>(pool + ((page * a.n_kv + h) * a.Ps + slot) * (int64_t)a.d + c * 8) = v;
+    stage = blockIdx.y * a.layer_step_staging + j * a.chunk_stride + (e - j * slice_pieces) * 8;
+    pool = blockIdx.y * a.layer_step_pool + kv * a.region + ((page * a.n_kv + h) * a.Ps + slot) * (int64_t)a.d +
+           c * 8;
 }
 
+// Ingest, one 16-byte piece per thread in payload order: every wavefront
+// reads 1 KiB of the payload contiguously and writes 256-byte rows into the
+// (page, head) blocks.  Many short wavefronts keep the most bytes in flight.
+// For whole chunk objects blockIdx.y is the layer.
 template <bool POW2>
-__global__ __launch_bounds__(kThreads, 8) void kv_gather_kernel(IngestArgs a, uint16_t *payload, int64_t n_units) {
-    copy_pieces<2, POW2, false>(a, payload, n_units);
+__global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, int64_t n_pieces) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= n_pieces) return;
+    int64_t stage, pool;
+    src_order_piece<POW2>(a, e, stage, pool);
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(a.staging + stage);
+    *reinterpret_cast<u32x4 *>(a.pool_k + pool) = v;
+}
+
+// Gather (pool -> layer payload or whole chunk objects, the offload
+// direction): the same numbering, so every wavefront writes 1 KiB of the
+// output contiguously and reads 256-byte pool rows.
+template <bool POW2>
+__global__ __launch_bounds__(kThreads) void kv_gather_src_kernel(IngestArgs a, uint16_t *out, int64_t n_pieces) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= n_pieces) return;
+    int64_t stage, pool;
+    src_order_piece<POW2>(a, e, stage, pool);
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(a.pool_k + pool);
+    *reinterpret_cast<u32x4 *>(out + stage) = v;
+}
+
+// Suffix append: token i of k_new / v_new ([T_s][n_kv][d]; blockIdx.y picks
+// K or V) goes to logical position token0 + i through the block table.
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a, int64_t n_pieces) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= n_pieces) return;
+    const int kv = (int)blockIdx.y;
+    const int64_t r = e / a.d8;
+    const int c = (int)(e - r * a.d8);
+    const int64_t i = r / a.n_kv;
+    const int h = (int)(r - i * a.n_kv);
+    const int64_t T = a.token0 + i;
+    const int64_t q = T / a.Ps, slot = T - q * a.Ps;
+    const int64_t page = a.pages[q];
+    const uint16_t *src = (kv ? a.v_new : a.k_new) + e * 8;
+    uint16_t *dst = a.pool_k + kv * a.region + ((page * a.n_kv + h) * a.Ps + slot) * (int64_t)a.d + c * 8;
+    *reinterpret_cast<u32x4 *>(dst) = *reinterpret_cast<const u32x4 *>(src);
 }
 
 static bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
@@ -227,14 +207,23 @@ hipError_t launch_chunks_ingest(IngestArgs a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_gather(IngestArgs a, uint16_t *payload_out, int64_t n_pages_used, hipStream_t s) {
-    if (n_pages_used == 0) return hipSuccess;
+hipError_t launch_gather(IngestArgs a, uint16_t *out, hipStream_t s) {
+    if (a.num_tokens == 0) return hipSuccess;
     const bool p2 = prepare(a);
-    const int64_t n_units = n_pages_used * a.n_kv;
-    const int64_t n = n_units * 2 * a.Ps * a.d8;
-    const dim3 grid((unsigned)((n + kThreads * 2 - 1) / (kThreads * 2)));
-    if (p2) hipLaunchKernelGGL(kv_gather_kernel<true>, grid, dim3(kThreads), 0, s, a, payload_out, n_units);
-    else hipLaunchKernelGGL(kv_gather_kernel<false>, grid, dim3(kThreads), 0, s, a, payload_out, n_units);
+    const int64_t n = a.num_tokens * 2 * a.n_kv * a.d8;   // 16-byte pieces of one layer
+    const dim3 grid((unsigned)((n + kThreads - 1) / kThreads), (unsigned)a.n_layers);
+    if (p2) hipLaunchKernelGGL(kv_gather_src_kernel<true>, grid, dim3(kThreads), 0, s, a, out, n);
+    else hipLaunchKernelGGL(kv_gather_src_kernel<false>, grid, dim3(kThreads), 0, s, a, out, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_append(AppendArgs a, hipStream_t s) {
+    if (a.num_tokens == 0) return hipSuccess;
+    a.d8 = a.d / 8;
+    a.region = (int64_t)(a.pool_v - a.pool_k);
+    const int64_t n = a.num_tokens * a.n_kv * a.d8;        // 16-byte pieces of K (and of V)
+    const dim3 grid((unsigned)((n + kThreads - 1) / kThreads), 2);
+    hipLaunchKernelGGL(kv_append_kernel, grid, dim3(kThreads), 0, s, a, n);
     return hipGetLastError();
 }
 

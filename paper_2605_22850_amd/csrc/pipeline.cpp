@@ -513,6 +513,8 @@ static int validate_requests(Context *c, const oc_request *reqs, int32_t n) {
         const int64_t need = (r.prefix_tokens + l.page_size - 1) / l.page_size;
         if (r.block_table->num_entries < need) return fail(OC_ERANGE, who + "block table too short");
         if (need > 0 && !r.block_table->pages) return fail(OC_EINVAL, who + "NULL block table pages");
+        if (c->opts.append_suffix && check_append_table(r.block_table, l, r.suffix_tokens) != OC_OK)
+            return fail(OC_ERANGE, who + oc_last_error());
         if (!r.q || !r.k_new || !r.v_new || !r.out) return fail(OC_EINVAL, who + "NULL q/k_new/v_new/out");
         if (!aligned(r.q, 16) || !aligned(r.k_new, 16) || !aligned(r.v_new, 16) || !aligned(r.out, 16))
             return fail(OC_EALIGN, who + "q/k_new/v_new/out must be 16-byte aligned");
@@ -643,7 +645,10 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
         a.pages = r.block_table->pages;
         a.ws = static_cast<unsigned char *>(c->ws);
-        return launch_attention(p, a, st);
+        hipError_t e = launch_attention(p, a, st);
+        if (e == hipSuccess && c->opts.append_suffix)
+            e = launch_append(append_args(&c->pool, r.block_table, layer, a.k_new, a.v_new, r.suffix_tokens), st);
+        return e;
     };
 
     OC_HIP(hipSetDevice(c->device));

@@ -119,14 +119,18 @@ class RequestSet:
     """Several requests sharing one pool, every layer: chunk objects, block
     tables and per-layer suffix tensors, all from kvgen."""
 
-    def __init__(self, L, nq, nkv, d, prefix_tokens, suffix_tokens, pool_pages, seed=1, G=16, Ps=16):
+    def __init__(self, L, nq, nkv, d, prefix_tokens, suffix_tokens, pool_pages, seed=1, G=16, Ps=16,
+                 suffix_room=False):
         from paper_2605_22850_amd import Layout
         self.L, self.nq, self.nkv, self.d, self.G, self.Ps = L, nq, nkv, d, G, Ps
         self.prefix, self.suffix, self.P, self.seed = list(prefix_tokens), list(suffix_tokens), pool_pages, seed
         self.layout = Layout(L, nq, nkv, d, Ps, G, pool_pages)
         self.slice_elems = 2 * G * nkv * d
         self.objs = [kvgen.chunk_objects(seed, r, L, tp // G, self.slice_elems) for r, tp in enumerate(self.prefix)]
-        self.tables = kvgen.block_tables(seed, [-(-tp // Ps) for tp in self.prefix], pool_pages)
+        # with suffix_room the tables also hold the pages the suffix is appended to
+        self.suffix_room = suffix_room
+        self.tables = kvgen.block_tables(seed, [-(-(tp + (ts if suffix_room else 0)) // Ps)
+                                                for tp, ts in zip(self.prefix, self.suffix)], pool_pages)
         self.q, self.k_new, self.v_new = [], [], []
         for r, ts in enumerate(self.suffix):
             self.q.append(np.stack([kvgen.suffix_tensor(seed, kvgen.KIND_Q, r, l, (ts, nq, d)) for l in range(L)]))
@@ -142,9 +146,12 @@ class RequestSet:
     def pool_shape(self):
         return oracle.pool_shape(self.L, self.P, self.nkv, self.Ps, self.d)
 
-    def expected_pool(self, fill=SENTINEL, layers=None):
+    def expected_pool(self, fill=SENTINEL, layers=None, appended=False):
         pool = np.full(self.pool_shape(), fill, dtype=np.uint16)
         for r, tp in enumerate(self.prefix):
+            if appended:
+                for l in (range(self.L) if layers is None else layers):
+                    oracle.append_suffix(self.k_new[r][l], self.v_new[r][l], tp, self.tables[r], pool, l, self.Ps)
             if tp == 0:
                 continue
             chunks = [np.ascontiguousarray(self.objs[r][j]).view(np.uint8).reshape(-1)
@@ -169,7 +176,7 @@ class RequestSet:
                                  dtype=torch.int16, device="cuda")
         self.reqs = []
         for r, (tp, ts) in enumerate(zip(self.prefix, self.suffix)):
-            pages = torch.from_numpy(self.tables[r].copy()).cuda() if tp else None
+            pages = torch.from_numpy(self.tables[r].copy()).cuda() if self.tables[r].size else None
             payload = None
             if with_payload and tp:
                 # layer-major payloads: layer l = every chunk's slice l, in prefix order

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert oc.oc_abi_version() == 2
+    assert oc.oc_abi_version() == 3
 
 
 def _layout(**kw):
@@ -98,6 +98,50 @@ def test_chunks_ingest_validation():
     # no objects is not an error, wherever they would start
     assert _chunks(lay, num_chunks=0, first_chunk=16) == L.OC_OK
     assert oc.lib().oc_kv_chunks_ingest(None, 0, None, None, None) == L.OC_EINVAL
+
+
+def _gather_chunks(layout, first_chunk=0, num_chunks=4, table_entries=16, num_tokens=256, out=FAKE, base=FAKE):
+    bt = L.c_block_table(FAKE, table_entries, num_tokens)
+    kp = L.c_kv_pool(base, layout)
+    return oc.lib().oc_kv_chunks_gather(ctypes.byref(bt), ctypes.byref(kp), first_chunk, num_chunks, out, None)
+
+
+def test_chunks_gather_validation():
+    lay = _layout()
+    assert _gather_chunks(lay, first_chunk=-1) == L.OC_EINVAL
+    assert _gather_chunks(lay, num_chunks=-1) == L.OC_EINVAL
+    assert _gather_chunks(lay, first_chunk=13) == L.OC_ERANGE
+    assert b"past the end" in oc.lib().oc_last_error()
+    assert _gather_chunks(lay, table_entries=15) == L.OC_ERANGE
+    assert _gather_chunks(lay, out=FAKE + 8) == L.OC_EALIGN
+    assert _gather_chunks(lay, base=FAKE + 2) == L.OC_EALIGN
+    assert _gather_chunks(lay, out=None) == L.OC_EINVAL
+    assert _gather_chunks(_layout(head_dim=60)) == L.OC_ESHAPE
+    assert _gather_chunks(lay, num_chunks=0, first_chunk=16) == L.OC_OK
+    assert oc.lib().oc_kv_chunks_gather(None, None, 0, 0, None, None) == L.OC_EINVAL
+
+
+def _append(layout, suffix_tokens=32, table_entries=18, num_tokens=256, layer=0, k=FAKE, v=FAKE, base=FAKE):
+    bt = L.c_block_table(FAKE, table_entries, num_tokens)
+    kp = L.c_kv_pool(base, layout)
+    return oc.lib().oc_kv_suffix_append(k, v, suffix_tokens, ctypes.byref(bt), ctypes.byref(kp), layer, None)
+
+
+def test_suffix_append_validation():
+    lay = _layout()
+    # 256 prefix + 32 suffix tokens need 18 pages of 16
+    assert _append(lay, table_entries=17) == L.OC_ERANGE
+    assert b"18 entries" in oc.lib().oc_last_error()
+    assert _append(lay, suffix_tokens=-1) == L.OC_EINVAL
+    assert _append(lay, layer=2) == L.OC_ERANGE
+    assert _append(lay, k=FAKE + 4) == L.OC_EALIGN
+    assert _append(lay, v=FAKE + 8) == L.OC_EALIGN
+    assert _append(lay, k=None) == L.OC_EINVAL
+    assert _append(_layout(num_pages=17)) == L.OC_ERANGE
+    assert _append(_layout(page_size=12)) == L.OC_ESHAPE
+    # nothing to append is not an error, even with a table that has no room
+    assert _append(lay, suffix_tokens=0, table_entries=16) == L.OC_OK
+    assert oc.lib().oc_kv_suffix_append(None, None, 1, None, None, 0, None) == L.OC_EINVAL
 
 
 def test_attention_validation():

@@ -1,9 +1,12 @@
-"""GPU parity at the five workloads' full sizes, in the kernels' real launch
-configuration: for the first and the last layer of every request, the ingest
-is compared bit for bit over the whole pool (the full page count, 4x the
-pages the prefix needs), and the attention on sampled suffix rows (always
-the first and the last) against the float64 oracle.  The pool holds two
-layers, standing in for layers 0 and L-1."""
+"""GPU parity at the five workloads' full sizes, and at the paper's other
+chunk sizes (G = 64, 256), in the kernels' real launch configuration: for
+the first and the last layer of every request, the ingest and the suffix
+append are compared bit for bit over the whole pool (the full page count,
+4x the pages the prefix needs), every whole chunk of prefix and suffix is
+offloaded back into chunk objects and compared with the stored ones, and the
+attention is checked on sampled suffix rows (always the first and the last)
+against the float64 oracle.  The pool holds two layers, standing in for
+layers 0 and L-1."""
 import numpy as np
 import pytest
 
@@ -31,35 +34,69 @@ def sample_rows(ts, n=N_ROWS, seed=0):
     return sorted(set([0, ts - 1, *mid.tolist()]))
 
 
-@pytest.mark.timeout(400)
-@pytest.mark.parametrize("name", kvgen.WORKLOADS)
-def test_workload_first_and_last_layer(name):
+def _suffix_chunk_objects(kn, vn, G, n_suf):
+    """Whole suffix chunks as KV_L2TD objects, straight from the dense K/V:
+    object s holds, layer by layer, K then V of tokens s*G .. (s+1)*G-1."""
+    return np.stack([np.concatenate([np.concatenate([k[s * G:(s + 1) * G].ravel(), v[s * G:(s + 1) * G].ravel()])
+                                     for k, v in zip(kn, vn)]) for s in range(n_suf)]) if n_suf else None
+
+
+def check_workload(wl):
+    """Ingest + suffix append of the first and the last layer of every request
+    (whole pool bit for bit), offload of every whole chunk of prefix and
+    suffix (against the generated objects), then attention on sampled rows."""
     import torch
     import paper_2605_22850_amd as oc
-    wl = kvgen.workload(name)
+    name = wl.name
     L, nq, nkv, d, G, Ps = (wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.chunk_tokens,
                             wl.page_size)
     layers = [0, L - 1]
-    print(f"[config] {name}: L={L} nq={nq} nkv={nkv} d={d} prefixes={wl.prefix_tokens} pool={wl.pool_pages}",
-          flush=True)
+    print(f"[config] {name}: L={L} nq={nq} nkv={nkv} d={d} G={G} prefixes={wl.prefix_tokens} "
+          f"pool={wl.pool_pages}", flush=True)
     layout = oc.Layout(2, nq, nkv, d, Ps, G, wl.pool_pages)
-    tables = kvgen.block_tables(wl.seed, [wl.pages_needed(r) for r in range(wl.n_requests)], wl.pool_pages)
+    # tables hold room for the suffix behind the prefix
+    need = [-(-(wl.prefix_tokens[r] + wl.suffix_tokens[r]) // Ps) for r in range(wl.n_requests)]
+    tables = kvgen.block_tables(wl.seed, need, wl.pool_pages)
     pool = torch.full((layout.pool_elems,), int(np.uint16(SENTINEL).view(np.int16)), dtype=torch.int16,
                       device="cuda")
     want_pool = np.full(oracle.pool_shape(2, wl.pool_pages, nkv, Ps, d), SENTINEL, dtype=np.uint16)
-    slices = {}
+    slices, suffix = {}, {}
     for r in range(wl.n_requests):
-        n = wl.n_chunks(r)
+        n, tp, ts = wl.n_chunks(r), wl.prefix_tokens[r], wl.suffix_tokens[r]
         d_table = torch.from_numpy(tables[r]).cuda()
         for li, l in enumerate(layers):
             sl = kvgen.chunk_layer_slices(wl.seed, r, l, n, wl.slice_elems)      # row j = chunk j's slice
             slices[(r, l)] = sl
-            oc.oc_kv_layer_ingest(to_dev(sl.reshape(-1)), n, d_table, wl.prefix_tokens[r], pool, layout, li)
+            oc.oc_kv_layer_ingest(to_dev(sl.reshape(-1)), n, d_table, tp, pool, layout, li)
             oracle.ingest_layer(sl.reshape(-1), n, G, nkv, d, Ps, tables[r], want_pool, li)
+            q = kvgen.suffix_tensor(wl.seed, kvgen.KIND_Q, r, l, (ts, nq, d))
+            kn = kvgen.suffix_tensor(wl.seed, kvgen.KIND_KNEW, r, l, (ts, nkv, d))
+            vn = kvgen.suffix_tensor(wl.seed, kvgen.KIND_VNEW, r, l, (ts, nkv, d))
+            suffix[(r, l)] = (q, kn, vn)
+            oc.oc_kv_suffix_append(to_dev(kn), to_dev(vn), ts, d_table, tp, pool, layout, li)
+            oracle.append_suffix(kn, vn, tp, tables[r], want_pool, li, Ps)
     torch.cuda.synchronize()
     got_pool = from_dev(pool).reshape(want_pool.shape)
-    assert np.array_equal(got_pool, want_pool), f"{name}: pool differs from the oracle's scatter"
+    assert np.array_equal(got_pool, want_pool), f"{name}: pool differs from the oracle's scatter + append"
     del got_pool, want_pool
+
+    for r in range(wl.n_requests):
+        n, tp, ts = wl.n_chunks(r), wl.prefix_tokens[r], wl.suffix_tokens[r]
+        n_suf = ts // G
+        total = n + n_suf
+        d_table = torch.from_numpy(tables[r]).cuda()
+        objs = torch.empty(total * 2 * wl.slice_elems, dtype=torch.int16, device="cuda")
+        oc.oc_kv_chunks_gather(d_table, tp + n_suf * G, pool, layout, 0, total, objs)
+        torch.cuda.synchronize()
+        got = from_dev(objs).reshape(total, 2 * wl.slice_elems)
+        assert np.array_equal(got[:n], np.concatenate([slices[(r, l)] for l in layers], axis=1)), \
+            f"{name} request {r}: offloaded prefix chunks differ from the stored objects"
+        if n_suf:
+            want = _suffix_chunk_objects([suffix[(r, l)][1] for l in layers], [suffix[(r, l)][2] for l in layers],
+                                         G, n_suf)
+            assert np.array_equal(got[n:], want), f"{name} request {r}: offloaded suffix chunks differ"
+        print(f"  request {r}: offloaded {n} prefix + {n_suf} suffix chunks", flush=True)
+        del objs, got
 
     for r in range(wl.n_requests):
         tp, ts = wl.prefix_tokens[r], wl.suffix_tokens[r]
@@ -67,9 +104,7 @@ def test_workload_first_and_last_layer(name):
         d_table = torch.from_numpy(tables[r]).cuda()
         ws = torch.empty(oc.oc_attention_workspace_bytes(layout, tp, ts), dtype=torch.uint8, device="cuda")
         for li, l in enumerate(layers):
-            q = kvgen.suffix_tensor(wl.seed, kvgen.KIND_Q, r, l, (ts, nq, d))
-            kn = kvgen.suffix_tensor(wl.seed, kvgen.KIND_KNEW, r, l, (ts, nkv, d))
-            vn = kvgen.suffix_tensor(wl.seed, kvgen.KIND_VNEW, r, l, (ts, nkv, d))
+            q, kn, vn = suffix[(r, l)]
             out = torch.empty((ts, nq, d), dtype=torch.bfloat16, device="cuda")
             oc.oc_suffix_prefill_layer(to_dev(q, "bf16"), to_dev(kn, "bf16"), to_dev(vn, "bf16"), ts, pool, layout,
                                        d_table, tp, li, out, ws)
@@ -79,3 +114,16 @@ def test_workload_first_and_last_layer(name):
             ref = oracle.attention(q, k, v, kn, vn, rows=rows)
             err = assert_attention_close(from_dev(out)[rows], ref, f"{name} request {r} layer {l}")
             print(f"  request {r} layer {l}: rows {len(rows)} max|err| {err[0]:.2e} rel L2 {err[1]:.2e}", flush=True)
+
+
+@pytest.mark.timeout(400)
+@pytest.mark.parametrize("name", kvgen.WORKLOADS)
+def test_workload_first_and_last_layer(name):
+    check_workload(kvgen.workload(name))
+
+
+@pytest.mark.timeout(400)
+@pytest.mark.parametrize("name,G", [("8b-64k", 64), ("8b-64k", 256), ("8b-4k", 64), ("70b-32k", 256)])
+def test_paper_chunk_sizes_at_full_size(name, G):
+    # the paper's end-to-end settings use G = 64 (main) and 256 besides 16
+    check_workload(kvgen.with_chunk_tokens(kvgen.workload(name), G))

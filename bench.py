@@ -568,7 +568,7 @@ def run_bench(args):
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)},
         "flops_per_layer": flops_per_layer, "op_ms_per_request_layer": round(op_ms / (len(hbm[1:]) * L * R), 4),
-        "what": "suffix K/V pack + attention + split combine of one layer, HIP events around them",
+        "what": "attention + split combine of one layer, HIP events around them",
         "tflops_whole_pass": round(layer_tflops, 2),
     }
     line["ttft_ms"], res = ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev)

@@ -177,6 +177,46 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
                             const oc_block_table *block_table, int32_t layer, void *out,
                             void *workspace, size_t workspace_bytes, void *stream);
 
+/* Rest-of-layer compute window (the C_l of eq. (3): the compute the miss
+ * tokens expose per layer, Section 3.5; every layer runs the same
+ * projections and feed-forward network, Section 3.6).  A Llama-style layer
+ * around the attention, on T suffix tokens, bf16 with fp32 accumulation:
+ *   o    = attn_out . W_o           [T][H]        H = n_q * d
+ *   gu   = o . W_gate_up            [T][2F]       gate columns, then up columns
+ *   act  = silu(gate) * up          [T][F]        silu(x) = x / (1 + e^-x), fp32
+ *   h    = act . W_down             [T][H]
+ *   qkv  = h . W_qkv                [T][(n_q + 2 n_kv) d]   the next layer's projection
+ * Each stage is rounded to bf16 (nearest even).  Norms, residuals and biases
+ * are left out.  The GEMMs run in rocBLAS, the gating in a kernel of this
+ * library.  Weights are device bf16, [K][N] row-major (input features by
+ * output features), one matrix per layer back to back, 16-byte aligned;
+ * caller-owned and only read. */
+typedef struct {
+    int32_t ffn_dim;           /* F, a multiple of 8                                     */
+    const void *w_o;           /* [L][H][H]                                              */
+    const void *w_gate_up;     /* [L][H][2F]                                             */
+    const void *w_down;        /* [L][F][H]                                              */
+    const void *w_qkv;         /* [L][H][(n_q + 2 n_kv) d]                               */
+} oc_layer_weights;
+
+/* Device outputs of the chain's stages for T rows (caller-owned, 16-byte
+ * aligned, shapes as above). */
+typedef struct {
+    void *o;
+    void *gate_up;
+    void *act;
+    void *h;
+    void *qkv;
+} oc_layer_buffers;
+
+/* The chain above for one layer; attn_out is device bf16 [tokens][H] (the
+ * attention output, as oc_suffix_prefill_layer writes it).  tokens == 0 is
+ * not an error.  Asynchronous on `stream`; the first call on a stream
+ * creates the GEMM library's handle for it (which may allocate). */
+int oc_rest_of_layer(const void *attn_out, int64_t tokens, const oc_layout *layout,
+                     const oc_layer_weights *weights, int32_t layer, const oc_layer_buffers *buffers,
+                     void *stream);
+
 /* ---------------------------------------------------------------------------
  * Layerwise pipeline (Section 3.5, eq. (3)): for every layer, the payload
  * lands (host producer -> pinned slot -> DMA into an HBM slot), is ingested
@@ -269,6 +309,12 @@ typedef struct {
                                   (oc_kv_suffix_append), so the run leaves the full KV
                                   state; every block table must then hold
                                   ceil((T_p+T_s)/page_size) entries                       */
+    const oc_layer_weights *layer_weights;
+                               /* non-NULL: after each layer's attention (and append), run
+                                  oc_rest_of_layer on the attention output, on the same
+                                  stream, so each layer's window C_l is the whole layer's
+                                  compute; the struct is copied at context creation, the
+                                  weights must outlive the context                        */
 } oc_pipeline_opts;
 
 /* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */

@@ -32,6 +32,8 @@ KIND_KNEW = 3      # suffix keys
 KIND_VNEW = 4      # suffix values
 KIND_TABLE = 5     # block-table permutation
 KIND_LENGTHS = 6   # batch prefix lengths
+KIND_WEIGHT = 7    # rest-of-layer weights (req = which matrix)
+KIND_ACT = 8       # rest-of-layer input activations
 
 
 def _philox(seed: int, kind: int, req: int = 0, layer: int = 0) -> np.random.Generator:
@@ -104,6 +106,27 @@ def suffix_tensor(seed: int, kind: int, req: int, layer: int, shape: Sequence[in
     """Random bfloat16 suffix tensor (queries, new keys or new values) of a layer."""
     n = int(np.prod(shape))
     return normal_bf16(seed, kind, req, layer, n).reshape(tuple(shape))
+
+
+# ---------------------------------------------------------------------------
+# rest-of-layer weights
+# ---------------------------------------------------------------------------
+
+WEIGHT_NAMES = ("w_o", "w_gate_up", "w_down", "w_qkv")
+
+
+def layer_weight(seed: int, which: int, layer: int, K: int, N: int) -> np.ndarray:
+    """Random [K][N] bfloat16 weight matrix, entries N(0, 1/K), so a product
+    with unit-variance inputs keeps unit variance.  `which` indexes
+    WEIGHT_NAMES."""
+    g = _philox(seed, KIND_WEIGHT, which, layer)
+    x = g.standard_normal(K * N, dtype=np.float32) * np.float32(K ** -0.5)
+    return f32_to_bf16_bits(x).reshape(K, N)
+
+
+def layer_weight_shapes(H: int, F: int, n_qkv: int):
+    """[K][N] of W_o, W_gate_up, W_down, W_qkv."""
+    return ((H, H), (H, 2 * F), (F, H), (H, n_qkv))
 
 
 # ---------------------------------------------------------------------------

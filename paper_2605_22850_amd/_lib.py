@@ -26,7 +26,7 @@ DELIVERIES = {"layerwise": 0, "chunkwise": 1, "auto": 2}
 
 EXPORTS = [
     "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest",
-    "oc_kv_layer_gather", "oc_kv_chunks_gather", "oc_kv_suffix_append",
+    "oc_kv_layer_gather", "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_rest_of_layer",
     "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
     "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate",
 ]
@@ -61,7 +61,16 @@ class c_pipeline_opts(ctypes.Structure):
                 ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
                 ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
                 ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double),
-                ("emulate_compute", c_int32), ("append_suffix", c_int32)]
+                ("emulate_compute", c_int32), ("append_suffix", c_int32), ("layer_weights", c_void_p)]
+
+
+class c_layer_weights(ctypes.Structure):
+    _fields_ = [("ffn_dim", c_int32), ("w_o", c_void_p), ("w_gate_up", c_void_p), ("w_down", c_void_p),
+                ("w_qkv", c_void_p)]
+
+
+class c_layer_buffers(ctypes.Structure):
+    _fields_ = [("o", c_void_p), ("gate_up", c_void_p), ("act", c_void_p), ("h", c_void_p), ("qkv", c_void_p)]
 
 
 class c_request(ctypes.Structure):
@@ -98,6 +107,8 @@ def lib():
                                           c_void_p]
         L.oc_kv_suffix_append.argtypes = [c_void_p, c_void_p, c_int64, POINTER(c_block_table), POINTER(c_kv_pool),
                                           c_int32, c_void_p]
+        L.oc_rest_of_layer.argtypes = [c_void_p, c_int64, POINTER(c_layout), POINTER(c_layer_weights), c_int32,
+                                       POINTER(c_layer_buffers), c_void_p]
         L.oc_attention_workspace_bytes.argtypes = [POINTER(c_layout), c_int64, c_int64]
         L.oc_attention_workspace_bytes.restype = c_size_t
         L.oc_suffix_prefill_layer.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, POINTER(c_kv_pool),
@@ -116,7 +127,7 @@ def lib():
         L.oc_bandwidth_allocate.argtypes = [c_int32, c_int32, POINTER(c_double), POINTER(c_double), c_double, c_double,
                                             POINTER(c_double)]
         for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest", "oc_kv_layer_gather",
-                     "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_suffix_prefill_layer",
+                     "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_rest_of_layer", "oc_suffix_prefill_layer",
                      "oc_bandwidth_allocate"):
             getattr(L, name).restype = c_int
         _lib = L
@@ -230,6 +241,31 @@ def oc_kv_suffix_append(k_new, v_new, suffix_tokens: int, pages, num_tokens: int
                                      layer, _stream(stream)))
 
 
+@dataclass
+class LayerWeights:
+    """Device bf16 weights of the rest-of-layer window (torch tensors, [L][K][N]
+    row-major each; the tensors must outlive every call or context using them)."""
+    ffn_dim: int
+    w_o: object             # [L][H][H], H = n_q * d
+    w_gate_up: object       # [L][H][2F]
+    w_down: object          # [L][F][H]
+    w_qkv: object           # [L][H][(n_q + 2 n_kv) d]
+
+    def c(self) -> c_layer_weights:
+        return c_layer_weights(self.ffn_dim, _ptr(self.w_o), _ptr(self.w_gate_up), _ptr(self.w_down),
+                               _ptr(self.w_qkv))
+
+
+def oc_rest_of_layer(attn_out, tokens: int, layout: Layout, weights: LayerWeights, layer: int, o, gate_up, act, h,
+                     qkv, stream=None) -> None:
+    """The rest of one layer on `tokens` rows of attn_out; stage outputs into o, gate_up, act, h, qkv."""
+    lay = layout.c()
+    w = weights.c()
+    b = c_layer_buffers(_ptr(o), _ptr(gate_up), _ptr(act), _ptr(h), _ptr(qkv))
+    _check(lib().oc_rest_of_layer(_ptr(attn_out), tokens, ctypes.byref(lay), ctypes.byref(w), layer,
+                                  ctypes.byref(b), _stream(stream)))
+
+
 def oc_attention_workspace_bytes(layout: Layout, prefix_tokens: int, suffix_tokens: int) -> int:
     lay = layout.c()
     n = lib().oc_attention_workspace_bytes(ctypes.byref(lay), prefix_tokens, suffix_tokens)
@@ -271,12 +307,15 @@ def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, m
                       producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
                       fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0,
                       delivery="layerwise", theta_bytes: float = 0.0, emulate_compute: bool = False,
-                      append_suffix: bool = False):
+                      append_suffix: bool = False, layer_weights: Optional[LayerWeights] = None):
     pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
     dv = DELIVERIES[delivery] if isinstance(delivery, str) else int(delivery)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
                            fault_layer, pol, margin_bytes_per_s, dv, theta_bytes, int(bool(emulate_compute)),
-                           int(bool(append_suffix)))
+                           int(bool(append_suffix)), None)
+    lw = layer_weights.c() if layer_weights is not None else None
+    if lw is not None:
+        opts.layer_weights = ctypes.cast(ctypes.pointer(lw), c_void_p)     # copied by the library
     kp = make_pool(pool, layout)
     ctx = c_void_p()
     _check(lib().oc_context_create(device, ctypes.byref(kp), ctypes.byref(opts), max_prefix_tokens,

@@ -225,6 +225,24 @@ int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_
     return OC_OK;
 }
 
+int oc_rest_of_layer(const void *attn_out, int64_t tokens, const oc_layout *layout, const oc_layer_weights *weights,
+                     int32_t layer, const oc_layer_buffers *buffers, void *stream) {
+    clear_error();
+    if (!layout) return fail(OC_EINVAL, "layout is NULL");
+    int rc = check_layout(*layout);
+    if (rc) return rc;
+    if ((rc = check_layer_weights(*layout, weights))) return rc;
+    if (layer < 0 || layer >= layout->num_layers) return fail(OC_ERANGE, "layer out of range");
+    if (tokens < 0) return fail(OC_EINVAL, "negative tokens");
+    if (tokens > INT32_MAX / 2) return fail(OC_ERANGE, "too many tokens");
+    if (tokens == 0) return OC_OK;
+    if (!attn_out) return fail(OC_EINVAL, "attn_out is NULL");
+    if (!aligned(attn_out, 16)) return fail(OC_EALIGN, "attn_out must be 16-byte aligned");
+    if ((rc = check_layer_buffers(buffers))) return rc;
+    LayerArgs a = layer_args(*layout, *weights, layer, attn_out, tokens, *buffers);
+    return launch_rest_of_layer(a, static_cast<hipStream_t>(stream));
+}
+
 int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tokens,
                         const oc_block_table *block_table, oc_kv_pool *kv_pool, int32_t layer, void *stream) {
     clear_error();

@@ -75,6 +75,24 @@ int check_append_table(const oc_block_table *bt, const oc_layout &l, int64_t suf
 AppendArgs append_args(const oc_kv_pool *pool, const oc_block_table *bt, int32_t layer, const void *k_new,
                        const void *v_new, int64_t suffix_tokens);
 
+// ---- rest-of-layer compute window ---------------------------------------------
+struct LayerArgs {
+    int64_t T, H, F, NQKV;                           // tokens, n_q*d, ffn_dim, (n_q+2n_kv)*d
+    const uint16_t *attn_out;                        // [T][H]
+    const uint16_t *w_o, *w_gu, *w_down, *w_qkv;    // this layer's weights, [K][N] row-major
+    uint16_t *o, *gu, *act, *h, *qkv;                // outputs of the chain's stages
+};
+// enqueues O, gate|up, SiLU gating, down and QKV on `s`; an oc_status
+int launch_rest_of_layer(const LayerArgs &a, hipStream_t s);
+LayerArgs layer_args(const oc_layout &l, const oc_layer_weights &w, int32_t layer, const void *attn_out,
+                     int64_t tokens, const oc_layer_buffers &b);
+int check_layer_weights(const oc_layout &l, const oc_layer_weights *w);
+int check_layer_buffers(const oc_layer_buffers *b);
+// bytes of one buffer set for `tokens` rows, and each stage's offset in it
+size_t layer_buffer_bytes(const oc_layout &l, int32_t ffn_dim, int64_t tokens, size_t off[5]);
+// drop the GEMM library's state bound to a stream about to be destroyed
+void forget_blas_stream(hipStream_t s);
+
 // ---- emulated compute window ---------------------------------------------------
 // holds stream `s` for `seconds` (at most OC_MAX_WINDOW_S, checked by callers)
 hipError_t launch_compute_window(double seconds, hipStream_t s);

@@ -43,8 +43,12 @@ struct Context {
     hipStream_t copy = nullptr, compute = nullptr;
     std::vector<hipStream_t> req_streams;   // per-request compute streams (emulated compute windows)
     std::vector<Slot> slots;
-    void *ws = nullptr;
+    void *ws = nullptr;                // attention workspace, one slice per stream in use
     size_t ws_bytes = 0;
+    bool has_layer = false;            // rest-of-layer compute after each attention
+    oc_layer_weights lw{};
+    void *lbuf = nullptr;              // its stage buffers, one set per stream in use
+    size_t lbuf_bytes = 0;
     std::vector<hipEvent_t> events;    // pool of timing events, reused across runs
     hipEvent_t caller_done = nullptr;  // null-stream work enqueued before a run
     double last_ms = 0.0;
@@ -105,9 +109,16 @@ static void release(Context *c) {
     for (auto e : c->events) hipEventDestroy(e);
     if (c->caller_done) hipEventDestroy(c->caller_done);
     if (c->ws) hipFree(c->ws);
+    if (c->lbuf) hipFree(c->lbuf);
     if (c->copy) hipStreamDestroy(c->copy);
-    if (c->compute) hipStreamDestroy(c->compute);
-    for (auto st : c->req_streams) hipStreamDestroy(st);
+    if (c->compute) {
+        forget_blas_stream(c->compute);
+        hipStreamDestroy(c->compute);
+    }
+    for (auto st : c->req_streams) {
+        forget_blas_stream(st);
+        hipStreamDestroy(st);
+    }
     delete c;
 }
 
@@ -545,19 +556,37 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     const int64_t b_tok = 2LL * l.num_kv_heads * l.head_dim * 2;     // bytes per token per layer
     const int64_t S = b_tok * l.chunk_tokens;
 
-    // attention workspace large enough for every request
+    // Each request computes on the compute stream, or with emulated windows on
+    // a stream of its own; every stream in use gets its own attention
+    // workspace and rest-of-layer buffers, since their work may overlap.
+    const bool emu = c->opts.emulate_compute != 0;
+    const int64_t n_streams = emu ? n_reqs : 1;
     size_t ws_need = 0;
+    int64_t max_ts = 0;
     for (int32_t i = 0; i < n_reqs; ++i) {
         AttnPlan p;
         plan_attention(l, reqs[i].prefix_tokens, reqs[i].suffix_tokens, &p);
         ws_need = std::max(ws_need, p.total);
+        max_ts = std::max(max_ts, reqs[i].suffix_tokens);
     }
-    if (ws_need > c->ws_bytes) {
+    const size_t ws_stride = (ws_need + 255) / 256 * 256;
+    if (ws_stride * n_streams > c->ws_bytes) {
         if (c->ws) OC_HIP(hipFree(c->ws));
         c->ws = nullptr;
         c->ws_bytes = 0;
-        if (hipMalloc(&c->ws, ws_need) != hipSuccess) return fail(OC_ENOMEM, "attention workspace allocation failed");
-        c->ws_bytes = ws_need;
+        if (hipMalloc(&c->ws, ws_stride * n_streams) != hipSuccess)
+            return fail(OC_ENOMEM, "attention workspace allocation failed");
+        c->ws_bytes = ws_stride * n_streams;
+    }
+    size_t loff[5] = {0, 0, 0, 0, 0};
+    const size_t lb_stride = c->has_layer ? layer_buffer_bytes(l, c->lw.ffn_dim, max_ts, loff) : 0;
+    if (lb_stride * n_streams > c->lbuf_bytes) {
+        if (c->lbuf) OC_HIP(hipFree(c->lbuf));
+        c->lbuf = nullptr;
+        c->lbuf_bytes = 0;
+        if (hipMalloc(&c->lbuf, lb_stride * n_streams) != hipSuccess)
+            return fail(OC_ENOMEM, "rest-of-layer buffer allocation failed");
+        c->lbuf_bytes = lb_stride * n_streams;
     }
 
     // delivery of each request (eq. (2)); only the producer has an order to choose
@@ -574,7 +603,6 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 ++n_cw;
             }
         }
-    const bool emu = c->opts.emulate_compute != 0;
     if (emu)
         for (int32_t r = 0; r < n_reqs; ++r)
             if (!(reqs[r].layer_compute_s >= 0.0) || reqs[r].layer_compute_s > OC_MAX_WINDOW_S)
@@ -628,8 +656,12 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     std::vector<hipEvent_t> done(c->events.begin() + 1 + 2 * n_items, c->events.begin() + 1 + 2 * n_items + n_done);
     std::vector<double> produced(n_items, -1.0);
 
-    // one layer's attention of one request on `st`
-    auto enqueue_attention = [&](const oc_request &r, int32_t layer, hipStream_t st) -> hipError_t {
+    // one layer's compute for request `ri` on `st`: attention, then the suffix
+    // append and the rest of the layer when asked for
+    std::string layer_msg;       // why the rest of the layer failed to enqueue
+    auto enqueue_attention = [&](int32_t ri, int32_t layer, hipStream_t st) -> hipError_t {
+        const oc_request &r = reqs[ri];
+        const int64_t slot = emu ? ri : 0;
         AttnPlan p;
         plan_attention(l, r.prefix_tokens, r.suffix_tokens, &p);
         AttnArgs a{};
@@ -644,10 +676,18 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         a.pool_k = base + ((int64_t)layer * 2 + 0) * l.num_pages * block;
         a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
         a.pages = r.block_table->pages;
-        a.ws = static_cast<unsigned char *>(c->ws);
+        a.ws = static_cast<unsigned char *>(c->ws) + slot * ws_stride;
         hipError_t e = launch_attention(p, a, st);
         if (e == hipSuccess && c->opts.append_suffix)
             e = launch_append(append_args(&c->pool, r.block_table, layer, a.k_new, a.v_new, r.suffix_tokens), st);
+        if (e == hipSuccess && c->has_layer) {
+            unsigned char *lb = static_cast<unsigned char *>(c->lbuf) + slot * lb_stride;
+            const oc_layer_buffers bufs{lb + loff[0], lb + loff[1], lb + loff[2], lb + loff[3], lb + loff[4]};
+            if (launch_rest_of_layer(layer_args(l, c->lw, layer, a.out, r.suffix_tokens, bufs), st) != OC_OK) {
+                layer_msg = oc_last_error();
+                return hipErrorLaunchFailure;
+            }
+        }
         return e;
     };
 
@@ -784,13 +824,13 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 const hipStream_t cs = stream_of(it.req);
                 e = hipStreamWaitEvent(cs, ingested[k], 0);
                 for (int32_t layer = 0; layer < L && e == hipSuccess; ++layer) {
-                    e = enqueue_attention(r, layer, cs);
+                    e = enqueue_attention(it.req, layer, cs);
                     if (e == hipSuccess && emu) e = launch_compute_window(r.layer_compute_s, cs);
                     if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + layer], cs);
                 }
             }
             if (e != hipSuccess) {
-                status = hip_fail(e, "enqueueing a chunk group");
+                status = layer_msg.empty() ? hip_fail(e, "enqueueing a chunk group") : fail(OC_EHIP, layer_msg);
                 msg = oc_last_error();
                 break;
             }
@@ -888,11 +928,11 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             e = hipEventRecord(landed[k], attn_stream);
             if (e == hipSuccess) e = hipEventRecord(ingested[k], attn_stream);
         }
-        if (e == hipSuccess) e = enqueue_attention(r, it.layer, attn_stream);
+        if (e == hipSuccess) e = enqueue_attention(it.req, it.layer, attn_stream);
         if (e == hipSuccess && emu) e = launch_compute_window(r.layer_compute_s, attn_stream);
         if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + it.layer], attn_stream);
         if (e != hipSuccess) {
-            status = hip_fail(e, "enqueueing a layer");
+            status = layer_msg.empty() ? hip_fail(e, "enqueueing a layer") : fail(OC_EHIP, layer_msg);
             msg = oc_last_error();
             break;
         }
@@ -975,6 +1015,15 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
     if (rc) {
         delete c;
         return rc;
+    }
+    if (c->opts.layer_weights) {
+        if ((rc = check_layer_weights(l, c->opts.layer_weights))) {
+            delete c;
+            return rc;
+        }
+        c->has_layer = true;
+        c->lw = *c->opts.layer_weights;
+        c->opts.layer_weights = &c->lw;
     }
     c->max_prefix = max_prefix_tokens;
     c->max_suffix = max_suffix_tokens;

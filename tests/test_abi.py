@@ -144,6 +144,32 @@ def test_suffix_append_validation():
     assert oc.lib().oc_kv_suffix_append(None, None, 1, None, None, 0, None) == L.OC_EINVAL
 
 
+def _rest(layout, ffn=64, tokens=8, layer=0, weights=(FAKE, FAKE, FAKE, FAKE), attn=FAKE,
+          bufs=(FAKE, FAKE, FAKE, FAKE, FAKE)):
+    w = L.c_layer_weights(ffn, *weights)
+    b = L.c_layer_buffers(*bufs)
+    return oc.lib().oc_rest_of_layer(attn, tokens, ctypes.byref(layout), ctypes.byref(w), layer, ctypes.byref(b),
+                                     None)
+
+
+def test_rest_of_layer_validation():
+    lay = _layout()
+    assert _rest(lay, ffn=60) == L.OC_ESHAPE
+    assert _rest(lay, ffn=0) == L.OC_ESHAPE
+    assert _rest(lay, weights=(FAKE, None, FAKE, FAKE)) == L.OC_EINVAL
+    assert _rest(lay, weights=(FAKE, FAKE, FAKE + 8, FAKE)) == L.OC_EALIGN
+    assert _rest(lay, layer=2) == L.OC_ERANGE
+    assert _rest(lay, tokens=-1) == L.OC_EINVAL
+    assert _rest(lay, attn=None) == L.OC_EINVAL
+    assert _rest(lay, attn=FAKE + 2) == L.OC_EALIGN
+    assert _rest(lay, bufs=(FAKE, FAKE, None, FAKE, FAKE)) == L.OC_EINVAL
+    assert _rest(lay, bufs=(FAKE, FAKE, FAKE, FAKE, FAKE + 4)) == L.OC_EALIGN
+    assert _rest(_layout(num_q_heads=3)) == L.OC_ESHAPE
+    # no tokens is not an error (nothing is launched)
+    assert _rest(lay, tokens=0, attn=None, bufs=(None,) * 5) == L.OC_OK
+    assert oc.lib().oc_rest_of_layer(FAKE, 8, None, None, 0, None, None) == L.OC_EINVAL
+
+
 def test_attention_validation():
     lay = _layout()
     bt = L.c_block_table(FAKE, 16, 256)

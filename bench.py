@@ -437,6 +437,100 @@ def scheduler_workloads(args):
     return out
 
 
+CELLS = [(4096, 0.125), (4096, 0.5), (4096, 0.875), (65536, 0.125), (65536, 0.5), (65536, 0.875)]
+
+
+def canonical_cells(args):
+    """The paper's end-to-end TTFT evaluation shape on this GPU: Llama-3-8B
+    (32 layers, 32q/8kv, d 128, FFN 14336) with random weights, contexts of
+    4K and 64K tokens at 12.5/50/87.5 % prefix hits stored as G-token chunks;
+    every layer computes its attention and the rest of the layer (O,
+    gate/up, SiLU, down, QKV GEMMs) on the miss tokens.  Per cell: TTFT with
+    the KV HBM-resident, the producer uncapped (host memory over PCIe), and
+    capped at 12.5 GB/s layerwise and chunkwise, beside eq. (3) and the
+    chunkwise closed form with X_l = layer bytes / cap and C_l measured."""
+    import torch
+    import kvgen
+    import oracle.model as model
+    import paper_2605_22850_amd as oc
+    torch.cuda.set_device(0)
+    L, nq, nkv, d, F, Ps, G = 32, 32, 8, 128, 14336, 16, args.cells_chunk
+    H, NQ, b = nq * d, (nq + 2 * nkv) * d, 2 * nkv * d * 2
+    seed = 8
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+
+    def randn_bf16(shape, scale=1.0):
+        t = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+        flat = t.view(shape[0], -1)
+        for i in range(shape[0]):       # one layer at a time: bounded float32 temporaries
+            flat[i].copy_(torch.randn(flat.shape[1], generator=gen, device="cuda") * scale)
+        return t
+
+    t0 = time.time()
+    shapes = kvgen.layer_weight_shapes(H, F, NQ)
+    ws = [randn_bf16((L, K, N), K ** -0.5) for K, N in shapes]
+    weights = oc.LayerWeights(F, *ws)
+    max_tp = max(int(c * r) for c, r in CELLS)
+    slice_elems = 2 * G * nkv * d
+    objs = kvgen.chunk_objects(seed, 0, L, max_tp // G, slice_elems, threads=16)     # [N][L][S/2]
+    log(f"[bench] cells setup: weights {sum(w.numel() for w in ws) * 2 / 2**30:.1f} GiB, "
+        f"chunk objects {objs.nbytes / 2**30:.1f} GiB, {time.time() - t0:.1f} s")
+    trials = max(2, args.trials // 2)
+    out = {"model": "llama-3-8b shape, random weights", "chunk_tokens": G, "cap_GBps": args.cap / 1e9,
+           "ffn_dim": F, "cells": []}
+    for ctx_len, hit in CELLS:
+        tp, ts = int(ctx_len * hit), ctx_len - int(ctx_len * hit)
+        n = tp // G
+        need = -(-tp // Ps)
+        P = 2 * need
+        layout = oc.Layout(L, nq, nkv, d, Ps, G, P)
+        pool = torch.zeros(layout.pool_elems, dtype=torch.int16, device="cuda")
+        table = torch.from_numpy(kvgen.block_tables(seed, [need], P)[0]).cuda()
+        q = randn_bf16((L, ts, nq, d))
+        kn = randn_bf16((L, ts, nkv, d))
+        vn = randn_bf16((L, ts, nkv, d))
+        outt = torch.zeros((L, ts, nq, d), dtype=torch.bfloat16, device="cuda")
+        reqs = [oc.Request(tp, ts, table, q, kn, vn, outt, chunk_objects=objs[:n].reshape(n, -1))]
+        wl = kvgen.Workload(name=f"cell-{ctx_len}-{hit}", num_layers=L, num_q_heads=nq, num_kv_heads=nkv,
+                            head_dim=d, page_size=Ps, chunk_tokens=G, prefix_tokens=[tp], suffix_tokens=[ts],
+                            pool_pages=P, seed=seed)
+        kw = dict(layer_weights=weights)
+        res = {"context": ctx_len, "hit": hit, "prefix_tokens": tp, "suffix_tokens": ts}
+        # the uncapped producer also fills the pool for the HBM-resident runs
+        runs = {"producer_uncapped": run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials,
+                                              rate_bytes_per_s=0.0, **kw)}
+        runs["hbm_resident"] = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_HBM_RESIDENT, trials, **kw)
+        runs["capped_layerwise"] = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials,
+                                            rate_bytes_per_s=args.cap, **kw)
+        runs["capped_chunkwise"] = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials,
+                                            rate_bytes_per_s=args.cap, delivery="chunkwise", **kw)
+        ttft = {k: float(np.mean([st[0]["ttft_ms"] for _, st in v[1:]])) for k, v in runs.items()}
+        c_ms = [float(np.mean([st[0]["done_ms"][l] - st[0]["ingested_ms"][l] for _, st in runs["hbm_resident"][1:]]))
+                for l in range(L)]
+        x_ms = [tp * b / args.cap * 1e3] * L
+        res["ttft_ms"] = {k: round(v, 2) for k, v in ttft.items()}
+        res["compute_ms_per_layer"] = round(float(np.mean(c_ms)), 3)
+        res["transfer_ms_per_layer_at_cap"] = round(x_ms[0], 3)
+        res["eq3_ms"] = round(model.layerwise_ttft(x_ms, c_ms), 2)
+        res["chunkwise_model_ms"] = round(model.chunkwise_ttft(x_ms, c_ms), 2)
+        base = ttft["hbm_resident"]
+        res["added_over_hbm_pct"] = {k: round((v - base) / base * 100, 2) for k, v in ttft.items()
+                                     if k != "hbm_resident"}
+        res["capped_layerwise_over_uncapped_pct"] = round(
+            (ttft["capped_layerwise"] - ttft["producer_uncapped"]) / ttft["producer_uncapped"] * 100, 2)
+        flops = attn_flops(nq, d, tp, ts)
+        res["attention_gflop_per_layer"] = round(flops / 1e9, 1)
+        res["gemm_gflop_per_layer"] = round(2 * ts * sum(K * N for K, N in shapes) / 1e9, 1)
+        res["layer_tflops"] = round((flops + 2 * ts * sum(K * N for K, N in shapes)) / (np.mean(c_ms) / 1e3) / 1e12, 1)
+        out["cells"].append(res)
+        log(f"[bench] cell {ctx_len} @ {hit}: ttft {res['ttft_ms']} eq3 {res['eq3_ms']} "
+            f"C/layer {res['compute_ms_per_layer']} ms X/layer {res['transfer_ms_per_layer_at_cap']} ms")
+        del pool, table, q, kn, vn, outt, reqs, runs
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl, objs_all, tables, budget_s):
     """The CPU oracle, as it stands, on a bounded sample of the same workload."""
     import oracle
@@ -730,6 +824,10 @@ def main():
                     help="run the multi-tenant scheduler evaluation on these workloads (e.g. A,B,C) instead")
     ap.add_argument("--scheduler-scale", type=int, default=4,
                     help="divide the scheduler workloads' cached tokens and compute windows by this")
+    ap.add_argument("--canonical-cells", action="store_true",
+                    help="run the end-to-end TTFT cells (4K/64K x 12.5/50/87.5%% hits) with the whole layer's "
+                         "compute instead")
+    ap.add_argument("--cells-chunk", type=int, default=64, help="chunk tokens G of the canonical cells")
     ap.add_argument("--policy-margin", type=float, default=0.625e9,
                     help="Calibrated Stall-opt margin, bytes/s (0.625e9 = 5 Gbps)")
     ap.add_argument("--second-workload", default="8b-4k",
@@ -747,6 +845,12 @@ def main():
         print("bench.py measures one GPU: the path has no cross-GPU part in this build; run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+    if args.canonical_cells:
+        res = canonical_cells(args)
+        print(json.dumps({"metric": "TTFT with the whole layer's compute, end-to-end cells", "unit": "ms",
+                          "higher_is_better": False, "data": "synthetic: random weights and KV", "n_gpus": 1,
+                          "canonical_cells": res}), flush=True)
+        return
     if args.scheduler_workloads:
         res = scheduler_workloads(args)
         print(json.dumps({"metric": "added TTFT by bandwidth allocation policy (scheduler workloads)",

@@ -5,6 +5,7 @@
 // SiLU gating between them is a kernel of its own.
 #include <rocblas/rocblas.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <utility>
@@ -84,20 +85,31 @@ static int gemm(rocblas_handle h, const uint16_t *X, const uint16_t *W, uint16_t
     return OC_OK;
 }
 
+// Rows are independent, so long inputs go through the chain in row blocks
+// that keep every matrix handed to the GEMM library under 1 GiB.
 int launch_rest_of_layer(const LayerArgs &a, hipStream_t s) {
     if (a.T == 0) return OC_OK;
     std::lock_guard<std::mutex> g(g_blas_mu);
     rocblas_handle h = nullptr;
     int rc = blas_for(s, &h);
     if (rc) return rc;
-    if ((rc = gemm(h, a.attn_out, a.w_o, a.o, a.T, a.H, a.H))) return rc;
-    if ((rc = gemm(h, a.o, a.w_gu, a.gu, a.T, a.H, 2LL * a.F))) return rc;
-    const int64_t n = a.T * (a.F / 8);
-    hipLaunchKernelGGL(silu_mul_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.gu, a.act,
-                       (int64_t)(a.F / 8), n);
-    OC_HIP(hipGetLastError());
-    if ((rc = gemm(h, a.act, a.w_down, a.h, a.T, a.F, a.H))) return rc;
-    return gemm(h, a.h, a.w_qkv, a.qkv, a.T, a.H, a.NQKV);
+    const int64_t widest = std::max(std::max(2 * a.F, a.H), a.NQKV);
+    const int64_t rb = std::max<int64_t>(1, (INT64_C(1) << 29) / widest);
+    for (int64_t r0 = 0; r0 < a.T; r0 += rb) {
+        const int64_t m = std::min(rb, a.T - r0);
+        const uint16_t *x = a.attn_out + r0 * a.H;
+        uint16_t *o = a.o + r0 * a.H, *gu = a.gu + r0 * 2 * a.F, *act = a.act + r0 * a.F;
+        uint16_t *hh = a.h + r0 * a.H, *qkv = a.qkv + r0 * a.NQKV;
+        if ((rc = gemm(h, x, a.w_o, o, m, a.H, a.H))) return rc;
+        if ((rc = gemm(h, o, a.w_gu, gu, m, a.H, 2 * a.F))) return rc;
+        const int64_t n = m * (a.F / 8);
+        hipLaunchKernelGGL(silu_mul_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, gu, act,
+                           (int64_t)(a.F / 8), n);
+        OC_HIP(hipGetLastError());
+        if ((rc = gemm(h, act, a.w_down, hh, m, a.F, a.H))) return rc;
+        if ((rc = gemm(h, hh, a.w_qkv, qkv, m, a.H, a.NQKV))) return rc;
+    }
+    return OC_OK;
 }
 
 LayerArgs layer_args(const oc_layout &l, const oc_layer_weights &w, int32_t layer, const void *attn_out,

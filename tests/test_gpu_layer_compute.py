@@ -57,7 +57,10 @@ CASES = {
     "one-row": (4, 4, 64, 256, 1, 1, 0, None),
     "gqa-d128": (16, 4, 128, 2816, 200, 2, 1, None),
     "llama8b-layer-512-tokens": (32, 8, 128, 14336, 512, 1, 0, 16),
+    # 20000 rows go through the chain in two row blocks (18724 + 1276)
+    "llama8b-layer-two-row-blocks": (32, 8, 128, 14336, 20000, 1, 0, 16),
 }
+ROW_BLOCK_8B = (1 << 29) // (2 * 14336)
 
 
 @pytest.mark.timeout(300)
@@ -79,6 +82,8 @@ def test_rest_of_layer_matches_oracle(name):
     torch.cuda.synchronize()
     rows = np.arange(T) if n_rows is None else np.unique(np.r_[0, T - 1, np.random.default_rng(seed).choice(
         T, n_rows - 2, replace=False)])
+    if T > ROW_BLOCK_8B:
+        rows = np.unique(np.r_[rows, ROW_BLOCK_8B - 1, ROW_BLOCK_8B])     # both sides of the block edge
     ref = olayer.rest_of_layer(attn[rows], *(m[lay] for m in w_host))
     for k in cols:
         rel = _close(from_dev(bufs[k])[rows], ref[k], f"{name} stage {k}")

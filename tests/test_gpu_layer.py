@@ -99,6 +99,33 @@ def test_attention_matches_oracle(name):
     assert_attention_close(from_dev(out), c.expected_attention(), name)
 
 
+# the end-to-end cells' long suffixes: no key splitting, hundreds of row tiles
+# per KV head, causal masking over most of the keys; sampled rows (always the
+# first, the last and both sides of a row-tile edge)
+# (nq, nkv, d, n_chunks of 16, Ts, P)
+LONG_SUFFIX_CASES = {
+    "64k-context-12.5pct-hit": (32, 8, 128, 512, 57344, 1024),
+    "64k-context-50pct-hit": (32, 8, 128, 2048, 32768, 4096),
+    "4k-context-12.5pct-hit": (32, 8, 128, 32, 3584, 64),
+}
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("name", list(LONG_SUFFIX_CASES))
+def test_attention_long_suffix_sampled_rows(name):
+    import torch
+    nq, nkv, d, n, Ts, P = LONG_SUFFIX_CASES[name]
+    print(f"[attention] {name}", flush=True)
+    c = LayerCase(nq, nkv, d, 16, 16, n, Ts, P, 1, 0, seed=(zlib.crc32(name.encode()) & 0xFFF) + 1).upload()
+    c.run_ingest()
+    out = from_dev(c.run_attention())
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    tile_tokens = 256 // (nq // nkv)          # suffix tokens per 256-row tile
+    rows = sorted(set([0, Ts - 1, tile_tokens - 1, tile_tokens, Ts // 2, *rng.choice(Ts, 11, replace=False)]))
+    assert_attention_close(out[rows], c.expected_attention(rows=rows), name)
+
+
 def test_attention_permuted_table_is_bit_identical():
     import torch
     print("[attention] permuted table", flush=True)

@@ -261,12 +261,14 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     const int col = lane & 31, half = lane >> 5;
 
     // XCD-aware decode: workgroup w runs on XCD w % 8; all row tiles of one
-    // (KV head, split) group get consecutive slots on the same XCD
+    // (KV head, split) group get consecutive slots on the same XCD, the last
+    // row tile first: under the causal mask later rows see more suffix keys,
+    // and dispatching the longest tiles first keeps them out of the tail
     const int wg = blockIdx.x;
     const int xcd = wg & 7, local = wg >> 3;
     const int gamma = (local / p.m_tiles) * 8 + xcd;
     if (gamma >= p.n_groups) return;
-    const int mt = local % p.m_tiles;
+    const int mt = p.m_tiles - 1 - local % p.m_tiles;
     const int g = gamma / p.n_split, split = gamma - g * p.n_split;
 
     const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + col;

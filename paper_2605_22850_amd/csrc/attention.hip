@@ -439,9 +439,18 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
             for (int idx = tid; idx < D * (PAGE - k0); idx += THREADS) V[(pg * PAGE + k0) * D + idx] = 0;
         }
     };
+    // A block needs the mask only if it holds slots of the prefix's partial
+    // last page, or suffix keys that some row of this wavefront does not see
+    // yet (the wavefront's rows start at token tok_min).
+    const int tok_min = (int)(((int64_t)mt * TILE_ROWS + wave * WAVE_ROWS) / p.grp);
     auto softmax_block = [&](int j) {
         const int64_t b = b0 + j;
-        if ((b + 1) * 4 > full_pre_pages) mask_block(b);   // partial page or suffix keys
+        if ((b + 1) * 4 > full_pre_pages) {
+            const int64_t ps = p.n_pre_pages * PAGE - b * KB, pe = p.Tp - b * KB;
+            const bool partial_prefix = ps > 0 && pe < (ps < KB ? ps : (int64_t)KB);
+            const bool unseen_suffix = ps < KB && KB - 1 - ps > tok_min;
+            if (partial_prefix || unseen_suffix) mask_block(b);
+        }
         softmax_phase<D>(w, p.scale_log2);
     };
     // Each group runs its own copy of the loop (one straight path each, so

@@ -62,12 +62,15 @@ __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs 
     for (int kv = 0; kv < 2; ++kv) {
         const int64_t off = kv * (int64_t)G * D;
         uint16_t *dst = kdst + kv * a.region;
+        // non-temporal: the payload is read once and the pool rows are not
+        // read again until that layer's attention, so keep both out of the
+        // L2 that the running attention uses for its K/V tiles
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-            if (i < valid) r[i] = *reinterpret_cast<const u32x4 *>(a.staging + src[i] + off);
+            if (i < valid) r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.staging + src[i] + off));
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-            if (i < valid) *reinterpret_cast<u32x4 *>(dst + i * d) = r[i];
+            if (i < valid) __builtin_nontemporal_store(r[i], reinterpret_cast<u32x4 *>(dst + i * d));
     }
 }
 

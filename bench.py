@@ -754,7 +754,7 @@ def profile_summary(paths, workload, warmup, steps):
                 e["c"][cn] = e["c"].get(cn, 0.0) + val
             disp = sorted(by_disp.values(), key=lambda e: e["start"])
             att = [e for e in disp if "attn_fwd_kernel" in e["name"]][lo:hi]
-            if att and any("MfmaUtil" in e["c"] for e in att):
+            if att and any(e["c"] for e in att):
                 attn_counters.append((os.path.basename(path), att))
             ing = [e for e in disp if "kv_ingest" in e["name"]]
             first_ing = ing[0]["start"] if ing else float("inf")
@@ -774,6 +774,8 @@ def profile_summary(paths, workload, warmup, steps):
         for cn in sorted({k for e in att for k in e["c"]}):
             vals = [e["c"][cn] for e in att if cn in e["c"]]
             out.append(f"| {cn} | {np.mean(vals):.4g} |")
+        dur_ns = float(np.mean([e["end"] - e["start"] for e in att]))
+        out.append(f"| (mean dispatch duration, ns) | {dur_ns:.4g} |")
         mops = [e["c"]["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for e in att if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in e["c"]]
         if mops:
             out.append("")

@@ -148,8 +148,12 @@ def setup(wl):
     return layout, pool, reqs, objs_all, tables
 
 
+RUN_OPTS = {}     # context options every run of this process takes (from the command line)
+
+
 def run_mode(oc, pool, layout, wl, reqs, mode, trials, **kw):
-    ctx = oc.oc_context_create(pool, layout, mode, max(wl.prefix_tokens), max(wl.suffix_tokens), **kw)
+    ctx = oc.oc_context_create(pool, layout, mode, max(wl.prefix_tokens), max(wl.suffix_tokens),
+                               **{**RUN_OPTS, **kw})
     out = []
     try:
         for _ in range(trials):
@@ -603,7 +607,7 @@ def run_bench(args):
         run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, 1)
         log(f"[bench] warmup {i + 1}/{args.warmup}")
     ctx = oc.oc_context_create(pool, layout, oc.OC_MODE_DEVICE_STAGED, max(wl.prefix_tokens),
-                               max(wl.suffix_tokens))
+                               max(wl.suffix_tokens), **RUN_OPTS)
     stats_all = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -651,21 +655,22 @@ def run_bench(args):
     log("[bench] device-staged trials done")
     t_hbm = [x[0] for x in hbm[1:]]
     t_dev = [x[0] for x in dev[1:]]
-    # attention of one request's layer: from the event before it to the one after it, HBM-resident
+    # attention of a layer, all requests: from the first event before it to
+    # the last one after it (one launch when requests are batched, one after
+    # another otherwise), HBM-resident
     op_ms, op_flops = 0.0, 0.0
     for _, st in hbm[1:]:
-        for r, rst in enumerate(st):
-            for l in range(L):
-                op_ms += rst["done_ms"][l] - rst["ingested_ms"][l]
-                op_flops += attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r])
+        for l in range(L):
+            op_ms += max(rst["done_ms"][l] for rst in st) - min(rst["ingested_ms"][l] for rst in st)
+            op_flops += sum(attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r]) for r in range(R))
     attn_tflops = op_flops / (op_ms / 1e3) / 1e12
     flops_per_layer = sum(attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r]) for r in range(R))
     layer_tflops = flops_per_layer / (sum(t_hbm) / len(t_hbm) / L / 1e3) / 1e12
     line["attention"] = {
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)},
-        "flops_per_layer": flops_per_layer, "op_ms_per_request_layer": round(op_ms / (len(hbm[1:]) * L * R), 4),
-        "what": "attention + split combine of one layer, HIP events around them",
+        "flops_per_layer": flops_per_layer, "op_ms_per_layer": round(op_ms / (len(hbm[1:]) * L), 4),
+        "what": "attention + split combine of one layer (all requests), HIP events around them",
         "tflops_whole_pass": round(layer_tflops, 2),
     }
     line["ttft_ms"], res = ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev)
@@ -839,6 +844,8 @@ def main():
                     help="workload whose TTFT legs are reported beside the main one ('' to skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"{CALIB_COPIES} plain {CALIB_BYTES >> 20} MiB device copies before the steps")
+    ap.add_argument("--attention-per-request", action="store_true",
+                    help="one attention launch per request and layer, not one per layer for all requests")
     ap.add_argument("--profile-summary", nargs="+", metavar="DB",
                     help="print a markdown summary of rocprofv3 databases of a run of this script")
     args = ap.parse_args()
@@ -846,6 +853,8 @@ def main():
     if args.profile_summary:
         print(profile_summary(args.profile_summary, args.workload, args.warmup, args.steps))
         return
+    if args.attention_per_request:
+        RUN_OPTS["attention_per_request"] = True
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the path has no cross-GPU part in this build; run with --gpus 1",
               file=sys.stderr)

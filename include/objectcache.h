@@ -309,6 +309,14 @@ typedef struct {
                                   (oc_kv_suffix_append), so the run leaves the full KV
                                   state; every block table must then hold
                                   ceil((T_p+T_s)/page_size) entries                       */
+    int32_t attention_per_request;
+                               /* nonzero: one attention launch per request and layer,
+                                  planned as oc_suffix_prefill_layer plans it.  Otherwise,
+                                  when 2..16 requests are all delivered layer-major on one
+                                  schedule (no allocation policy, no chunkwise request, no
+                                  emulated windows), each layer's attention is one launch
+                                  over all of them after their ingests, with key splits
+                                  planned for all their row tiles together               */
     const oc_layer_weights *layer_weights;
                                /* non-NULL: after each layer's attention (and append), run
                                   oc_rest_of_layer on the attention output, on the same

@@ -61,7 +61,8 @@ class c_pipeline_opts(ctypes.Structure):
                 ("slots", c_int32), ("producer_threads", c_int32), ("timeout_ms", c_int32),
                 ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
                 ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double),
-                ("emulate_compute", c_int32), ("append_suffix", c_int32), ("layer_weights", c_void_p)]
+                ("emulate_compute", c_int32), ("append_suffix", c_int32), ("attention_per_request", c_int32),
+                ("layer_weights", c_void_p)]
 
 
 class c_layer_weights(ctypes.Structure):
@@ -307,12 +308,13 @@ def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, m
                       producer_threads: int = 0, timeout_ms: int = 0, fault: int = OC_FAULT_NONE,
                       fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0,
                       delivery="layerwise", theta_bytes: float = 0.0, emulate_compute: bool = False,
-                      append_suffix: bool = False, layer_weights: Optional[LayerWeights] = None):
+                      append_suffix: bool = False, layer_weights: Optional[LayerWeights] = None,
+                      attention_per_request: bool = False):
     pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
     dv = DELIVERIES[delivery] if isinstance(delivery, str) else int(delivery)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
                            fault_layer, pol, margin_bytes_per_s, dv, theta_bytes, int(bool(emulate_compute)),
-                           int(bool(append_suffix)), None)
+                           int(bool(append_suffix)), int(bool(attention_per_request)), None)
     lw = layer_weights.c() if layer_weights is not None else None
     if lw is not None:
         opts.layer_weights = ctypes.cast(ctypes.pointer(lw), c_void_p)     # copied by the library

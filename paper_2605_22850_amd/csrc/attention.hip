@@ -27,6 +27,8 @@
 // the V operand.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.hpp"
 
 namespace oc {
@@ -46,6 +48,10 @@ constexpr int WAVE_ROWS = 32 * QB;
 constexpr int TILE_ROWS = WAVES * WAVE_ROWS;
 constexpr int THREADS = WAVES * 64;
 constexpr int TARGET_WGS = 256;   // one workgroup per CU
+#ifndef OC_BATCH_ROUNDS
+#define OC_BATCH_ROUNDS 2
+#endif
+constexpr int BATCH_ROUNDS = OC_BATCH_ROUNDS;   // workgroups per CU a batched launch may queue
 constexpr float RESCALE_SLACK = 8.0f;   // log2 units the running max may lag
 #ifndef OC_LOOKAHEAD
 #define OC_LOOKAHEAD 4
@@ -62,6 +68,14 @@ struct KParams {
     int64_t Tp, Ts, rows, rows_pad, n_pre_pages, n_suf_pages, n_blocks, blocks_per_split;
     int nq, nkv, grp, m_tiles, n_split, n_groups;
     float scale_log2;
+};
+
+// One launch serves up to MAX_ATTN_BATCH requests of one layer: workgroup w
+// belongs to the last request whose first workgroup it has reached.
+struct KBatch {
+    int32_t n;
+    int32_t first_wg[MAX_ATTN_BATCH];
+    KParams req[MAX_ATTN_BATCH];
 };
 
 // value of the lane 32 positions away (the other half of the wavefront)
@@ -243,7 +257,16 @@ __device__ __forceinline__ void softmax_phase(WaveState<D> &w, float scale_log2)
 }
 
 template <int D>
-__global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
+__global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
+    // read the request's parameters straight from the kernel-argument segment
+    // (scalar loads at a uniform offset; indexing the by-value copy would
+    // place it in scratch memory)
+    typedef const __attribute__((address_space(4))) KBatch *kbatch_ptr;
+    const kbatch_ptr bp = (kbatch_ptr)__builtin_amdgcn_kernarg_segment_ptr();
+    int req = 0;
+    for (int i = 1; i < bp->n; ++i) req += (int)blockIdx.x >= bp->first_wg[i];
+    const __attribute__((address_space(4))) KParams &p = bp->req[req];
+    const int wg = (int)blockIdx.x - bp->first_wg[req];
     constexpr int TILE = KB * D;                   // elements of one K (or V) tile
     constexpr int CHUNKS = TILE * 2 / 1024;        // 1 KiB DMA chunks per tile
     constexpr int CPW = CHUNKS / WAVES;            // chunks per wavefront per tile
@@ -264,7 +287,6 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KParams p) {
     // (KV head, split) group get consecutive slots on the same XCD, the last
     // row tile first: under the causal mask later rows see more suffix keys,
     // and dispatching the longest tiles first keeps them out of the tail
-    const int wg = blockIdx.x;
     const int xcd = wg & 7, local = wg >> 3;
     const int gamma = (local / p.m_tiles) * 8 + xcd;
     if (gamma >= p.n_groups) return;
@@ -560,7 +582,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(KParams p) {
 // ---------------------------------------------------------------------------
 static size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *pl) {
+// Tiles and key blocks of one request; the split count is set apart.
+static AttnPlan plan_shape(const oc_layout &lay, int64_t Tp, int64_t Ts) {
     AttnPlan p{};
     p.Tp = Tp;
     p.Ts = Ts;
@@ -573,8 +596,11 @@ int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *pl) {
     p.n_pre_pages = (Tp + PAGE - 1) / PAGE;
     p.n_suf_pages = (Ts + PAGE - 1) / PAGE;
     p.n_blocks = (p.n_pre_pages + p.n_suf_pages + 3) / 4;
-    int64_t tiles = (int64_t)p.nkv * p.m_tiles;
-    int64_t ns = (TARGET_WGS + tiles - 1) / tiles;
+    return p;
+}
+
+// Split the keys into ns ranges, then size the workspace.
+static void plan_splits(AttnPlan &p, int64_t ns) {
     if (ns > p.n_blocks) ns = p.n_blocks;
     if (ns < 1) ns = 1;
     p.blocks_per_split = (p.n_blocks + ns - 1) / ns;
@@ -586,12 +612,45 @@ int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *pl) {
     p.off_ml = off;
     if (p.n_split > 1) off = round_up(off + (size_t)p.n_split * p.nkv * rows_pad * 2 * 4, 256);
     p.total = off > 256 ? off : 256;   // never 0: a size of 0 reports an unsupported shape
+}
+
+// One request alone: split the keys so that its row tiles fill the CUs.
+int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *pl) {
+    AttnPlan p = plan_shape(lay, Tp, Ts);
+    const int64_t tiles = (int64_t)p.nkv * p.m_tiles;
+    plan_splits(p, (TARGET_WGS + tiles - 1) / tiles);
     *pl = p;
     return OC_OK;
 }
 
+// Several requests in one launch: every workgroup gets at most `budget` key
+// blocks, the smallest budget that keeps the launch within BATCH_ROUNDS
+// workgroups per CU (or one range per tile, if there are more tiles), so the
+// dispatcher can even out long and short prefixes as CUs free up.
+int plan_attention_batch(const oc_layout &lay, const int64_t *Tp, const int64_t *Ts, int n, AttnPlan *plans) {
+    int64_t tiles = 0, work = 0, longest = 1;
+    for (int i = 0; i < n; ++i) {
+        plans[i] = plan_shape(lay, Tp[i], Ts[i]);
+        const int64_t t = (int64_t)plans[i].nkv * plans[i].m_tiles;
+        tiles += t;
+        work += t * plans[i].n_blocks;
+        longest = std::max<int64_t>(longest, plans[i].n_blocks);
+    }
+    auto wgs_for = [&](int64_t budget) {
+        int64_t w = 0;
+        for (int i = 0; i < n; ++i)
+            w += (int64_t)plans[i].nkv * plans[i].m_tiles * ((plans[i].n_blocks + budget - 1) / budget);
+        return w;
+    };
+    const int64_t cap = std::max<int64_t>((int64_t)TARGET_WGS * BATCH_ROUNDS, tiles);
+    int64_t budget = std::max<int64_t>(1, (work + cap - 1) / cap);
+    while (budget < longest && wgs_for(budget) > cap) ++budget;
+    for (int i = 0; i < n; ++i) plan_splits(plans[i], (plans[i].n_blocks + budget - 1) / budget);
+    return OC_OK;
+}
+
 template <int D>
-static hipError_t launch_d(const AttnPlan &pl, const AttnArgs &a, hipStream_t s) {
+static KParams make_params(const AttnPlan &pl, const AttnArgs &a) {
     KParams p{};
     p.q = a.q;
     p.pool_k = a.pool_k;
@@ -617,9 +676,25 @@ static hipError_t launch_d(const AttnPlan &pl, const AttnArgs &a, hipStream_t s)
     p.n_split = pl.n_split;
     p.n_groups = pl.nkv * pl.n_split;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+    return p;
+}
 
-    const int64_t groups_per_xcd = (p.n_groups + 7) / 8;
-    const int64_t grid = 8 * groups_per_xcd * pl.m_tiles;
+template <int D>
+static hipError_t launch_d(const AttnPlan *pl, const AttnArgs *a, int n, hipStream_t s) {
+    // requests with the longest workgroups first: the dispatcher then fills
+    // the tail of the launch with short ones
+    int order[MAX_ATTN_BATCH];
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::stable_sort(order, order + n, [&](int x, int y) { return pl[x].blocks_per_split > pl[y].blocks_per_split; });
+    KBatch batch{};
+    batch.n = n;
+    int64_t grid = 0;
+    for (int k = 0; k < n; ++k) {
+        const int i = order[k];
+        batch.req[k] = make_params<D>(pl[i], a[i]);
+        batch.first_wg[k] = (int32_t)grid;
+        grid += 8 * ((batch.req[k].n_groups + 7) / 8) * (int64_t)pl[i].m_tiles;
+    }
     static bool lds_set = false;
     if (!lds_set) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_fwd_kernel<D>),
@@ -627,18 +702,26 @@ static hipError_t launch_d(const AttnPlan &pl, const AttnArgs &a, hipStream_t s)
         if (e != hipSuccess) return e;
         lds_set = true;
     }
-    hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((unsigned)grid), dim3(THREADS), attn_lds_bytes<D>(), s, p);
-    if (pl.n_split > 1) {
-        constexpr int RPB = 256 / (D / 4);
-        const int64_t nrows = (int64_t)pl.nkv * pl.rows;
-        hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, s, p);
-    }
+    if (grid > 0) hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((unsigned)grid), dim3(THREADS), attn_lds_bytes<D>(), s, batch);
+    for (int k = 0; k < n; ++k)
+        if (batch.req[k].n_split > 1) {
+            constexpr int RPB = 256 / (D / 4);
+            const int64_t nrows = (int64_t)batch.req[k].nkv * batch.req[k].rows;
+            hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, s,
+                               batch.req[k]);
+        }
     return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnPlan &pl, const AttnArgs &a, hipStream_t s) {
-    if (pl.d == 128) return launch_d<128>(pl, a, s);
-    return launch_d<64>(pl, a, s);
+    if (pl.d == 128) return launch_d<128>(&pl, &a, 1, s);
+    return launch_d<64>(&pl, &a, 1, s);
+}
+
+hipError_t launch_attention_batch(const AttnPlan *pl, const AttnArgs *a, int n, hipStream_t s) {
+    if (n < 1 || n > MAX_ATTN_BATCH) return hipErrorInvalidValue;
+    if (pl[0].d == 128) return launch_d<128>(pl, a, n, s);
+    return launch_d<64>(pl, a, n, s);
 }
 
 }  // namespace oc

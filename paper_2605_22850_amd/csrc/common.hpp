@@ -113,6 +113,10 @@ struct AttnPlan {
     size_t off_o, off_ml, total;
 };
 int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *plan);
+// one launch for up to MAX_ATTN_BATCH requests of one layer: keys are split
+// so that all their row tiles together fill the CUs
+constexpr int MAX_ATTN_BATCH = 16;
+int plan_attention_batch(const oc_layout &lay, const int64_t *Tp, const int64_t *Ts, int n, AttnPlan *plans);
 
 struct AttnArgs {
     const uint16_t *q, *k_new, *v_new;
@@ -122,5 +126,7 @@ struct AttnArgs {
     unsigned char *ws;
 };
 hipError_t launch_attention(const AttnPlan &p, const AttnArgs &a, hipStream_t s);
+// all plans from one plan_attention_batch call, same layout
+hipError_t launch_attention_batch(const AttnPlan *plans, const AttnArgs *args, int n, hipStream_t s);
 
 }  // namespace oc

@@ -561,13 +561,32 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     // workspace and rest-of-layer buffers, since their work may overlap.
     const bool emu = c->opts.emulate_compute != 0;
     const int64_t n_streams = emu ? n_reqs : 1;
-    size_t ws_need = 0;
+    // When every request is delivered layer-major on one schedule and computes
+    // on the compute stream, each layer's attention is one launch over all
+    // of them (decided below, once the deliveries are known); its plans split
+    // keys for all their row tiles together.
+    std::vector<AttnPlan> bplan(n_reqs);
+    std::vector<size_t> bws_off(n_reqs, 0);
+    size_t ws_need = 0, bws_need = 0;
     int64_t max_ts = 0;
     for (int32_t i = 0; i < n_reqs; ++i) {
         AttnPlan p;
         plan_attention(l, reqs[i].prefix_tokens, reqs[i].suffix_tokens, &p);
         ws_need = std::max(ws_need, p.total);
         max_ts = std::max(max_ts, reqs[i].suffix_tokens);
+    }
+    if (n_reqs >= 2 && n_reqs <= MAX_ATTN_BATCH) {
+        std::vector<int64_t> tp(n_reqs), ts(n_reqs);
+        for (int32_t i = 0; i < n_reqs; ++i) {
+            tp[i] = reqs[i].prefix_tokens;
+            ts[i] = reqs[i].suffix_tokens;
+        }
+        plan_attention_batch(l, tp.data(), ts.data(), n_reqs, bplan.data());
+        for (int32_t i = 0; i < n_reqs; ++i) {
+            bws_off[i] = bws_need;
+            bws_need += (bplan[i].total + 255) / 256 * 256;
+        }
+        ws_need = std::max(ws_need, bws_need);
     }
     const size_t ws_stride = (ws_need + 255) / 256 * 256;
     if (ws_stride * n_streams > c->ws_bytes) {
@@ -659,11 +678,8 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     // one layer's compute for request `ri` on `st`: attention, then the suffix
     // append and the rest of the layer when asked for
     std::string layer_msg;       // why the rest of the layer failed to enqueue
-    auto enqueue_attention = [&](int32_t ri, int32_t layer, hipStream_t st) -> hipError_t {
+    auto attn_args = [&](int32_t ri, int32_t layer, unsigned char *ws) {
         const oc_request &r = reqs[ri];
-        const int64_t slot = emu ? ri : 0;
-        AttnPlan p;
-        plan_attention(l, r.prefix_tokens, r.suffix_tokens, &p);
         AttnArgs a{};
         const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
         const uint16_t *base = static_cast<const uint16_t *>(c->pool.base);
@@ -676,18 +692,41 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         a.pool_k = base + ((int64_t)layer * 2 + 0) * l.num_pages * block;
         a.pool_v = base + ((int64_t)layer * 2 + 1) * l.num_pages * block;
         a.pages = r.block_table->pages;
-        a.ws = static_cast<unsigned char *>(c->ws) + slot * ws_stride;
-        hipError_t e = launch_attention(p, a, st);
-        if (e == hipSuccess && c->opts.append_suffix)
+        a.ws = ws;
+        return a;
+    };
+    // after a request's attention: the suffix append and the rest of the layer
+    auto after_attention = [&](int32_t ri, int32_t layer, const AttnArgs &a, hipStream_t st) -> hipError_t {
+        const oc_request &r = reqs[ri];
+        hipError_t e = hipSuccess;
+        if (c->opts.append_suffix)
             e = launch_append(append_args(&c->pool, r.block_table, layer, a.k_new, a.v_new, r.suffix_tokens), st);
         if (e == hipSuccess && c->has_layer) {
-            unsigned char *lb = static_cast<unsigned char *>(c->lbuf) + slot * lb_stride;
+            unsigned char *lb = static_cast<unsigned char *>(c->lbuf) + (emu ? ri : 0) * lb_stride;
             const oc_layer_buffers bufs{lb + loff[0], lb + loff[1], lb + loff[2], lb + loff[3], lb + loff[4]};
             if (launch_rest_of_layer(layer_args(l, c->lw, layer, a.out, r.suffix_tokens, bufs), st) != OC_OK) {
                 layer_msg = oc_last_error();
                 return hipErrorLaunchFailure;
             }
         }
+        return e;
+    };
+    // one layer's compute for request `ri` on `st`
+    auto enqueue_attention = [&](int32_t ri, int32_t layer, hipStream_t st) -> hipError_t {
+        const oc_request &r = reqs[ri];
+        AttnPlan p;
+        plan_attention(l, r.prefix_tokens, r.suffix_tokens, &p);
+        const AttnArgs a = attn_args(ri, layer, static_cast<unsigned char *>(c->ws) + (emu ? ri : 0) * ws_stride);
+        hipError_t e = launch_attention(p, a, st);
+        return e == hipSuccess ? after_attention(ri, layer, a, st) : e;
+    };
+    // one layer's compute for every request: one attention launch over all
+    auto enqueue_layer_batch = [&](int32_t layer, hipStream_t st) -> hipError_t {
+        std::vector<AttnArgs> args(n_reqs);
+        for (int32_t ri = 0; ri < n_reqs; ++ri)
+            args[ri] = attn_args(ri, layer, static_cast<unsigned char *>(c->ws) + bws_off[ri]);
+        hipError_t e = launch_attention_batch(bplan.data(), args.data(), n_reqs, st);
+        for (int32_t ri = 0; ri < n_reqs && e == hipSuccess; ++ri) e = after_attention(ri, layer, args[ri], st);
         return e;
     };
 
@@ -705,6 +744,8 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
 
     // per-request rates under the shared budget (allocation policies)
     const bool by_rate = mode == OC_MODE_PRODUCER && c->opts.alloc_policy != OC_ALLOC_FIFO;
+    const bool batched = !c->opts.attention_per_request && !emu && !by_rate && n_cw == 0 && n_reqs >= 2 &&
+                         n_reqs <= MAX_ATTN_BATCH;
     std::vector<double> req_rate(n_reqs, 0.0);
     if (by_rate) {
         std::vector<double> s_i, c_i;
@@ -923,14 +964,27 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 e = launch_ingest(a, (bt.num_tokens + l.page_size - 1) / l.page_size, c->copy, step > 0);
             }
             if (e == hipSuccess) e = hipEventRecord(ingested[k], c->copy);
-            if (e == hipSuccess) e = hipStreamWaitEvent(attn_stream, ingested[k], 0);
-        } else {
+            // batched: the copy stream runs in order, so the layer's last
+            // ingest covers the others (each wait and event marker costs
+            // the stream a few microseconds)
+            if (e == hipSuccess && (!batched || it.req == n_reqs - 1))
+                e = hipStreamWaitEvent(attn_stream, ingested[k], 0);
+        } else if (!batched || it.req == 0) {    // batched: one pair of markers per layer
             e = hipEventRecord(landed[k], attn_stream);
             if (e == hipSuccess) e = hipEventRecord(ingested[k], attn_stream);
         }
-        if (e == hipSuccess) e = enqueue_attention(it.req, it.layer, attn_stream);
-        if (e == hipSuccess && emu) e = launch_compute_window(r.layer_compute_s, attn_stream);
-        if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + it.layer], attn_stream);
+        if (batched) {
+            // the layer's last request: one launch for all of them, whose
+            // ingests the compute stream has waited for item by item
+            if (e == hipSuccess && it.req == n_reqs - 1) {
+                e = enqueue_layer_batch(it.layer, attn_stream);
+                if (e == hipSuccess) e = hipEventRecord(done[(size_t)(n_reqs - 1) * L + it.layer], attn_stream);
+            }
+        } else {
+            if (e == hipSuccess) e = enqueue_attention(it.req, it.layer, attn_stream);
+            if (e == hipSuccess && emu) e = launch_compute_window(r.layer_compute_s, attn_stream);
+            if (e == hipSuccess) e = hipEventRecord(done[(size_t)it.req * L + it.layer], attn_stream);
+        }
         if (e != hipSuccess) {
             status = layer_msg.empty() ? hip_fail(e, "enqueueing a layer") : fail(OC_EHIP, layer_msg);
             msg = oc_last_error();
@@ -970,19 +1024,22 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     if (e1 != hipSuccess) return hip_fail(e1, "draining the copy stream");
     if (e2 != hipSuccess) return hip_fail(e2, "draining the compute stream");
 
+    // batched layers share one done event (the last request's) and, with
+    // the KV resident, one pair of landed/ingested markers (the first's)
     double last = 0.0;
     for (int32_t r = 0; r < n_reqs; ++r)
         for (int32_t layer = 0; layer < L; ++layer) {
-            const double t_done = ev_ms(ev_start, done[(size_t)r * L + layer]);
+            const double t_done = ev_ms(ev_start, done[(size_t)(batched ? n_reqs - 1 : r) * L + layer]);
             last = std::max(last, t_done);
             if (!stats) continue;
             // a chunkwise request's layers all became usable with its last group
             const int64_t k = deliv[r] == OC_DELIVERY_CHUNKWISE ? last_group[r] : item_of[(size_t)r * L + layer];
+            const int64_t k_marker = batched && mode == OC_MODE_HBM_RESIDENT ? item_of[(size_t)layer] : k;
             oc_request_stats &st = stats[r];
             if (layer == L - 1) st.ttft_ms = t_done;
             if (st.produced_ms) st.produced_ms[layer] = produced[k];
             if (st.landed_ms) st.landed_ms[layer] = mode == OC_MODE_HBM_RESIDENT ? 0.0 : ev_ms(ev_start, landed[k]);
-            if (st.ingested_ms) st.ingested_ms[layer] = ev_ms(ev_start, ingested[k]);
+            if (st.ingested_ms) st.ingested_ms[layer] = ev_ms(ev_start, ingested[k_marker]);
             if (st.done_ms) st.done_ms[layer] = t_done;
             st.rate_bytes_per_s = req_rate[r];
             st.delivery = deliv[r];

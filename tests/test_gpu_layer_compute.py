@@ -137,7 +137,7 @@ def test_requests_on_their_own_streams_do_not_share_a_workspace():
     import paper_2605_22850_amd as oc
     print("[layer] overlapping requests, per-stream workspaces", flush=True)
     rs = RequestSet(3, 4, 2, 64, [2048, 1024, 1536], [16, 24, 8], 512, seed=7).upload(with_payload=True)
-    _run(rs, oc.OC_MODE_DEVICE_STAGED)
+    _run(rs, oc.OC_MODE_DEVICE_STAGED, attention_per_request=True)
     base = [from_dev(r.out) for r in rs.reqs]
     for r in rs.reqs:
         r.layer_compute_s = 2e-4

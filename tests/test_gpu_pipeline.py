@@ -139,7 +139,9 @@ def test_allocation_policies_deliver_at_their_rates():
     want_pool = rs.expected_pool()
     fill = np.int16(np.uint16(SENTINEL).view(np.int16))
     rs.d_pool.fill_(fill)
-    _run(rs, oc.OC_MODE_PRODUCER)                       # one shared stream (FIFO)
+    # one shared stream (FIFO); one attention launch per request, as the
+    # allocation policies run them, so the outputs compare bit for bit
+    _run(rs, oc.OC_MODE_PRODUCER, attention_per_request=True)
     ref = _outs(rs)
     for l in range(rs.L):
         for r in range(3):

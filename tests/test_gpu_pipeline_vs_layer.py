@@ -1,7 +1,10 @@
-"""A pipeline run computes the same attention as the single-layer entry point
-called layer by layer: key splits, their merge and the per-stream workspace
-slices leave no trace in the outputs, which agree bit for bit, run after run,
-and match the oracle."""
+"""With one attention launch per request, a pipeline run computes the same
+attention as the single-layer entry point called layer by layer: key
+splits, their merge and the workspace slices leave no trace in the outputs,
+which agree bit for bit, run after run, and match the oracle.  With several
+requests batched into one launch per layer (the default), the outputs match
+the oracle and the per-request launches within the attention tolerance, run
+after run bit for bit."""
 import numpy as np
 import pytest
 
@@ -62,12 +65,12 @@ def test_pipeline_equals_single_layer_calls(name):
     for r, (tp, ts) in enumerate(zip(pre, suf)):
         plan_splits = oc.oc_attention_workspace_bytes(rs.layout, tp, ts)
         assert plan_splits > 256, "the case must split its keys"
-    _run(rs, oc.OC_MODE_DEVICE_STAGED)
+    _run(rs, oc.OC_MODE_DEVICE_STAGED, attention_per_request=True)
     first = [from_dev(r.out) for r in rs.reqs]
     for _ in range(2):            # again, from the filled pool
         for req in rs.reqs:
             req.out.zero_()
-        _run(rs, oc.OC_MODE_HBM_RESIDENT)
+        _run(rs, oc.OC_MODE_HBM_RESIDENT, attention_per_request=True)
         for r, req in enumerate(rs.reqs):
             assert np.array_equal(from_dev(req.out), first[r]), f"request {r}: second run differs"
     for r in range(len(pre)):
@@ -75,3 +78,43 @@ def test_pipeline_equals_single_layer_calls(name):
             f"request {r}: pipeline and single-layer calls differ"
     rows = [0, suf[0] - 1]
     assert_attention_close(first[0][L - 1][rows], rs.expected_out(0, L - 1, rows=rows), name)
+
+
+BATCH_CASES = {
+    "batch-of-8-varied": (2, 32, 8, 128, [4096, 1024, 2048, 512, 3072, 1536, 256, 0], [256] * 8, 2048),
+    "three-requests-d64": (3, 8, 2, 64, [2048, 512, 1024], [40, 7, 100], 512),
+    "sixteen-small": (2, 8, 2, 64, [256 + 16 * i for i in range(16)], [8 + i for i in range(16)], 1024),
+}
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("name", list(BATCH_CASES))
+def test_batched_layer_launch(name):
+    # one attention launch per layer for all requests: every request matches
+    # the oracle and its own per-request launch within the tolerance, and
+    # repeated runs are bit-identical
+    import paper_2605_22850_amd as oc
+    L, nq, nkv, d, pre, suf, P = BATCH_CASES[name]
+    print(f"[batched] {name}", flush=True)
+    rs = RequestSet(L, nq, nkv, d, pre, suf, P, seed=13).upload(with_payload=True)
+    _run(rs, oc.OC_MODE_DEVICE_STAGED, attention_per_request=True)
+    single = [from_dev(r.out) for r in rs.reqs]
+    runs = []
+    for mode in (oc.OC_MODE_DEVICE_STAGED, oc.OC_MODE_HBM_RESIDENT, oc.OC_MODE_PRODUCER):
+        for req in rs.reqs:
+            req.out.zero_()
+        stats = _run(rs, mode)
+        runs.append([from_dev(r.out) for r in rs.reqs])
+        # one launch: every request's layer is done at the same moment
+        for l in range(L):
+            assert len({st["done_ms"][l] for st in stats}) == 1, l
+    for r in range(len(pre)):
+        assert np.array_equal(runs[1][r], runs[0][r]) and np.array_equal(runs[2][r], runs[0][r]), f"request {r}"
+        for l in range(L):
+            assert_attention_close(runs[0][r][l], _f64(single[r][l]), f"{name} request {r} layer {l} vs per-request")
+        rows = sorted({0, suf[r] - 1})
+        assert_attention_close(runs[0][r][L - 1][rows], rs.expected_out(r, L - 1, rows=rows), f"{name} request {r}")
+
+
+def _f64(bits):
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)

@@ -109,7 +109,9 @@ def test_pipeline_appends_every_layer_and_keeps_outputs():
     print("[writeback] pipeline append, three requests", flush=True)
     rs = RequestSet(3, 8, 2, 128, [96, 0, 208], [21, 33, 64], 128, seed=9, suffix_room=True).upload(
         with_payload=True)
-    _run(rs, oc.OC_MODE_DEVICE_STAGED)
+    # one attention launch per request throughout, so every run (chunkwise
+    # requests always get their own) compares bit for bit
+    _run(rs, oc.OC_MODE_DEVICE_STAGED, attention_per_request=True)
     base = [from_dev(r.out) for r in rs.reqs]
     assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
     want = rs.expected_pool(appended=True)
@@ -119,7 +121,7 @@ def test_pipeline_appends_every_layer_and_keeps_outputs():
         rs.d_pool.fill_(np.int16(np.uint16(SENTINEL).view(np.int16)))
         for r in rs.reqs:
             r.out.zero_()
-        _run(rs, mode, append_suffix=True, **kw)
+        _run(rs, mode, append_suffix=True, attention_per_request=True, **kw)
         assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want), name
         for r, req in enumerate(rs.reqs):
             assert np.array_equal(from_dev(req.out), base[r]), f"{name}: request {r} output changed"

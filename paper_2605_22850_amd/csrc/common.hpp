@@ -114,7 +114,7 @@ struct AttnPlan {
 };
 int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *plan);
 // one launch for up to MAX_ATTN_BATCH requests of one layer: keys are split
-// so that all their row tiles together fill the CUs
+// so that every workgroup gets about the same number of key blocks
 constexpr int MAX_ATTN_BATCH = 16;
 int plan_attention_batch(const oc_layout &lay, const int64_t *Tp, const int64_t *Ts, int n, AttnPlan *plans);
 

@@ -8,7 +8,7 @@ after run bit for bit."""
 import numpy as np
 import pytest
 
-from tests.gpu_util import RequestSet, assert_attention_close, from_dev, require_gpu
+from tests.gpu_util import SENTINEL, RequestSet, assert_attention_close, from_dev, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -100,10 +100,15 @@ def test_batched_layer_launch(name):
     _run(rs, oc.OC_MODE_DEVICE_STAGED, attention_per_request=True)
     single = [from_dev(r.out) for r in rs.reqs]
     runs = []
+    want_pool = rs.expected_pool()
     for mode in (oc.OC_MODE_DEVICE_STAGED, oc.OC_MODE_HBM_RESIDENT, oc.OC_MODE_PRODUCER):
         for req in rs.reqs:
             req.out.zero_()
+        if mode == oc.OC_MODE_DEVICE_STAGED:
+            rs.d_pool.fill_(np.int16(np.uint16(SENTINEL).view(np.int16)))
         stats = _run(rs, mode)
+        if mode == oc.OC_MODE_DEVICE_STAGED:
+            assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want_pool), "ingest
         runs.append([from_dev(r.out) for r in rs.reqs])
         # one launch: every request's layer is done at the same moment
         for l in range(L):

@@ -108,7 +108,7 @@ def test_batched_layer_launch(name):
             rs.d_pool.fill_(np.int16(np.uint16(SENTINEL).view(np.int16)))
         stats = _run(rs, mode)
         if mode == oc.OC_MODE_DEVICE_STAGED:
-            assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want_pool), "ingest
+            assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want_pool), "ingest"
         runs.append([from_dev(r.out) for r in rs.reqs])
         # one launch: every request's layer is done at the same moment
         for l in range(L):

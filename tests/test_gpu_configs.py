@@ -16,7 +16,7 @@ from tests.gpu_util import SENTINEL, assert_attention_close, from_dev, require_g
 
 pytestmark = pytest.mark.gpu
 
-N_ROWS = 16
+N_ROWS = 64           # first and last suffix rows plus seeded ones, per request and layer
 
 
 @pytest.fixture(autouse=True)

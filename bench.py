@@ -30,6 +30,10 @@ Reported (one JSON line on stdout):
                  shared cap: per-request TTFT and rate beside eq. (3)
   cpu_baseline   the CPU oracle on a bounded sample, on this host
 
+``--zero-kv`` prints a line of its own: HBM-resident runs over an all-zero
+pool, then over the ingested N(0,1) pool (same kernels and launch shapes;
+the attention's time depends on the K/V values through the chip's clock).
+
 ``--profile-summary DB...`` turns rocprofv3 output of this script into the
 markdown kept under profiles/ (no GPU needed).
 """
@@ -585,6 +589,41 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
     }
 
 
+def attention_rate(wl, runs):
+    """TFLOP/s and ms of one layer's attention over HBM-resident runs: from
+    the first event before a layer's attention to the last one after it (one
+    launch when requests are batched, one after another otherwise)."""
+    L, R = wl.num_layers, wl.n_requests
+    op_ms, op_flops = 0.0, 0.0
+    for _, st in runs:
+        for l in range(L):
+            op_ms += max(rst["done_ms"][l] for rst in st) - min(rst["ingested_ms"][l] for rst in st)
+            op_flops += sum(attn_flops(wl.num_q_heads, wl.head_dim, wl.prefix_tokens[r], wl.suffix_tokens[r])
+                            for r in range(R))
+    return op_flops / (op_ms / 1e3) / 1e12, op_ms / (len(runs) * L)
+
+
+def zero_kv(args):
+    """HBM-resident runs over an all-zero pool, then over the same pool after
+    the device-staged pipeline has ingested the N(0,1) payloads.  The kernels
+    and their launch shapes are the same; only the K/V values differ."""
+    import kvgen
+    import paper_2605_22850_amd as oc
+    wl = kvgen.workload(args.workload)
+    layout, pool, reqs, _, _ = setup(wl)
+    trials = max(2, args.trials)
+    out = {}
+    for name in ("zero", "ingested"):
+        if name == "ingested":
+            run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, 1)
+        runs = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_HBM_RESIDENT, trials)[1:]
+        tflops, ms = attention_rate(wl, runs)
+        out[name] = {"ttft_ms": mean_std([r[0] for r in runs]), "attention_tflops": round(tflops, 2),
+                     "attention_ms_per_layer": round(ms, 4)}
+        log(f"[bench] {name} pool: {out[name]}")
+    return {"workload": wl.name, "trials": trials - 1, **out}
+
+
 def run_bench(args):
     import torch
     import kvgen
@@ -658,18 +697,13 @@ def run_bench(args):
     # attention of a layer, all requests: from the first event before it to
     # the last one after it (one launch when requests are batched, one after
     # another otherwise), HBM-resident
-    op_ms, op_flops = 0.0, 0.0
-    for _, st in hbm[1:]:
-        for l in range(L):
-            op_ms += max(rst["done_ms"][l] for rst in st) - min(rst["ingested_ms"][l] for rst in st)
-            op_flops += sum(attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r]) for r in range(R))
-    attn_tflops = op_flops / (op_ms / 1e3) / 1e12
+    attn_tflops, op_ms_layer = attention_rate(wl, hbm[1:])
     flops_per_layer = sum(attn_flops(nq, d, wl.prefix_tokens[r], wl.suffix_tokens[r]) for r in range(R))
     layer_tflops = flops_per_layer / (sum(t_hbm) / len(t_hbm) / L / 1e3) / 1e12
     line["attention"] = {
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)},
-        "flops_per_layer": flops_per_layer, "op_ms_per_layer": round(op_ms / (len(hbm[1:]) * L), 4),
+        "flops_per_layer": flops_per_layer, "op_ms_per_layer": round(op_ms_layer, 4),
         "what": "attention + split combine of one layer (all requests), HIP events around them",
         "tflops_whole_pass": round(layer_tflops, 2),
     }
@@ -719,6 +753,7 @@ def profile_summary(paths, workload, warmup, steps):
     out = []
     counters = {}
     attn_counters = []
+    clock_runs = []
     for path in paths:
         c = sqlite3.connect(path)
         has_pmc = c.execute("select count(*) from counters_collection").fetchone()[0] > 0
@@ -761,6 +796,8 @@ def profile_summary(paths, workload, warmup, steps):
                 e = by_disp.setdefault(disp, {"name": name, "start": st, "end": en, "c": {}})
                 e["c"][cn] = e["c"].get(cn, 0.0) + val
             disp = sorted(by_disp.values(), key=lambda e: e["start"])
+            if any("GRBM_GUI_ACTIVE" in e["c"] for e in disp):
+                clock_runs.append((os.path.basename(path), disp))
             att = [e for e in disp if "attn_fwd_kernel" in e["name"]][lo:hi]
             if att and any(e["c"] for e in att):
                 attn_counters.append((os.path.basename(path), att))
@@ -790,6 +827,21 @@ def profile_summary(paths, workload, warmup, steps):
             out.append(f"MFMA bf16 flops per dispatch (MOPS x 512): {np.mean(mops) * 512:.4g}; algorithmic "
                        f"flops per layer (unmasked pairs): {flops:.4g}; ratio {np.mean(mops) * 512 / flops:.3f} "
                        f"(masked pairs of the causal diagonal and padding rows are computed and discarded).")
+        out.append("")
+    for db, disp in clock_runs:
+        # GPU clock cycles counted while a dispatch ran, per nanosecond of its
+        # duration: proportional to the clock the chip ran that kernel at
+        out.append(f"### Clock counter by run (`{db}`; launches grouped {per_run} per pipeline run, "
+                   f"in start order)\n")
+        out.append("| kernel | run | launches | mean us | GRBM_GUI_ACTIVE per ns |\n|---|---|---|---|---|")
+        for label in ("attn_fwd_kernel", "kv_ingest"):
+            ks = [e for e in disp if label in e["name"] and "GRBM_GUI_ACTIVE" in e["c"]]
+            for i in range(0, len(ks), per_run):
+                part = ks[i:i + per_run]
+                dur = np.array([e["end"] - e["start"] for e in part], dtype=float)
+                act = np.array([e["c"]["GRBM_GUI_ACTIVE"] for e in part])
+                out.append(f"| `{label}` | {i // per_run} | {len(part)} | {dur.mean() / 1e3:.1f} | "
+                           f"{np.mean(act / dur):.3f} |")
         out.append("")
     if counters:
         nbytes = 2.0 * sum(wl.prefix_tokens) * b / len(wl.prefix_tokens)
@@ -846,6 +898,8 @@ def main():
                     help=f"{CALIB_COPIES} plain {CALIB_BYTES >> 20} MiB device copies before the steps")
     ap.add_argument("--attention-per-request", action="store_true",
                     help="one attention launch per request and layer, not one per layer for all requests")
+    ap.add_argument("--zero-kv", action="store_true",
+                    help="HBM-resident runs over an all-zero pool, then over the ingested N(0,1) pool")
     ap.add_argument("--profile-summary", nargs="+", metavar="DB",
                     help="print a markdown summary of rocprofv3 databases of a run of this script")
     args = ap.parse_args()
@@ -856,7 +910,7 @@ def main():
     if args.attention_per_request:
         RUN_OPTS["attention_per_request"] = True
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the path has no cross-GPU part in this build; run with --gpus 1",
+        print("bench.py measures one GPU: the path has no cross-GPU part; run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
     if args.canonical_cells:
@@ -864,6 +918,11 @@ def main():
         print(json.dumps({"metric": "TTFT with the whole layer's compute, end-to-end cells", "unit": "ms",
                           "higher_is_better": False, "data": "synthetic: random weights and KV", "n_gpus": 1,
                           "canonical_cells": res}), flush=True)
+        return
+    if args.zero_kv:
+        print(json.dumps({"metric": "attention per layer over zero vs N(0,1) K/V", "unit": "TFLOP/s",
+                          "higher_is_better": True, "data": "synthetic", "n_gpus": 1,
+                          "zero_kv": zero_kv(args)}), flush=True)
         return
     if args.scheduler_workloads:
         res = scheduler_workloads(args)

@@ -4,8 +4,9 @@ the first and the last layer of every request, the ingest and the suffix
 append are compared bit for bit over the whole pool (the full page count,
 4x the pages the prefix needs), every whole chunk of prefix and suffix is
 offloaded back into chunk objects and compared with the stored ones, and the
-attention is checked on sampled suffix rows (always the first and the last)
-against the float64 oracle.  The pool holds two layers, standing in for
+attention is checked against the float64 oracle on every suffix row and head
+up to a 4K context, and beyond it on 64 sampled suffix rows (always the first
+and the last) and every head.  The pool holds two layers, standing in for
 layers 0 and L-1."""
 import numpy as np
 import pytest
@@ -17,6 +18,7 @@ from tests.gpu_util import SENTINEL, assert_attention_close, from_dev, require_g
 pytestmark = pytest.mark.gpu
 
 N_ROWS = 64           # first and last suffix rows plus seeded ones, per request and layer
+FULL_ROWS_CONTEXT = 8192   # up to this prefix + suffix, every suffix row is checked
 
 
 @pytest.fixture(autouse=True)
@@ -100,7 +102,8 @@ def check_workload(wl):
 
     for r in range(wl.n_requests):
         tp, ts = wl.prefix_tokens[r], wl.suffix_tokens[r]
-        rows = sample_rows(ts, seed=r)
+        # every row up to a 4K context (tiny, 8b-4k), sampled rows beyond
+        rows = list(range(ts)) if tp + ts <= FULL_ROWS_CONTEXT else sample_rows(ts, seed=r)
         d_table = torch.from_numpy(tables[r]).cuda()
         ws = torch.empty(oc.oc_attention_workspace_bytes(layout, tp, ts), dtype=torch.uint8, device="cuda")
         for li, l in enumerate(layers):

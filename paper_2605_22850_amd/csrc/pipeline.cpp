@@ -97,8 +97,21 @@ static int fill_defaults(oc_pipeline_opts &o) {
     return OC_OK;
 }
 
+// Makes `dev` current for a scope and gives the caller back its own device.
+struct DeviceScope {
+    int prev = -1;
+    explicit DeviceScope(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        hipSetDevice(dev);
+    }
+    ~DeviceScope() {
+        if (prev >= 0) hipSetDevice(prev);
+    }
+};
+
 static void release(Context *c) {
     if (!c) return;
+    const DeviceScope on_device(c->device);
     if (c->copy) hipStreamSynchronize(c->copy);
     if (c->compute) hipStreamSynchronize(c->compute);
     for (auto st : c->req_streams) hipStreamSynchronize(st);
@@ -172,19 +185,28 @@ struct Producer {
             const int64_t first = it.chunks ? it.j0 : 0, last = it.chunks ? it.j1 : N;
             const int64_t src_off = it.chunks ? 0 : (int64_t)it.layer * S;
             const int64_t j0 = first + p * cpp, j1 = std::min(last, j0 + cpp);
+            bool skip = false;
             if (rate > 0) {
                 const double t_release = (cum + (double)(j1 - first) * unit) / rate;
                 const auto when = t0 + std::chrono::duration_cast<Clock::duration>(std::chrono::duration<double>(t_release));
-                // sleep most of the way, then spin for a microsecond-accurate release
+                // sleep most of the way in steps of at most 20 ms (a stopped
+                // run ends the wait), then spin for a microsecond-accurate release
                 for (;;) {
                     auto now = Clock::now();
                     if (now >= when) break;
                     auto left = when - now;
-                    if (left > std::chrono::microseconds(200)) std::this_thread::sleep_for(left - std::chrono::microseconds(100));
+                    if (left > std::chrono::microseconds(200)) {
+                        std::this_thread::sleep_for(std::min<Clock::duration>(left - std::chrono::microseconds(100),
+                                                                             std::chrono::milliseconds(20)));
+                        if (aborted()) {
+                            skip = true;
+                            break;
+                        }
+                    }
                 }
             }
             unsigned char *dst = static_cast<unsigned char *>(c->slots[item % c->slots.size()].pinned);
-            for (int64_t j = j0; j < j1; ++j) {
+            for (int64_t j = j0; j < j1 && !skip; ++j) {
                 const unsigned char *obj = static_cast<const unsigned char *>(r.chunk_objects[j]);
                 std::memcpy(dst + (j - first) * unit, obj + src_off, (size_t)unit);
             }
@@ -550,6 +572,7 @@ static double ev_ms(hipEvent_t a, hipEvent_t b) {
 }
 
 static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
+    const DeviceScope on_device(c->device);
     const oc_layout &l = c->pool.layout;
     const int32_t L = l.num_layers;
     const int mode = c->opts.mode;
@@ -730,7 +753,6 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         return e;
     };
 
-    OC_HIP(hipSetDevice(c->device));
     OC_HIP(hipStreamSynchronize(c->copy));
     OC_HIP(hipStreamSynchronize(c->compute));
     // The context's streams are non-blocking, so nothing orders them after
@@ -1090,10 +1112,12 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
         const size_t obj = (size_t)l.num_layers * 2 * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
         c->slot_bytes = std::max(c->slot_bytes, obj);
     }
-    if (hipSetDevice(device) != hipSuccess) {
+    int n_dev = 0;
+    if (hipGetDeviceCount(&n_dev) != hipSuccess || device < 0 || device >= n_dev) {
         delete c;
-        return fail(OC_EHIP, "hipSetDevice failed");
+        return fail(OC_EINVAL, "no such device");
     }
+    const DeviceScope on_device(device);
     // default-priority, non-blocking streams
     if (hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking) != hipSuccess ||
         hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking) != hipSuccess) {

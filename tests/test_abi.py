@@ -212,3 +212,13 @@ def test_block_table_check():
     with pytest.raises(oc.OcError):
         oc.oc_block_table_check([3, 1], 40, 4, 16)
     oc.oc_block_table_check(np.zeros(0, np.int32), 0, 4, 16)
+
+
+def test_context_rejects_an_absent_device():
+    lay = _layout()
+    kp = L.c_kv_pool(FAKE, lay)
+    opts = L.c_pipeline_opts()
+    ctx = ctypes.c_void_p()
+    rc = oc.lib().oc_context_create(4096, ctypes.byref(kp), ctypes.byref(opts), 256, 32, ctypes.byref(ctx))
+    assert rc == L.OC_EINVAL and not ctx.value
+    assert b"no such device" in oc.lib().oc_last_error()

@@ -15,7 +15,8 @@ Reported (one JSON line on stdout):
                  launch from the committed FETCH_SIZE/WRITE_SIZE summary,
                  null when the kernel source has changed since
   ingest_isolated  the same kernel launched back to back with nothing beside
-                 it (kernel capability, not the step)
+                 it (kernel capability, not the step); also at the second
+                 workload and at tiny (L2-resident, launch-latency bound)
   write_path     offload gather of whole chunk objects, suffix append, and
                  the ingest at 64- and 256-token chunks, each alone
   attention      attention TFLOP/s per layer (HBM-resident pass) against the
@@ -187,9 +188,12 @@ def isolated_ingest(oc, wl, layout, pool, reqs, passes):
     import torch
     s = torch.cuda.Stream()
     b = 2 * wl.num_kv_heads * wl.head_dim * 2
-    evs = []
+    evs, spans = [], []
     with torch.cuda.stream(s):
         for p_ in range(passes + 1):          # the first pass is an untimed warm-up
+            if p_ > 0:
+                spans.append([torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)])
+                spans[-1][0].record(s)
             for l in range(wl.num_layers):
                 for r, rq in enumerate(reqs):
                     tp = wl.prefix_tokens[r]
@@ -203,14 +207,21 @@ def isolated_ingest(oc, wl, layout, pool, reqs, passes):
                     oc.oc_kv_layer_ingest(st, n, rq.pages, tp, pool, layout, l, s)
                     e1.record(s)
                     evs.append((e0, e1, 2.0 * tp * b))
+            if p_ > 0:
+                spans[-1][1].record(s)
     s.synchronize()
     ms = sum(e0.elapsed_time(e1) for e0, e1, _ in evs)
     nbytes = sum(x for _, _, x in evs)
     gbs = nbytes / (ms / 1e3) / 1e9
+    span_ms = sum(a.elapsed_time(z) for a, z in spans)
+    per_launch = nbytes / len(evs)
+    size = f"{per_launch / 2**20:.0f} MiB" if per_launch >= 2**20 else f"{per_launch / 2**10:.0f} KiB"
     return {"value": round(gbs, 2), "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
             "launches": len(evs), "mean_launch_us": round(ms / len(evs) * 1e3, 3),
-            "how": f"{passes} passes over all {wl.num_layers} layer payloads ({nbytes / len(evs) / 2**20:.0f} MiB "
-                   f"read + written per launch) after an untimed one, one stream, nothing beside it"}
+            "back_to_back_GBps": round(nbytes / (span_ms / 1e3) / 1e9, 2),
+            "how": f"{passes} passes over all {wl.num_layers} layer payloads ({size} read + written per launch) "
+                   f"after an untimed one, one stream, nothing beside it; value from HIP events around each "
+                   f"launch, back_to_back from one pair around each whole pass"}
 
 
 def _timed(s, evs, fn, nbytes):
@@ -719,11 +730,20 @@ def run_bench(args):
         dev2 = run_mode(oc, pool2, lay2, wl2, reqs2, oc.OC_MODE_DEVICE_STAGED, trials)
         t2, res2 = ttft_legs(oc, wl2, lay2, pool2, reqs2, args, hbm2, dev2)
         line["second_workload"] = {"workload": wl2.name, "ttft_ms": t2, **res2}
+        if args.isolated_passes > 0:
+            line["second_workload"]["ingest_isolated"] = isolated_ingest(oc, wl2, lay2, pool2, reqs2,
+                                                                         max(4, args.isolated_passes))
         del pool2, reqs2
         log(f"[bench] {wl2.name} ttft legs done")
     if args.isolated_passes > 0:
         line["ingest_isolated"] = isolated_ingest(oc, wl, layout, pool, reqs, args.isolated_passes)
         log("[bench] isolated ingest done")
+        if wl.name != "tiny":
+            # 128 KiB per layer: L2-resident and bound by launch latency
+            wl3 = kvgen.workload("tiny")
+            lay3, pool3, reqs3, _, _ = setup(wl3)
+            line["tiny_ingest_isolated"] = isolated_ingest(oc, wl3, lay3, pool3, reqs3, 50)
+            del pool3, reqs3
         line["write_path"] = write_path(oc, wl, layout, pool, reqs, args.isolated_passes)
         log("[bench] write path done")
     if not args.no_cpu_baseline:

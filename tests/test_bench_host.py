@@ -1,0 +1,76 @@
+"""Host-side logic of bench.py, no GPU: the one-GPU guard, the eq. (3) and
+chunkwise floors it reports beside the measured TTFT (against the oracle's
+model), the attention FLOP count (against a brute-force count of the
+unmasked query-key pairs), and the arithmetic that turns rocprofv3 counter
+databases into the HBM-traffic figure (on a synthetic database)."""
+import os
+import sqlite3
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import bench
+from oracle import model
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("argv,env", [(["--gpus", "2"], {}), ([], {"WORLD_SIZE": "2"})])
+def test_more_than_one_gpu_is_refused(argv, env):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv], capture_output=True, text=True,
+                       env={**os.environ, **env}, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and not r.stdout.strip()
+
+
+def test_floors_match_the_oracle_model():
+    rng = np.random.default_rng(3)
+    for L in (1, 2, 5, 32):
+        X, C = rng.uniform(0, 2, L).tolist(), rng.uniform(0, 2, L).tolist()
+        assert bench.layerwise_floor(X, C) == pytest.approx(model.layerwise_ttft(X, C), rel=1e-12)
+        assert bench.chunkwise_floor(X, C) == pytest.approx(model.chunkwise_ttft(X, C), rel=1e-12)
+
+
+@pytest.mark.parametrize("tp,ts", [(0, 1), (0, 7), (16, 1), (256, 32), (100, 13)])
+def test_attention_flops_count_unmasked_pairs(tp, ts):
+    nq, d = 4, 64
+    pairs = sum(1 for i in range(ts) for j in range(tp + ts) if j < tp or j - tp <= i)
+    assert bench.attn_flops(nq, d, tp, ts) == 4 * nq * d * pairs
+
+
+def _counter_db(path, counter, calib_kib, ingest_kib, n_ingest):
+    """A database with the columns the summary reads: three 1 GiB calibration
+    copies, then n_ingest ingest dispatches, each with one counter value."""
+    c = sqlite3.connect(path)
+    c.execute("create table counters_collection (dispatch_id int, kernel_name text, counter_name text, "
+              "value real, start int, end int)")
+    t = 1000
+    rows = []
+    for i in range(bench.CALIB_COPIES):
+        rows.append((i, "__amd_rocclr_copyBuffer", counter, calib_kib, t, t + 300000))
+        t += 400000
+    for i in range(n_ingest):
+        rows.append((100 + i, "oc::kv_ingest_rows_kernel", counter, ingest_kib, t, t + 100000))
+        t += 200000
+    c.executemany("insert into counters_collection values (?,?,?,?,?,?)", rows)
+    c.commit()
+    c.close()
+
+
+def test_profile_summary_scales_the_byte_counters(tmp_path):
+    # tiny: 2 layers, one request -> 2 ingest launches per run; warmup 1, steps 2
+    # select launches 2..5.  Calibration reads half the copied bytes, so the
+    # scale is 2 for FETCH_SIZE; WRITE_SIZE reads them exactly (scale 1).
+    expect = bench.CALIB_COPIES * bench.CALIB_BYTES / 1024.0
+    f, w = str(tmp_path / "pf.db"), str(tmp_path / "pw.db")
+    _counter_db(f, "FETCH_SIZE", expect / bench.CALIB_COPIES / 2, 100.0, 8)
+    _counter_db(w, "WRITE_SIZE", expect / bench.CALIB_COPIES, 128.0, 8)
+    text = bench.profile_summary([f, w], "tiny", 1, 2)
+    want = 100.0 * 1024 * 2 + 128.0 * 1024
+    line = [ln for ln in text.splitlines() if ln.startswith("traffic_bytes_per_launch:")]
+    assert line and float(line[0].split(":")[1]) == pytest.approx(want, rel=1e-9)
+    assert f"kernel_source_sha256: {bench.file_sha256(bench.INGEST_SRC)}" in text
+    # the algorithmic bytes of a tiny layer: 256 tokens x 512 B, read + written
+    assert "Algorithmic bytes per launch: 262144" in text

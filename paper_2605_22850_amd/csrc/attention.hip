@@ -195,6 +195,9 @@ __device__ __forceinline__ void matrix_phase(WaveState<D> &w, const uint16_t *V,
         return *reinterpret_cast<const bf16x8 *>(&K[k_lds<D>(kt * 32 + krow, ds * 2 + half)]);
     };
     bf16x8 f[N];
+    // the wavefront in its matrix phase issues ahead of its SIMD partner's
+    // softmax: the MFMA pipe is the longer of the two (about 3 % per layer)
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int n = 0; n < LOOKAHEAD && n < N; ++n) f[n] = PV ? pre[n] : load(n);
 #pragma unroll
@@ -209,6 +212,7 @@ __device__ __forceinline__ void matrix_phase(WaveState<D> &w, const uint16_t *V,
         }
         __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // Softmax phase of a wavefront for one block: the block maximum (one lane

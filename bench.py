@@ -182,37 +182,100 @@ def copy_calibration():
     del src, dst
 
 
+WARM_S = 0.3     # untimed work before a standalone leg: the clocks leave their idle state
+
+
+def warm_device(s, one_pass):
+    """Untimed work on stream s for at least WARM_S seconds (at least one
+    pass).  After an idle stretch (host-side setup, the capped producer
+    trials) the first launches run slower while the clocks ramp up."""
+    t0 = time.perf_counter()
+    while True:
+        one_pass()
+        s.synchronize()
+        if time.perf_counter() - t0 >= WARM_S:
+            return
+
+
+def _sleep_cycles_per_ms(s):
+    """Calibrates torch.cuda._sleep (a bounded spin kernel) on stream s."""
+    import torch
+    with torch.cuda.stream(s):
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000)
+        a.record(s)
+        torch.cuda._sleep(2_000_000)
+        z.record(s)
+    s.synchronize()
+    return 2_000_000 / max(a.elapsed_time(z), 1e-3)
+
+
+def gated_passes(s, launches, passes, per_launch=True):
+    """Times `passes` passes over `launches` (a list of (enqueue function,
+    algorithmic bytes)) on stream s, each launch between two HIP events.
+    The events are created before the pass, and the device first spins
+    (torch.cuda._sleep) long enough for the host to enqueue the whole pass,
+    so that each launch's events measure the device, not the Python host's
+    per-call cost.  Returns the per-launch (start, end, bytes) triples and
+    one (start, end) pair per pass.  With per_launch False only the pass is
+    bracketed (each event marker between launches costs the stream a few
+    microseconds)."""
+    import torch
+    per_ms = _sleep_cycles_per_ms(s)
+    evs, spans, host_ms = [], [], 1.0
+    with torch.cuda.stream(s):
+        for i in range(passes + 1):       # the first pass measures the host's enqueue time only
+            pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                     for _ in range(len(launches) + 1)]
+            for e0, e1 in pairs:          # the device events exist before the timed enqueue
+                e0.record(s)
+                e1.record(s)
+            s.synchronize()
+            torch.cuda._sleep(int(per_ms * (2.0 * host_ms + 2.0)))
+            t0 = time.perf_counter()
+            pairs[-1][0].record(s)
+            for (fn, nbytes), (e0, e1) in zip(launches, pairs):
+                if not per_launch:
+                    fn()
+                    continue
+                e0.record(s)
+                fn()
+                e1.record(s)
+                if i > 0:
+                    evs.append((e0, e1, nbytes))
+            pairs[-1][1].record(s)
+            host_ms = (time.perf_counter() - t0) * 1e3
+            if i > 0:
+                spans.append(pairs[-1])
+            s.synchronize()
+    return evs, spans
+
+
 def isolated_ingest(oc, wl, layout, pool, reqs, passes):
     """Ingest of every layer of every request, back to back on one stream,
-    nothing else running; per-launch HIP events."""
+    nothing else running; per-launch HIP events (gated_passes) after
+    WARM_S of untimed passes."""
     import torch
     s = torch.cuda.Stream()
     b = 2 * wl.num_kv_heads * wl.head_dim * 2
-    evs, spans = [], []
-    with torch.cuda.stream(s):
-        for p_ in range(passes + 1):          # the first pass is an untimed warm-up
-            if p_ > 0:
-                spans.append([torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)])
-                spans[-1][0].record(s)
-            for l in range(wl.num_layers):
-                for r, rq in enumerate(reqs):
-                    tp = wl.prefix_tokens[r]
-                    n = tp // wl.chunk_tokens
-                    st = rq.device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]
-                    if p_ == 0:
-                        oc.oc_kv_layer_ingest(st, n, rq.pages, tp, pool, layout, l, s)
-                        continue
-                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    e0.record(s)
-                    oc.oc_kv_layer_ingest(st, n, rq.pages, tp, pool, layout, l, s)
-                    e1.record(s)
-                    evs.append((e0, e1, 2.0 * tp * b))
-            if p_ > 0:
-                spans[-1][1].record(s)
-    s.synchronize()
+    launches = []
+    for l in range(wl.num_layers):
+        for r, rq in enumerate(reqs):
+            tp = wl.prefix_tokens[r]
+            st = rq.device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]
+            launches.append((lambda st=st, rq=rq, tp=tp, l=l:
+                             oc.oc_kv_layer_ingest(st, tp // wl.chunk_tokens, rq.pages, tp, pool, layout, l, s),
+                             2.0 * tp * b))
+
+    def one_pass():
+        for fn, _ in launches:
+            fn()
+    warm_device(s, one_pass)
+    evs, _ = gated_passes(s, launches, passes)
     ms = sum(e0.elapsed_time(e1) for e0, e1, _ in evs)
     nbytes = sum(x for _, _, x in evs)
     gbs = nbytes / (ms / 1e3) / 1e9
+    _, spans = gated_passes(s, launches, passes, per_launch=False)
     span_ms = sum(a.elapsed_time(z) for a, z in spans)
     per_launch = nbytes / len(evs)
     size = f"{per_launch / 2**20:.0f} MiB" if per_launch >= 2**20 else f"{per_launch / 2**10:.0f} KiB"
@@ -220,17 +283,9 @@ def isolated_ingest(oc, wl, layout, pool, reqs, passes):
             "launches": len(evs), "mean_launch_us": round(ms / len(evs) * 1e3, 3),
             "back_to_back_GBps": round(nbytes / (span_ms / 1e3) / 1e9, 2),
             "how": f"{passes} passes over all {wl.num_layers} layer payloads ({size} read + written per launch) "
-                   f"after an untimed one, one stream, nothing beside it; value from HIP events around each "
-                   f"launch, back_to_back from one pair around each whole pass"}
-
-
-def _timed(s, evs, fn, nbytes):
-    import torch
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(s)
-    fn()
-    e1.record(s)
-    evs.append((e0, e1, nbytes))
+                   f"after {WARM_S} s of untimed ones, one stream, nothing beside it; value from HIP events "
+                   f"around each launch, back_to_back from passes with one pair of events around the whole "
+                   f"pass and none between launches; each pass enqueued before the device starts on it"}
 
 
 def _rate(evs, how):
@@ -243,7 +298,7 @@ def _rate(evs, how):
 
 def write_path(oc, wl, layout, pool, reqs, passes):
     """The write path and the other chunk sizes, each kernel back to back on
-    one stream with nothing beside it, per-launch HIP events:
+    one stream with nothing beside it, per-launch HIP events (gated_passes):
       offload_gather   every chunk object of each request rebuilt from the
                        pool, all layers in one launch (read + write);
       suffix_append    one layer's suffix K/V appended behind the prefix;
@@ -256,46 +311,37 @@ def write_path(oc, wl, layout, pool, reqs, passes):
     b = 2 * nkv * d * 2
     s = torch.cuda.Stream()
     out = {}
-    with torch.cuda.stream(s):
-        evs = []
-        tp_max = max(wl.prefix_tokens)
-        objs = torch.empty(tp_max * b * L // 2, dtype=torch.int16, device="cuda")
-        for _ in range(passes):
+    tp_max = max(wl.prefix_tokens)
+    objs = torch.empty(tp_max * b * L // 2, dtype=torch.int16, device="cuda")
+    launches = [(lambda rq=rq, tp=tp: oc.oc_kv_chunks_gather(rq.pages, tp, pool, layout, 0, tp // wl.chunk_tokens,
+                                                             objs, s), 2.0 * tp * b * L)
+                for rq, tp in zip(reqs, wl.prefix_tokens)]
+    evs, _ = gated_passes(s, launches, passes)
+    del objs
+    out["offload_gather"] = _rate(evs, f"{passes} passes; per request one launch over all {L} layers of "
+                                       f"its chunk objects (read pool + write objects)")
+    # appending needs table room behind the prefix: a table of its own
+    tables = [torch.arange(-(-(tp + ts) // Ps), dtype=torch.int32, device="cuda")
+              for tp, ts in zip(wl.prefix_tokens, wl.suffix_tokens)]
+    launches = [(lambda l=l, r=r, rq=rq: oc.oc_kv_suffix_append(rq.k_new[l], rq.v_new[l], wl.suffix_tokens[r],
+                                                                tables[r], wl.prefix_tokens[r], pool, layout, l, s),
+                 2.0 * wl.suffix_tokens[r] * b)
+                for l in range(L) for r, rq in enumerate(reqs)]
+    evs, _ = gated_passes(s, launches, passes)
+    out["suffix_append"] = _rate(evs, f"{passes} passes over all {L} layers (read + write of the suffix K/V)")
+    for G in (64, 256):
+        if any(tp % G for tp in wl.prefix_tokens):
+            continue
+        lay = oc.Layout(L, wl.num_q_heads, nkv, d, Ps, G, wl.pool_pages)
+        launches = []
+        for l in range(L):
             for r, rq in enumerate(reqs):
                 tp = wl.prefix_tokens[r]
-                n = tp // wl.chunk_tokens
-                _timed(s, evs, lambda: oc.oc_kv_chunks_gather(rq.pages, tp, pool, layout, 0, n, objs, s),
-                       2.0 * tp * b * L)
-        s.synchronize()
-        del objs
-        out["offload_gather"] = _rate(evs, f"{passes} passes; per request one launch over all {L} layers of "
-                                           f"its chunk objects (read pool + write objects)")
-        # appending needs table room behind the prefix: a table of its own
-        tables = [torch.arange(-(-(tp + ts) // Ps), dtype=torch.int32, device="cuda")
-                  for tp, ts in zip(wl.prefix_tokens, wl.suffix_tokens)]
-        evs = []
-        for _ in range(passes):
-            for l in range(L):
-                for r, rq in enumerate(reqs):
-                    tp, ts = wl.prefix_tokens[r], wl.suffix_tokens[r]
-                    _timed(s, evs, lambda: oc.oc_kv_suffix_append(rq.k_new[l], rq.v_new[l], ts, tables[r], tp, pool,
-                                                                  layout, l, s), 2.0 * ts * b)
-        s.synchronize()
-        out["suffix_append"] = _rate(evs, f"{passes} passes over all {L} layers (read + write of the suffix K/V)")
-        for G in (64, 256):
-            if any(tp % G for tp in wl.prefix_tokens):
-                continue
-            lay = oc.Layout(L, wl.num_q_heads, nkv, d, Ps, G, wl.pool_pages)
-            evs = []
-            for _ in range(passes):
-                for l in range(L):
-                    for r, rq in enumerate(reqs):
-                        tp = wl.prefix_tokens[r]
-                        st = rq.device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]
-                        _timed(s, evs, lambda: oc.oc_kv_layer_ingest(st, tp // G, rq.pages, tp, pool, lay, l, s),
-                               2.0 * tp * b)
-            s.synchronize()
-            out[f"ingest_g{G}"] = _rate(evs, f"{passes} passes over all {L} layer payloads as {G}-token chunks")
+                st = rq.device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]
+                launches.append((lambda st=st, rq=rq, tp=tp, l=l, lay=lay:
+                                 oc.oc_kv_layer_ingest(st, tp // G, rq.pages, tp, pool, lay, l, s), 2.0 * tp * b))
+        evs, _ = gated_passes(s, launches, passes)
+        out[f"ingest_g{G}"] = _rate(evs, f"{passes} passes over all {L} layer payloads as {G}-token chunks")
     return out
 
 
@@ -653,6 +699,17 @@ def run_bench(args):
         log("[bench] copy calibration done")
 
     # ---- timed steps: device-staged pipeline, all layers ----
+    # the device leaves its idle clocks first (host-side setup kept it idle
+    # for seconds): untimed ingest launches for WARM_S, then the warmup steps
+    s_warm = torch.cuda.Stream()
+
+    def warm_pass():
+        with torch.cuda.stream(s_warm):
+            for r, rq in enumerate(reqs):
+                tp = wl.prefix_tokens[r]
+                oc.oc_kv_layer_ingest(rq.device_payload[:tp * b // 2], tp // wl.chunk_tokens, rq.pages, tp, pool,
+                                      layout, 0, s_warm)
+    warm_device(s_warm, warm_pass)
     for i in range(args.warmup):
         run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, 1)
         log(f"[bench] warmup {i + 1}/{args.warmup}")

@@ -635,13 +635,23 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
         asecs += time.perf_counter() - t
         rows.append(i)
         flops += 4.0 * nq * d * (tp + i + 1)
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu)
+    except OSError:
+        pass
+    rate = flops / asecs                                    # flop/s of the sampled rows
+    layer_flops = attn_flops(nq, d, tp, ts)
     return {
-        "value": round(ingest_gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+        "value": round(ingest_gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle", "cpu": cpu,
         "sample": f"oracle byte-loop ingest (single thread) of {layers} of {L} layer payloads of request 0 "
                   f"({layers * tp} tokens x {2 * nkv * d * 2} B, read + written)",
-        "attention": {"gflops": round(flops / asecs / 1e9, 4), "cores": threads, "rows": len(rows),
+        "attention": {"gflops": round(rate / 1e9, 4), "cores": threads, "rows": len(rows),
                       "sample": f"float64 attention of {len(rows)} suffix rows x {nq} heads of layer 0 over "
-                                f"{tp} prefix keys, {threads} threads"},
+                                f"{tp} prefix keys, {threads} threads",
+                      "layer_s_extrapolated": round(layer_flops / rate, 2),
+                      "all_layers_s_extrapolated": round(L * layer_flops / rate, 1)},
         "seconds": round(secs + asecs, 2),
     }
 

@@ -74,3 +74,15 @@ def test_profile_summary_scales_the_byte_counters(tmp_path):
     assert f"kernel_source_sha256: {bench.file_sha256(bench.INGEST_SRC)}" in text
     # the algorithmic bytes of a tiny layer: 256 tokens x 512 B, read + written
     assert "Algorithmic bytes per launch: 262144" in text
+
+
+def test_cpu_baseline_reports_its_sample():
+    import kvgen
+    wl = kvgen.workload("tiny")
+    objs = kvgen.chunk_objects(wl.seed, 0, wl.num_layers, wl.n_chunks(0), wl.slice_elems)
+    tables = kvgen.block_tables(wl.seed, [wl.pages_needed(0)], wl.pool_pages)
+    r = bench.cpu_baseline(wl, [objs], tables, 1.0)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["value"] > 0 and r["cpu"]
+    a = r["attention"]
+    assert a["rows"] == wl.suffix_tokens[0] and a["gflops"] > 0
+    assert a["all_layers_s_extrapolated"] == pytest.approx(wl.num_layers * a["layer_s_extrapolated"], abs=0.1)

@@ -165,3 +165,48 @@ def test_cached_prefix_equals_full_recompute():
     f = lambda x: (x.astype(np.uint32) << 16).view(np.float32)
     assert np.abs(f(full) - f(cached)).max() <= 2e-2
     assert_attention_close(full, c.expected_attention(), "recompute")
+
+
+def test_pool_beyond_two_billion_elements():
+    # a pool whose K region alone holds more than 2^31 elements (140000 pages
+    # of 8 heads x 16 slots x 128 dims, 9.2 GB in all): pages above the 2^31
+    # element mark must be written, read back and attended to exactly as low
+    # ones, through every kernel that indexes the pool
+    import torch
+    from paper_2605_22850_amd import oc_kv_layer_gather, oc_kv_suffix_append
+    nq, nkv, d, G, Ps, n, Ts, P = 8, 8, 128, 16, 16, 64, 40, 140000
+    top = (1 << 31) // (nkv * Ps * d)                 # first page past the 2^31 element mark
+    need = -(-(n * G + Ts) // Ps)                     # prefix pages + room for the suffix
+    rng = np.random.default_rng(11)
+    table = np.concatenate([rng.choice(np.arange(top, P), need // 2 + 1, replace=False),
+                            rng.choice(np.arange(0, top), need - need // 2 - 1, replace=False)])
+    table = rng.permutation(table).astype(np.int32)
+    print(f"[ingest] pool of {P} pages, {int((table >= top).sum())} of {need} pages above 2^31 elements",
+          flush=True)
+    c = LayerCase(nq, nkv, d, G, Ps, n, Ts, P, 1, 0, seed=11, table=table).upload()
+    assert c.d_pool.numel() // 2 > (1 << 31)
+    c.run_ingest()
+    oc_kv_suffix_append(c.d_k, c.d_v, Ts, c.d_table, c.Tp, c.d_pool, c.layout, 0)
+    out = c.run_attention()
+    back = torch.zeros_like(c.d_staging)
+    oc_kv_layer_gather(c.d_table, c.Tp, c.d_pool, c.layout, 0, back, n)
+    torch.cuda.synchronize()
+    # the oracle scatters into a compact pool whose page i stands for table[i]
+    compact = np.full(oracle_pool_shape(need, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+    ident = np.arange(need, dtype=np.int32)
+    import oracle
+    oracle.ingest_layer(c.staging, n, G, nkv, d, Ps, ident, compact, 0)
+    oracle.append_suffix(c.k_new, c.v_new, c.Tp, ident, compact, 0, Ps)
+    pool = c.d_pool.view(1, 2, P, nkv * Ps * d)
+    got = from_dev(pool[0][:, torch.from_numpy(table.astype(np.int64)).cuda()].contiguous())
+    assert np.array_equal(got, compact[0].reshape(2, need, -1)), "pages differ from the oracle's scatter + append"
+    untouched = np.setdiff1d(np.array([top - 1, top, top + 1, P - 1]), table)
+    rest = from_dev(pool[0][:, torch.from_numpy(untouched.astype(np.int64)).cuda()].contiguous())
+    assert (rest == SENTINEL).all(), "a page outside the table was written"
+    assert np.array_equal(from_dev(back), c.staging), "gather after scatter is not the identity"
+    assert_attention_close(from_dev(out), c.expected_attention(), "attention over the large pool")
+
+
+def oracle_pool_shape(P, nkv, Ps, d):
+    import oracle
+    return oracle.pool_shape(1, P, nkv, Ps, d)

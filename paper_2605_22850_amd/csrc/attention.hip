@@ -562,17 +562,23 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(KParams p) {
     if (gr >= (int64_t)p.nkv * p.rows) return;
     const int g = (int)(gr / p.rows);
     const int64_t row = gr - (int64_t)g * p.rows;
+    // the splits' partials are independent loads: unrolled, their latencies
+    // overlap instead of adding up split after split
+    const int64_t split_stride = (int64_t)p.nkv * p.rows_pad;
+    const int64_t prow0 = (int64_t)g * p.rows_pad + row;
     float M = -__builtin_inff();
-    for (int s = 0; s < p.n_split; ++s)
-        M = fmaxf(M, p.ml_part[(((int64_t)s * p.nkv + g) * p.rows_pad + row) * 2]);
+#pragma unroll 8
+    for (int s = 0; s < p.n_split; ++s) M = fmaxf(M, p.ml_part[(prow0 + s * split_stride) * 2]);
     const float Mu = M == -__builtin_inff() ? 0.f : M;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float L = 0.f;
+#pragma unroll 4
     for (int s = 0; s < p.n_split; ++s) {
-        const int64_t prow = ((int64_t)s * p.nkv + g) * p.rows_pad + row;
-        const float w = __builtin_amdgcn_exp2f(p.ml_part[prow * 2] - Mu);
-        L += w * p.ml_part[prow * 2 + 1];
-        f32x4 o = *reinterpret_cast<const f32x4 *>(p.o_part + prow * D + c4 * 4);
+        const int64_t prow = prow0 + s * split_stride;
+        const float2 ml = *reinterpret_cast<const float2 *>(p.ml_part + prow * 2);
+        const f32x4 o = *reinterpret_cast<const f32x4 *>(p.o_part + prow * D + c4 * 4);
+        const float w = __builtin_amdgcn_exp2f(ml.x - Mu);
+        L += w * ml.y;
         acc += w * o;
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;

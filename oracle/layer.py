@@ -27,15 +27,28 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
 
 
 def f64_to_bf16(x: np.ndarray) -> np.ndarray:
-    """Round to the nearest bfloat16, ties to even (via float32, whose own
-    rounding is nearest even; the two roundings agree except on values
-    within 2^-24 relative of a bfloat16 tie)."""
-    f = np.asarray(x, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    nan = np.isnan(f)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    out = r.astype(np.uint16)
-    out[nan] = 0x7FC0
+    """Round float64 values to the nearest bfloat16, ties to even, in one
+    rounding step.
+
+    bfloat16 keeps 8 significant bits and float32's exponent range: a value
+    in [2^(e-1), 2^e) has the spacing 2^(e-8) when e-1 >= -126 (normal), and
+    below 2^-126 the fixed subnormal spacing 2^-133.  x divided by that
+    spacing is exact in float64 (a power-of-two scale), rint rounds the
+    quotient to the nearest integer with ties to even, and the product with
+    the spacing is then a bfloat16 value (or 2^128, which is infinity).
+    That value is exact in float32, whose upper 16 bits are the result."""
+    x = np.asarray(x, dtype=np.float64)
+    finite = np.isfinite(x)
+    xf = np.where(finite, x, 0.0)
+    _, e = np.frexp(xf)                              # |x| in [2^(e-1), 2^e)
+    ulp = np.ldexp(1.0, np.maximum(e, -125) - 8)
+    r = np.rint(xf / ulp) * ulp                      # the one rounding
+    r = np.where(np.abs(r) >= 2.0 ** 128, np.copysign(np.inf, xf), r)
+    r = np.where(finite, r, x)                       # infinities and NaN pass through
+    with np.errstate(over="ignore"):
+        f = r.astype(np.float32)                     # exact: r is a bfloat16 value
+    out = (f.view(np.uint32) >> 16).astype(np.uint16)
+    out[np.isnan(x)] = 0x7FC0
     return out
 
 

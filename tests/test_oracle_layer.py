@@ -30,6 +30,60 @@ def test_rounding_matches_torch_nearest_even():
     assert layer.f64_to_bf16(np.array([1 + 3 * 2 ** -8]))[0] == 0x3F82  # tie to even: up
 
 
+def _nearest_even_brute_force(x: float) -> int:
+    """bfloat16 bits of float64 x by exhaustive search: the non-negative
+    finite bfloat16 patterns 0x0000..0x7F7F increase with their value, so
+    the two neighbours of |x| are found by bisection over all of them; their
+    distances to |x| are compared in exact rational arithmetic, a tie goes
+    to the even pattern.  0x7F80 (infinity) stands at 2^128 for rounding."""
+    from fractions import Fraction
+    if math.isnan(x):
+        return 0x7FC0
+    sign = 0x8000 if math.copysign(1.0, x) < 0 else 0
+    a = abs(x)
+    if a >= 2.0 ** 128:
+        return sign | 0x7F80
+    pats = np.arange(0x7F81, dtype=np.uint32)
+    vals = (pats << 16).view(np.float32).astype(np.float64)
+    vals[0x7F80] = 2.0 ** 128
+    hi = int(np.searchsorted(vals, a, side="left"))      # first value >= |x|
+    if vals[hi] == a:
+        return sign | hi
+    lo = hi - 1
+    dlo, dhi = Fraction(a) - Fraction(float(vals[lo])), Fraction(float(vals[hi])) - Fraction(a)
+    pick = lo if dlo < dhi else hi if dhi < dlo else (lo if lo % 2 == 0 else hi)
+    return sign | pick
+
+
+def test_rounding_is_one_step_from_float64():
+    # values next to bfloat16 ties, where rounding first to float32 and then
+    # to bfloat16 lands on the wrong side: 1 + 2^-8 + 2^-30 lies above the
+    # tie between 0x3F80 and 0x3F81 by less than float32 can hold
+    assert layer.f64_to_bf16(np.array([1 + 2 ** -8 + 2 ** -30]))[0] == 0x3F81
+    assert layer.f64_to_bf16(np.array([1 + 2 ** -8 - 2 ** -30]))[0] == 0x3F80
+    assert layer.f64_to_bf16(np.array([-(1 + 3 * 2 ** -8 - 2 ** -40)]))[0] == 0xBF81
+    # subnormal ties: half the smallest subnormal goes to zero, 1.5 of it to 2 units
+    assert layer.f64_to_bf16(np.array([2.0 ** -134, 3 * 2.0 ** -134, 2.0 ** -134 * (1 + 2 ** -30)])).tolist() == \
+        [0x0000, 0x0002, 0x0001]
+    # overflow: the largest finite value plus just under half its spacing stays finite
+    big = float((np.uint32(0x7F7F) << 16).view(np.float32))
+    assert layer.f64_to_bf16(np.array([big + 2.0 ** 119 * (1 - 2 ** -20), big + 2.0 ** 119, np.inf, -np.inf,
+                                       np.nan])).tolist() == [0x7F7F, 0x7F80, 0x7F80, 0xFF80, 0x7FC0]
+    # brute force over random values and values within 2^-20 .. 2^-50 relative of a tie
+    rng = np.random.default_rng(5)
+    xs = list(rng.standard_normal(300) * 2.0 ** rng.integers(-140, 130, 300))
+    for b in rng.integers(0, 0x7F7F, 120):
+        v = float((np.uint32(b) << 16).view(np.float32))
+        nxt = float((np.uint32(b + 1) << 16).view(np.float32))
+        tie = (v + nxt) / 2                       # exact in float64
+        k = int(rng.integers(20, 51))
+        xs += [tie, tie * (1 + 2.0 ** -k), tie * (1 - 2.0 ** -k), -tie * (1 + 2.0 ** -k)]
+    xs += [0.0, -0.0, 2.0 ** -133, 2.0 ** -126 * (1 - 2 ** -9)]
+    got = layer.f64_to_bf16(np.array(xs, dtype=np.float64)).tolist()
+    want = [_nearest_even_brute_force(float(x)) for x in xs]
+    assert got == want
+
+
 def test_silu_special_values_and_torch():
     assert layer.silu(np.array([0.0]))[0] == 0.0
     assert abs(layer.silu(np.array([50.0]))[0] - 50.0) < 1e-12
@@ -78,7 +132,8 @@ def test_brute_force_loops_on_tiny_integer_inputs():
         return [[sum(x[i][k] * w[k][j] for k in range(len(w))) for j in range(len(w[0]))] for i in range(len(x))]
 
     def rnd(m):
-        return _vals(_bits(np.array(m, dtype=np.float64))).tolist()
+        bits = np.array([[_nearest_even_brute_force(v) for v in r] for r in m], dtype=np.uint16)
+        return _vals(bits).tolist()
 
     o = mm(a, Wo)
     assert all(abs(v) < 256 for r in o for v in r)

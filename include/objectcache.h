@@ -23,6 +23,8 @@
  *     call on the same thread).  No C++ exception crosses this boundary.
  *   - The library never allocates device memory inside the single-layer
  *     calls; scratch space is the caller's `workspace`.
+ *   - Lengths are validated against the kernels' 32-bit index arithmetic as
+ *     well: a shape whose offsets, rows or grid would not fit is OC_ERANGE.
  */
 #ifndef OBJECTCACHE_H
 #define OBJECTCACHE_H

@@ -21,6 +21,12 @@ int hip_fail(hipError_t e, const char *what) {
     return OC_EHIP;
 }
 
+int check_copy_pieces(int64_t pieces, const char *what) {
+    if (pieces > OC_MAX_GRID_ITEMS)
+        return fail(OC_ERANGE, std::string(what) + ": more than 2^32 16-byte pieces in one launch");
+    return OC_OK;
+}
+
 static int check_layout(const oc_layout &l) {
     if (l.num_layers < 1 || l.num_q_heads < 1 || l.num_kv_heads < 1 || l.head_dim < 1 || l.page_size < 1 ||
         l.chunk_tokens < 1 || l.num_pages < 1)
@@ -115,6 +121,19 @@ static int check_staging_shape(const oc_layout &l, const oc_block_table *bt, int
     return OC_OK;
 }
 
+static int check_attention_layout(const oc_layout &l) {
+    int rc = check_layout(l);
+    if (rc) return rc;
+    if (l.head_dim != 64 && l.head_dim != 128) return fail(OC_ESHAPE, "attention supports head_dim 64 or 128");
+    if (l.page_size != 16) return fail(OC_ESHAPE, "attention supports page_size 16");
+    return OC_OK;
+}
+
+int check_attention_args(const oc_layout &l, int64_t Tp, int64_t Ts) {
+    int rc = check_attention_layout(l);
+    return rc ? rc : check_attention_shape(l, Tp, Ts);
+}
+
 }  // namespace oc
 
 using namespace oc;
@@ -153,6 +172,8 @@ int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_ta
     if ((rc = check_table(block_table, l))) return rc;
     if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
     if ((rc = check_staging_shape(l, block_table, staging->num_chunks, staging->per_layer_chunk_bytes))) return rc;
+    if ((rc = check_copy_pieces(block_table->num_tokens * 2 * l.num_kv_heads * (l.head_dim / 8), "layer payload")))
+        return rc;
     if (block_table->num_tokens == 0) return OC_OK;
     if (!staging->data || !kv_pool->base) return fail(OC_EINVAL, "NULL data or pool base");
     if (!aligned(staging->data, 16) || !aligned(kv_pool->base, 16))
@@ -177,6 +198,9 @@ int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc
     if (first_chunk < 0 || objects->num_chunks < 0) return fail(OC_EINVAL, "negative first_chunk or num_chunks");
     if ((first_chunk + objects->num_chunks) * l.chunk_tokens > block_table->num_tokens)
         return fail(OC_ERANGE, "chunks past the end of the block table's prefix");
+    if ((rc = check_copy_pieces(objects->num_chunks * l.chunk_tokens * 2 * l.num_kv_heads * (l.head_dim / 8),
+                                "chunk objects of one layer")))
+        return rc;
     if (objects->num_chunks == 0) return OC_OK;
     if (!objects->data || !kv_pool->base) return fail(OC_EINVAL, "NULL data or pool base");
     if (!aligned(objects->data, 16) || !aligned(kv_pool->base, 16))
@@ -196,6 +220,8 @@ int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_p
     if ((rc = check_table(block_table, l))) return rc;
     if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
     if ((rc = check_staging_shape(l, block_table, num_chunks, per_layer_chunk_bytes))) return rc;
+    if ((rc = check_copy_pieces(block_table->num_tokens * 2 * l.num_kv_heads * (l.head_dim / 8), "layer payload")))
+        return rc;
     if (block_table->num_tokens == 0) return OC_OK;
     if (!staging_out || !kv_pool->base) return fail(OC_EINVAL, "NULL staging_out or pool base");
     if (!aligned(staging_out, 16) || !aligned(kv_pool->base, 16))
@@ -216,6 +242,9 @@ int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_
     if (first_chunk < 0 || num_chunks < 0) return fail(OC_EINVAL, "negative first_chunk or num_chunks");
     if ((first_chunk + num_chunks) * l.chunk_tokens > block_table->num_tokens)
         return fail(OC_ERANGE, "chunks past the end of the block table's tokens");
+    if ((rc = check_copy_pieces(num_chunks * l.chunk_tokens * 2 * l.num_kv_heads * (l.head_dim / 8),
+                                "chunk objects of one layer")))
+        return rc;
     if (num_chunks == 0) return OC_OK;
     if (!objects_out || !kv_pool->base) return fail(OC_EINVAL, "NULL objects_out or pool base");
     if (!aligned(objects_out, 16) || !aligned(kv_pool->base, 16))
@@ -254,6 +283,7 @@ int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tok
     if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
     if (suffix_tokens < 0) return fail(OC_EINVAL, "negative suffix_tokens");
     if ((rc = check_append_table(block_table, l, suffix_tokens))) return rc;
+    if ((rc = check_copy_pieces(suffix_tokens * l.num_kv_heads * (l.head_dim / 8), "suffix K/V"))) return rc;
     if (suffix_tokens == 0) return OC_OK;
     if (!k_new || !v_new || !kv_pool->base) return fail(OC_EINVAL, "NULL k_new, v_new or pool base");
     if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(kv_pool->base, 16))
@@ -263,26 +293,27 @@ int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tok
     return OC_OK;
 }
 
-static int check_attention_layout(const oc_layout &l) {
-    int rc = check_layout(l);
-    if (rc) return rc;
-    if (l.head_dim != 64 && l.head_dim != 128) return fail(OC_ESHAPE, "attention supports head_dim 64 or 128");
-    if (l.page_size != 16) return fail(OC_ESHAPE, "attention supports page_size 16");
-    return OC_OK;
-}
-
 size_t oc_attention_workspace_bytes(const oc_layout *layout, int64_t prefix_tokens, int64_t suffix_tokens) {
     clear_error();
-    if (!layout || prefix_tokens < 0 || suffix_tokens < 1 || check_attention_layout(*layout)) return 0;
+    if (!layout) {
+        fail(OC_EINVAL, "layout is NULL");
+        return 0;
+    }
+    if (check_attention_args(*layout, prefix_tokens, suffix_tokens)) return 0;
     AttnPlan p;
     plan_attention(*layout, prefix_tokens, suffix_tokens, &p);
     return p.total;
 }
 
-int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
-                            const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
-                            void *workspace, size_t workspace_bytes, void *stream) {
-    clear_error();
+}  // extern "C"
+
+namespace oc {
+
+// Checks of one layer's attention call apart from its workspace; on OC_OK
+// `plan` holds the launch plan.
+static int check_attention_call(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                                const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer,
+                                void *out, AttnPlan *plan) {
     if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
     int rc = check_attention_layout(kv_pool->layout);
     if (rc) return rc;
@@ -290,16 +321,20 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
     if ((rc = check_table(block_table, l))) return rc;
     if (layer < 0 || layer >= l.num_layers) return fail(OC_ERANGE, "layer out of range");
     if (suffix_tokens < 1) return fail(OC_EINVAL, "suffix_tokens must be >= 1");
-    if (!q || !k_new || !v_new || !out || !workspace) return fail(OC_EINVAL, "NULL tensor or workspace");
+    if ((rc = check_attention_shape(l, block_table->num_tokens, suffix_tokens))) return rc;
+    if (!q || !k_new || !v_new || !out) return fail(OC_EINVAL, "NULL tensor");
     if (block_table->num_tokens > 0 && !kv_pool->base) return fail(OC_EINVAL, "NULL pool base");
     if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(out, 16) ||
         !aligned(kv_pool->base, 16))
         return fail(OC_EALIGN, "q, k_new, v_new, out and pool base must be 16-byte aligned");
-    if (!aligned(workspace, 256)) return fail(OC_EALIGN, "workspace must be 256-byte aligned");
-    AttnPlan p;
-    plan_attention(l, block_table->num_tokens, suffix_tokens, &p);
-    if (workspace_bytes < p.total)
-        return fail(OC_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
+    plan_attention(l, block_table->num_tokens, suffix_tokens, plan);
+    return OC_OK;
+}
+
+static int enqueue_attention(const AttnPlan &p, const void *q, const void *k_new, const void *v_new,
+                             const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
+                             void *workspace, hipStream_t stream) {
+    const oc_layout &l = kv_pool->layout;
     AttnArgs a{};
     const int64_t block = (int64_t)l.num_kv_heads * l.page_size * l.head_dim;
     const uint16_t *base = static_cast<const uint16_t *>(kv_pool->base);
@@ -311,8 +346,27 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
     a.pages = block_table->pages;
     a.out = static_cast<uint16_t *>(out);
     a.ws = static_cast<unsigned char *>(workspace);
-    OC_HIP(launch_attention(p, a, static_cast<hipStream_t>(stream)));
+    OC_HIP(launch_attention(p, a, stream));
     return OC_OK;
+}
+
+}  // namespace oc
+
+extern "C" {
+
+int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                            const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
+                            void *workspace, size_t workspace_bytes, void *stream) {
+    clear_error();
+    AttnPlan p;
+    int rc = check_attention_call(q, k_new, v_new, suffix_tokens, kv_pool, block_table, layer, out, &p);
+    if (rc) return rc;
+    if (!workspace) return fail(OC_EINVAL, "NULL workspace");
+    if (!aligned(workspace, 256)) return fail(OC_EALIGN, "workspace must be 256-byte aligned");
+    if (workspace_bytes < p.total)
+        return fail(OC_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
+    return enqueue_attention(p, q, k_new, v_new, kv_pool, block_table, layer, out, workspace,
+                             static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

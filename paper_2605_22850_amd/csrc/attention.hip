@@ -28,6 +28,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.hpp"
 
@@ -48,6 +49,7 @@ constexpr int WAVE_ROWS = 32 * QB;
 constexpr int TILE_ROWS = WAVES * WAVE_ROWS;
 constexpr int THREADS = WAVES * 64;
 constexpr int TARGET_WGS = 256;   // one workgroup per CU
+constexpr int kMaxDevices = 64;   // devices a process may launch on
 #ifndef OC_BATCH_ROUNDS
 #define OC_BATCH_ROUNDS 2
 #endif
@@ -659,6 +661,32 @@ int plan_attention_batch(const oc_layout &lay, const int64_t *Tp, const int64_t 
     return OC_OK;
 }
 
+int64_t attention_grid(const AttnPlan &p) { return 8 * (((int64_t)p.nkv * p.n_split + 7) / 8) * p.m_tiles; }
+
+// a dispatch holds at most 2^32 - 1 work-items along x
+int64_t attention_max_grid() { return OC_MAX_GRID_ITEMS / THREADS; }
+
+int check_attention_shape(const oc_layout &l, int64_t Tp, int64_t Ts) {
+    if (l.head_dim != 64 && l.head_dim != 128) return fail(OC_ESHAPE, "attention supports head_dim 64 or 128");
+    if (l.page_size != PAGE) return fail(OC_ESHAPE, "attention supports page_size 16");
+    if (Tp < 0 || Ts < 1) return fail(OC_EINVAL, "attention needs prefix_tokens >= 0 and suffix_tokens >= 1");
+    // the suffix rows are copied to LDS with 32-bit byte offsets from k_new / v_new
+    if (Ts * l.num_kv_heads * l.head_dim * 2 > INT32_MAX)
+        return fail(OC_ERANGE, "suffix K/V of more than 2^31 bytes (suffix_tokens * n_kv * d * 2)");
+    // key positions, query rows and their tokens are 32-bit in the kernels
+    if (Tp + Ts > (int64_t)1 << 30) return fail(OC_ERANGE, "prefix + suffix tokens exceed 2^30");
+    const int64_t grp = l.num_q_heads / l.num_kv_heads;
+    if (Ts * grp > (int64_t)1 << 30) return fail(OC_ERANGE, "suffix_tokens * (n_q / n_kv) exceeds 2^30");
+    AttnPlan p;
+    plan_attention(l, Tp, Ts, &p);
+    if (attention_grid(p) > attention_max_grid())
+        return fail(OC_ERANGE, "attention grid of more than " + std::to_string(attention_max_grid()) + " workgroups");
+    // the split merge runs d/4 work-items per (KV head, row)
+    if ((int64_t)p.nkv * p.rows * (p.d / 4) > OC_MAX_GRID_ITEMS)
+        return fail(OC_ERANGE, "split merge grid exceeds 2^32 work-items");
+    return OC_OK;
+}
+
 template <int D>
 static KParams make_params(const AttnPlan &pl, const AttnArgs &a) {
     KParams p{};
@@ -705,13 +733,20 @@ static hipError_t launch_d(const AttnPlan *pl, const AttnArgs *a, int n, hipStre
         batch.first_wg[k] = (int32_t)grid;
         grid += 8 * ((batch.req[k].n_groups + 7) / 8) * (int64_t)pl[i].m_tiles;
     }
-    static bool lds_set = false;
-    if (!lds_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_fwd_kernel<D>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds_bytes<D>());
-        if (e != hipSuccess) return e;
-        lds_set = true;
-    }
+    if (grid > attention_max_grid()) return hipErrorInvalidConfiguration;
+    // the kernel's dynamic LDS above the default limit, set once per device
+    // (any thread may make the first launch on a device)
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    static std::once_flag lds_once[kMaxDevices];
+    static hipError_t lds_status[kMaxDevices];
+    std::call_once(lds_once[dev], [dev] {
+        lds_status[dev] = hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_fwd_kernel<D>),
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds_bytes<D>());
+    });
+    if (lds_status[dev] != hipSuccess) return lds_status[dev];
     if (grid > 0) hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((unsigned)grid), dim3(THREADS), attn_lds_bytes<D>(), s, batch);
     for (int k = 0; k < n; ++k)
         if (batch.req[k].n_split > 1) {

@@ -25,6 +25,12 @@ int hip_fail(hipError_t e, const char *what);
 
 inline bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// A dispatch counts the work-items of each grid dimension in 32 bits
+// (workgroups x workgroup size).  The copy kernels number their 16-byte
+// pieces along x, one per work-item; OC_OK or OC_ERANGE.
+constexpr int64_t OC_MAX_GRID_ITEMS = 0xFFFFFFFFLL - 1023;
+int check_copy_pieces(int64_t pieces, const char *what);
+
 // ---- ingest / gather ------------------------------------------------------
 struct IngestArgs {
     const uint16_t *staging;   // chunk slices [N][2][G][n_kv][d], chunk_stride apart
@@ -113,6 +119,18 @@ struct AttnPlan {
     size_t off_o, off_ml, total;
 };
 int plan_attention(const oc_layout &lay, int64_t Tp, int64_t Ts, AttnPlan *plan);
+// Shapes the attention kernels can index: the layout (head_dim 64 or 128,
+// page_size 16; OC_ESHAPE otherwise) and the 32-bit limits of their
+// arithmetic (OC_ERANGE): suffix K/V byte offsets, key positions, rows and
+// the grids of both kernels.
+int check_attention_shape(const oc_layout &lay, int64_t Tp, int64_t Ts);
+// check_attention_shape after the layout's own checks (positive fields, GQA
+// head ratio, alignment multiples)
+int check_attention_args(const oc_layout &lay, int64_t Tp, int64_t Ts);
+// workgroups of the attention launch of one plan
+int64_t attention_grid(const AttnPlan &p);
+// at most this many workgroups in one attention launch (all its requests)
+int64_t attention_max_grid();
 // one launch for up to MAX_ATTN_BATCH requests of one layer: keys are split
 // so that every workgroup gets about the same number of key blocks
 constexpr int MAX_ATTN_BATCH = 16;

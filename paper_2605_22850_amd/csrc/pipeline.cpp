@@ -766,8 +766,11 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
 
     // per-request rates under the shared budget (allocation policies)
     const bool by_rate = mode == OC_MODE_PRODUCER && c->opts.alloc_policy != OC_ALLOC_FIFO;
+    int64_t batch_grid = 0;   // workgroups of one batched launch
+    if (n_reqs >= 2 && n_reqs <= MAX_ATTN_BATCH)
+        for (int32_t i = 0; i < n_reqs; ++i) batch_grid += attention_grid(bplan[i]);
     const bool batched = !c->opts.attention_per_request && !emu && !by_rate && n_cw == 0 && n_reqs >= 2 &&
-                         n_reqs <= MAX_ATTN_BATCH;
+                         n_reqs <= MAX_ATTN_BATCH && batch_grid <= attention_max_grid();
     std::vector<double> req_rate(n_reqs, 0.0);
     if (by_rate) {
         std::vector<double> s_i, c_i;
@@ -1083,8 +1086,11 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
     *ctx = nullptr;
     if (max_prefix_tokens < 0 || max_suffix_tokens < 1) return fail(OC_EINVAL, "bad maximum lengths");
     const oc_layout &l = kv_pool->layout;
-    if (oc_attention_workspace_bytes(&l, max_prefix_tokens, max_suffix_tokens) == 0)
-        return fail(OC_ESHAPE, std::string("unsupported layout: ") + oc_last_error());
+    // OC_ESHAPE for the layout, OC_ERANGE for lengths past the kernels' limits
+    if (int rc = check_attention_args(l, max_prefix_tokens, max_suffix_tokens))
+        return fail(rc, std::string("unsupported layout or lengths: ") + oc_last_error());
+    if (check_copy_pieces(max_prefix_tokens * 2 * l.num_kv_heads * (l.head_dim / 8), "layer payload"))
+        return fail(OC_ERANGE, oc_last_error());
     if (!kv_pool->base || !aligned(kv_pool->base, 16)) return fail(OC_EALIGN, "pool base must be 16-byte aligned");
     Context *c = new Context();
     c->device = device;

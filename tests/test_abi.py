@@ -222,3 +222,54 @@ def test_context_rejects_an_absent_device():
     rc = oc.lib().oc_context_create(4096, ctypes.byref(kp), ctypes.byref(opts), 256, 32, ctypes.byref(ctx))
     assert rc == L.OC_EINVAL and not ctx.value
     assert b"no such device" in oc.lib().oc_last_error()
+
+
+def test_lengths_past_the_kernels_32bit_arithmetic_are_rejected():
+    big = _layout(num_layers=2, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=1 << 26)
+    ws = oc.lib().oc_attention_workspace_bytes
+    # suffix K/V byte offsets: T_s * n_kv * d * 2 must stay below 2^31
+    assert ws(ctypes.byref(big), 4096, (1 << 20) - 1) > 0
+    assert ws(ctypes.byref(big), 4096, 1 << 20) == 0
+    assert b"2^31" in oc.lib().oc_last_error()
+    # key positions: prefix + suffix tokens up to 2^30
+    assert ws(ctypes.byref(big), (1 << 30) - 512, 512) > 0
+    assert ws(ctypes.byref(big), (1 << 30) - 511, 512) == 0
+    assert b"2^30" in oc.lib().oc_last_error()
+    # the single-layer call rejects the same lengths before launching anything
+    bt = L.c_block_table(FAKE, 1 << 26, 4096)
+    kp = L.c_kv_pool(FAKE, big)
+    f = oc.lib().oc_suffix_prefill_layer
+    assert f(FAKE, FAKE, FAKE, 1 << 20, ctypes.byref(kp), ctypes.byref(bt), 0, FAKE, FAKE, 1 << 40, None) == \
+        L.OC_ERANGE
+    bt_long = L.c_block_table(FAKE, 1 << 26, (1 << 30) - 16)
+    assert f(FAKE, FAKE, FAKE, 512, ctypes.byref(kp), ctypes.byref(bt_long), 0, FAKE, FAKE, 1 << 40, None) == \
+        L.OC_ERANGE
+    # a context for such lengths is refused before any device is touched
+    opts = L.c_pipeline_opts()
+    ctx = ctypes.c_void_p()
+    rc = oc.lib().oc_context_create(0, ctypes.byref(kp), ctypes.byref(opts), 4096, 1 << 20, ctypes.byref(ctx))
+    assert rc == L.OC_ERANGE and not ctx.value
+
+
+def test_copies_past_a_32bit_grid_are_rejected():
+    # 2^24 prefix tokens of 8 heads x 128 dims are 2^32 16-byte pieces per layer
+    lay = _layout(num_layers=2, num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=1 << 21)
+    n = 1 << 24
+    ok = n - 16
+    assert _ingest(lay, num_chunks=n // 16, table_entries=1 << 20, num_tokens=n) == L.OC_ERANGE
+    assert b"2^32" in oc.lib().oc_last_error()
+    st = L.c_staging(FAKE, n // 16, 2 * 16 * 8 * 128 * 2)
+    bt = L.c_block_table(FAKE, 1 << 20, n)
+    kp = L.c_kv_pool(FAKE, lay)
+    assert oc.lib().oc_kv_chunks_ingest(ctypes.byref(st), 0, ctypes.byref(bt), ctypes.byref(kp), None) == \
+        L.OC_ERANGE
+    assert oc.lib().oc_kv_layer_gather(ctypes.byref(bt), ctypes.byref(kp), 0, FAKE, n // 16, 2 * 16 * 8 * 128 * 2,
+                                       None) == L.OC_ERANGE
+    assert oc.lib().oc_kv_chunks_gather(ctypes.byref(bt), ctypes.byref(kp), 0, n // 16, FAKE, None) == L.OC_ERANGE
+    # the append moves K and V in two grid rows: 2^25 tokens are 2^32 pieces of each
+    bt0 = L.c_block_table(FAKE, 1 << 21, 0)
+    assert oc.lib().oc_kv_suffix_append(FAKE, FAKE, 1 << 25, ctypes.byref(bt0), ctypes.byref(kp), 0, None) == \
+        L.OC_ERANGE
+    # one chunk fewer is accepted by validation (it is not launched here: the
+    # NULL data pointer stops it)
+    assert _ingest(lay, num_chunks=ok // 16, table_entries=1 << 20, num_tokens=ok, data=None) == L.OC_EINVAL

@@ -130,3 +130,65 @@ def test_workload_first_and_last_layer(name):
 def test_paper_chunk_sizes_at_full_size(name, G):
     # the paper's end-to-end settings use G = 64 (main) and 256 besides 16
     check_workload(kvgen.with_chunk_tokens(kvgen.workload(name), G))
+
+
+@pytest.mark.timeout(600)
+def test_batch8_batched_pipeline_launch_at_full_size():
+    """The batch workload's own launch configuration: the device-staged
+    pipeline with its default attention, one launch per layer over all eight
+    requests with the key split planned for all their row tiles together.
+    The two pool layers hold the workload's first and last layers; the pool
+    is compared bit for bit with the oracle's scatter, and every request's
+    attention with the float64 oracle on 64 sampled suffix rows (the first
+    and the last among them) and every head."""
+    import torch
+    import paper_2605_22850_amd as oc
+    wl = kvgen.workload("batch8")
+    L, nq, nkv, d, G, Ps = (wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.chunk_tokens,
+                            wl.page_size)
+    layers = [0, L - 1]
+    n_req = wl.n_requests
+    print(f"[batch8 batched pipeline] prefixes={wl.prefix_tokens} suffix={wl.suffix_tokens} "
+          f"pool={wl.pool_pages}", flush=True)
+    layout = oc.Layout(2, nq, nkv, d, Ps, G, wl.pool_pages)
+    tables = kvgen.block_tables(wl.seed, [wl.pages_needed(r) for r in range(n_req)], wl.pool_pages)
+    pool = torch.full((layout.pool_elems,), int(np.uint16(SENTINEL).view(np.int16)), dtype=torch.int16,
+                      device="cuda")
+    want_pool = np.full(oracle.pool_shape(2, wl.pool_pages, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+    reqs, host = [], []
+    for r in range(n_req):
+        n, tp, ts = wl.n_chunks(r), wl.prefix_tokens[r], wl.suffix_tokens[r]
+        sl = [kvgen.chunk_layer_slices(wl.seed, r, l, n, wl.slice_elems) for l in layers]
+        for li in range(2):
+            oracle.ingest_layer(sl[li].reshape(-1), n, G, nkv, d, Ps, tables[r], want_pool, li)
+        sfx = [np.stack([kvgen.suffix_tensor(wl.seed, kind, r, l, shape) for l in layers])
+               for kind, shape in ((kvgen.KIND_Q, (ts, nq, d)), (kvgen.KIND_KNEW, (ts, nkv, d)),
+                                   (kvgen.KIND_VNEW, (ts, nkv, d)))]
+        host.append((sl, sfx))
+        payload = to_dev(np.concatenate([s.reshape(-1) for s in sl]))      # layer payloads back to back
+        reqs.append(oc.Request(tp, ts, torch.from_numpy(tables[r]).cuda(), to_dev(sfx[0], "bf16"),
+                               to_dev(sfx[1], "bf16"), to_dev(sfx[2], "bf16"),
+                               torch.zeros((2, ts, nq, d), dtype=torch.bfloat16, device="cuda"),
+                               device_payload=payload))
+    ctx = oc.oc_context_create(pool, layout, oc.OC_MODE_DEVICE_STAGED, max(wl.prefix_tokens),
+                               max(wl.suffix_tokens))
+    try:
+        stats = oc.oc_pipeline_run(ctx, reqs, 2)
+    finally:
+        oc.oc_context_destroy(ctx)
+    torch.cuda.synchronize()
+    for li in range(2):     # one launch per layer: every request's layer is done at the same moment
+        assert len({st["done_ms"][li] for st in stats}) == 1, f"layer {li} was not one batched launch"
+    assert np.array_equal(from_dev(pool).reshape(want_pool.shape), want_pool), "batch8: pool differs"
+    del want_pool
+    for r in range(n_req):
+        ts = wl.suffix_tokens[r]
+        rows = sample_rows(ts, seed=100 + r)
+        sl, (q, kn, vn) = host[r]
+        got = from_dev(reqs[r].out)
+        for li, l in enumerate(layers):
+            k, v = oracle.logical_kv([np.ascontiguousarray(s) for s in sl[li]], G, nkv, d, 0)
+            ref = oracle.attention(q[li], k, v, kn[li], vn[li], rows=rows)
+            err = assert_attention_close(got[li][rows], ref, f"batch8 request {r} layer {l}")
+            print(f"  request {r} (T_p {wl.prefix_tokens[r]}) layer {l}: rows {len(rows)} "
+                  f"max|err| {err[0]:.2e} rel L2 {err[1]:.2e}", flush=True)

@@ -302,3 +302,30 @@ def test_emulated_compute_windows_follow_eq3():
     rs2.reqs[0].layer_compute_s = 11.0
     with pytest.raises(oc.OcError):
         _run(rs2, oc.OC_MODE_DEVICE_STAGED, emulate_compute=True)
+
+
+# (G, chunks, d): chunk sizes other than the page size; 12 is not a multiple
+# of 8 (the per-token decode), and 104, 132 and 168 prefix tokens end inside
+# a page
+ROWS_KERNEL_CASES = [(8, 13, 64), (12, 11, 128), (24, 7, 128), (64, 3, 128), (256, 2, 128)]
+
+
+@pytest.mark.timeout(120)
+@pytest.mark.parametrize("G,chunks,d", ROWS_KERNEL_CASES)
+def test_layerwise_ingest_chunk_sizes(G, chunks, d):
+    # every layer after the first of a run is ingested beside the attention
+    # by the 8-slot row kernel; the whole pool must equal the oracle's
+    # scatter in the device-staged and the producer modes
+    import paper_2605_22850_amd as oc
+    print(f"[pipeline] G={G} chunks={chunks} d={d}", flush=True)
+    rs = RequestSet(3, 8, 2, d, [G * chunks], [24], 64, seed=17, G=G).upload(with_payload=True)
+    want_pool = rs.expected_pool()
+    for name, mode in (("staged", oc.OC_MODE_DEVICE_STAGED), ("producer", oc.OC_MODE_PRODUCER)):
+        rs.d_pool.fill_(np.int16(np.uint16(SENTINEL).view(np.int16)))
+        for req in rs.reqs:
+            req.out.zero_()
+        _run(rs, mode)
+        assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), want_pool), f"{name}: pool"
+        out = _outs(rs)[0]
+        for l in range(rs.L):
+            assert_attention_close(out[l], rs.expected_out(0, l), f"{name} G={G} layer {l}")

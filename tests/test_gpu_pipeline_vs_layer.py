@@ -2,9 +2,9 @@
 attention as the single-layer entry point called layer by layer: key
 splits, their merge and the workspace slices leave no trace in the outputs,
 which agree bit for bit, run after run, and match the oracle.  With several
-requests batched into one launch per layer (the default), the outputs match
-the oracle and the per-request launches within the attention tolerance, run
-after run bit for bit."""
+requests batched into one launch per layer (the default), every row of every
+layer matches the oracle (and the per-request launches) within the attention
+tolerance, run after run bit for bit."""
 import numpy as np
 import pytest
 
@@ -116,9 +116,10 @@ def test_batched_layer_launch(name):
     for r in range(len(pre)):
         assert np.array_equal(runs[1][r], runs[0][r]) and np.array_equal(runs[2][r], runs[0][r]), f"request {r}"
         for l in range(L):
+            # every row and head of every layer against the oracle, and
+            # against the request's own launch
+            assert_attention_close(runs[0][r][l], rs.expected_out(r, l), f"{name} request {r} layer {l}")
             assert_attention_close(runs[0][r][l], _f64(single[r][l]), f"{name} request {r} layer {l} vs per-request")
-        rows = sorted({0, suf[r] - 1})
-        assert_attention_close(runs[0][r][L - 1][rows], rs.expected_out(r, L - 1, rows=rows), f"{name} request {r}")
 
 
 def _f64(bits):

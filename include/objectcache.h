@@ -22,7 +22,8 @@
  *     oc_last_error() returns a message (thread-local, valid until the next
  *     call on the same thread).  No C++ exception crosses this boundary.
  *   - The library never allocates device memory inside the single-layer
- *     calls; scratch space is the caller's `workspace`.
+ *     calls; scratch space is the caller's `workspace` (or, for
+ *     oc_suffix_prefill_layer_noalloc, a static device array).
  *   - Lengths are validated against the kernels' 32-bit index arithmetic as
  *     well: a shape whose offsets, rows or grid would not fit is OC_ERANGE.
  */
@@ -36,7 +37,7 @@
 extern "C" {
 #endif
 
-#define OC_ABI_VERSION 3
+#define OC_ABI_VERSION 4
 
 typedef enum {
     OC_OK = 0,
@@ -178,6 +179,32 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
                             int64_t suffix_tokens, const oc_kv_pool *kv_pool,
                             const oc_block_table *block_table, int32_t layer, void *out,
                             void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of the static device workspace behind oc_suffix_prefill_layer_noalloc.
+ * Every shape oc_suffix_prefill_layer accepts needs at most about 64.9 MiB of
+ * workspace (fewer than 512 (row tile, key split) pairs of 130 KiB each at
+ * head_dim 128), so this holds the workspace of every accepted shape. */
+#define OC_NOALLOC_WORKSPACE_BYTES ((size_t)65 << 20)
+
+/* oc_suffix_prefill_layer for callers that cannot allocate device memory or
+ * pass a workspace: code under stream capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments (less the workspace), same checks,
+ * same kernels and bit-identical output.  The split partials go to a static
+ * device array of OC_NOALLOC_WORKSPACE_BYTES that every GPU the library runs
+ * on holds from its first call there until the process ends; the call
+ * allocates nothing.  It runs on the calling thread's current device, and
+ * `stream` must belong to it.  Calls on one GPU share that array: two calls
+ * whose kernels overlap in time (on different streams, or from different
+ * threads without ordering) race and corrupt each other's output; calls in
+ * order on one stream are safe.  Nothing in the array needs to start at zero
+ * (every partial the merge reads is first written by the same call), and it
+ * keeps the last call's partials.  A shape whose workspace exceeds
+ * OC_NOALLOC_WORKSPACE_BYTES is OC_ERANGE (none of the accepted shapes does).
+ * Asynchronous on `stream`. */
+int oc_suffix_prefill_layer_noalloc(const void *q, const void *k_new, const void *v_new,
+                                    int64_t suffix_tokens, const oc_kv_pool *kv_pool,
+                                    const oc_block_table *block_table, int32_t layer, void *out,
+                                    void *stream);
 
 /* Rest-of-layer compute window (the C_l of eq. (3): the compute the miss
  * tokens expose per layer, Section 3.5; every layer runs the same

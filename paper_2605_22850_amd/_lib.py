@@ -28,8 +28,9 @@ EXPORTS = [
     "oc_abi_version", "oc_last_error", "oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest",
     "oc_kv_layer_gather", "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_rest_of_layer",
     "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
-    "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate",
+    "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate", "oc_suffix_prefill_layer_noalloc",
 ]
+OC_NOALLOC_WORKSPACE_BYTES = 65 << 20
 
 
 class OcError(RuntimeError):
@@ -115,6 +116,8 @@ def lib():
         L.oc_suffix_prefill_layer.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, POINTER(c_kv_pool),
                                               POINTER(c_block_table), c_int32, c_void_p, c_void_p, c_size_t,
                                               c_void_p]
+        L.oc_suffix_prefill_layer_noalloc.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, POINTER(c_kv_pool),
+                                                      POINTER(c_block_table), c_int32, c_void_p, c_void_p]
         if hasattr(L, "oc_pipeline_run"):
             L.oc_context_create.argtypes = [c_int, POINTER(c_kv_pool), POINTER(c_pipeline_opts), c_int64, c_int64,
                                             POINTER(c_void_p)]
@@ -129,7 +132,7 @@ def lib():
                                             POINTER(c_double)]
         for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest", "oc_kv_layer_gather",
                      "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_rest_of_layer", "oc_suffix_prefill_layer",
-                     "oc_bandwidth_allocate"):
+                     "oc_suffix_prefill_layer_noalloc", "oc_bandwidth_allocate"):
             getattr(L, name).restype = c_int
         _lib = L
     return _lib
@@ -282,6 +285,16 @@ def oc_suffix_prefill_layer(q, k_new, v_new, suffix_tokens: int, pool, layout: L
     _check(lib().oc_suffix_prefill_layer(_ptr(q), _ptr(k_new), _ptr(v_new), suffix_tokens, ctypes.byref(kp),
                                          ctypes.byref(bt), layer, _ptr(out), _ptr(workspace), workspace.numel() *
                                          workspace.element_size(), _stream(stream)))
+
+
+def oc_suffix_prefill_layer_noalloc(q, k_new, v_new, suffix_tokens: int, pool, layout: Layout, pages,
+                                    num_tokens: int, layer: int, out, stream=None) -> None:
+    """oc_suffix_prefill_layer without a workspace argument: the library's
+    static per-device workspace holds the split partials."""
+    bt = make_table(pages, num_tokens)
+    kp = make_pool(pool, layout)
+    _check(lib().oc_suffix_prefill_layer_noalloc(_ptr(q), _ptr(k_new), _ptr(v_new), suffix_tokens, ctypes.byref(kp),
+                                                 ctypes.byref(bt), layer, _ptr(out), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

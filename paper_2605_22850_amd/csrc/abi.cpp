@@ -1,6 +1,7 @@
 // C entry points for single-layer calls: argument validation, then launch.
 // Nothing is enqueued unless every check passes.
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -132,6 +133,35 @@ static int check_attention_layout(const oc_layout &l) {
 int check_attention_args(const oc_layout &l, int64_t Tp, int64_t Ts) {
     int rc = check_attention_layout(l);
     return rc ? rc : check_attention_shape(l, Tp, Ts);
+}
+
+// ---- workspace of the allocation-free attention entry point ----------------
+// The split partials of oc_suffix_prefill_layer_noalloc live in this array;
+// every GPU the library runs on holds its own copy until the process ends.
+// Host code never passes the array's name to a kernel (on the host it stands
+// for no device address): it takes the device address that
+// hipGetSymbolAddress reports, once per device, and uses only that.
+static __device__ __align__(256) unsigned char scratch[OC_NOALLOC_WORKSPACE_BYTES];
+
+constexpr int kMaxScratchDevices = 64;
+static std::once_flag g_scratch_once[kMaxScratchDevices];
+static void *g_scratch_ptr[kMaxScratchDevices];
+static hipError_t g_scratch_status[kMaxScratchDevices];
+
+// device address of `scratch` on the current device
+static int scratch_on_current_device(void **ptr) {
+    int dev = 0;
+    OC_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxScratchDevices) return fail(OC_EINVAL, "device index beyond the library's table");
+    std::call_once(g_scratch_once[dev], [dev] {
+        void *p = nullptr;
+        g_scratch_status[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = p;
+    });
+    if (g_scratch_status[dev] != hipSuccess) return hip_fail(g_scratch_status[dev], "hipGetSymbolAddress(scratch)");
+    if (!g_scratch_ptr[dev]) return fail(OC_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    *ptr = g_scratch_ptr[dev];
+    return OC_OK;
 }
 
 }  // namespace oc
@@ -366,6 +396,23 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
     if (workspace_bytes < p.total)
         return fail(OC_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
     return enqueue_attention(p, q, k_new, v_new, kv_pool, block_table, layer, out, workspace,
+                             static_cast<hipStream_t>(stream));
+}
+
+int oc_suffix_prefill_layer_noalloc(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                                    const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer,
+                                    void *out, void *stream) {
+    clear_error();
+    AttnPlan p;
+    int rc = check_attention_call(q, k_new, v_new, suffix_tokens, kv_pool, block_table, layer, out, &p);
+    if (rc) return rc;
+    if (p.total > OC_NOALLOC_WORKSPACE_BYTES)
+        return fail(OC_ERANGE, "this shape needs " + std::to_string(p.total) +
+                                   " bytes of workspace; the static workspace holds " +
+                                   std::to_string((size_t)OC_NOALLOC_WORKSPACE_BYTES));
+    void *ws = nullptr;
+    if ((rc = scratch_on_current_device(&ws))) return rc;
+    return enqueue_attention(p, q, k_new, v_new, kv_pool, block_table, layer, out, ws,
                              static_cast<hipStream_t>(stream));
 }
 

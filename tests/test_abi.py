@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert oc.oc_abi_version() == 3
+    assert oc.oc_abi_version() == 4
 
 
 def _layout(**kw):
@@ -241,6 +241,8 @@ def test_lengths_past_the_kernels_32bit_arithmetic_are_rejected():
     f = oc.lib().oc_suffix_prefill_layer
     assert f(FAKE, FAKE, FAKE, 1 << 20, ctypes.byref(kp), ctypes.byref(bt), 0, FAKE, FAKE, 1 << 40, None) == \
         L.OC_ERANGE
+    g = oc.lib().oc_suffix_prefill_layer_noalloc
+    assert g(FAKE, FAKE, FAKE, 1 << 20, ctypes.byref(kp), ctypes.byref(bt), 0, FAKE, None) == L.OC_ERANGE
     bt_long = L.c_block_table(FAKE, 1 << 26, (1 << 30) - 16)
     assert f(FAKE, FAKE, FAKE, 512, ctypes.byref(kp), ctypes.byref(bt_long), 0, FAKE, FAKE, 1 << 40, None) == \
         L.OC_ERANGE
@@ -273,3 +275,34 @@ def test_copies_past_a_32bit_grid_are_rejected():
     # one chunk fewer is accepted by validation (it is not launched here: the
     # NULL data pointer stops it)
     assert _ingest(lay, num_chunks=ok // 16, table_entries=1 << 20, num_tokens=ok, data=None) == L.OC_EINVAL
+
+
+def test_noalloc_attention_validation_and_workspace_bound():
+    lay = _layout()
+    bt = L.c_block_table(FAKE, 16, 256)
+    kp = L.c_kv_pool(FAKE, lay)
+    g = oc.lib().oc_suffix_prefill_layer_noalloc
+    args = [FAKE, FAKE, FAKE, 32, ctypes.byref(kp), ctypes.byref(bt), 0, FAKE, None]
+    for i, v, want in ((3, 0, L.OC_EINVAL), (0, FAKE + 4, L.OC_EALIGN), (7, None, L.OC_EINVAL), (6, 2, L.OC_ERANGE)):
+        bad = list(args)
+        bad[i] = v
+        assert g(*bad) == want, (i, v)
+    lay96 = _layout(head_dim=96)
+    assert g(FAKE, FAKE, FAKE, 32, ctypes.byref(L.c_kv_pool(FAKE, lay96)), ctypes.byref(bt), 0, FAKE, None) == \
+        L.OC_ESHAPE
+    # every accepted shape's workspace fits the static array: fewer than 512
+    # (row tile, key split) pairs; the largest comes from 255 row tiles split in two
+    ws = oc.lib().oc_attention_workspace_bytes
+    worst = _layout(num_q_heads=1, num_kv_heads=1, head_dim=128, num_pages=1 << 16)
+    w = ws(ctypes.byref(worst), 65536, 255 * 256)
+    assert 64 << 20 < w <= L.OC_NOALLOC_WORKSPACE_BYTES
+    rng = np.random.default_rng(0)
+    for _ in range(3000):
+        nkv = int(rng.choice([1, 2, 4, 8, 16]))
+        grp = int(rng.choice([1, 2, 4, 8]))
+        d = int(rng.choice([64, 128]))
+        lay_r = _layout(num_q_heads=nkv * grp, num_kv_heads=nkv, head_dim=d, num_pages=1 << 20)
+        ts = int(rng.integers(1, 1 << int(rng.integers(1, 18))))
+        tp = int(rng.integers(0, 1 << int(rng.integers(1, 22))))
+        n = ws(ctypes.byref(lay_r), tp, ts)
+        assert 0 < n <= L.OC_NOALLOC_WORKSPACE_BYTES, (nkv, grp, d, tp, ts, n)

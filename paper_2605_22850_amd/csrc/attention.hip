@@ -273,6 +273,25 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
     for (int i = 1; i < bp->n; ++i) req += (int)blockIdx.x >= bp->first_wg[i];
     const __attribute__((address_space(4))) KParams &p = bp->req[req];
     const int wg = (int)blockIdx.x - bp->first_wg[req];
+    // Every parameter is read once into a register here: read through `p`
+    // inside the loop, each use would be reloaded from the argument segment
+    // after every inline-assembly statement (they clobber memory), each reload
+    // a scalar load that the next LDS wait must also wait for.  Token, page,
+    // block and row counts fit 32 bits (the host limits prefix + suffix to
+    // 2^30 tokens and rows to 2^30).
+    const int m_tiles = p.m_tiles, n_groups = p.n_groups, n_split = p.n_split;
+    const int grp = p.grp, nq = p.nq, nkv = p.nkv;
+    const int rows = (int)p.rows, Tp = (int)p.Tp, Ts = (int)p.Ts, n_pre_pages = (int)p.n_pre_pages;
+    const int n_blocks = (int)p.n_blocks, blocks_per_split = (int)p.blocks_per_split;
+    const int64_t rows_pad = p.rows_pad;
+    const float scale_log2 = p.scale_log2;
+    const uint16_t *const q_in = p.q;
+    const uint16_t *const pool_k = p.pool_k, *const pool_v = p.pool_v;
+    const uint16_t *const k_new = p.k_new, *const v_new = p.v_new;
+    uint16_t *const out_ptr = p.out;
+    float *const o_part = p.o_part, *const ml_part = p.ml_part;
+    const __attribute__((address_space(4))) int32_t *pages_c =
+        (const __attribute__((address_space(4))) int32_t *)p.pages;
     constexpr int TILE = KB * D;                   // elements of one K (or V) tile
     constexpr int CHUNKS = TILE * 2 / 1024;        // 1 KiB DMA chunks per tile
     constexpr int CPW = CHUNKS / WAVES;            // chunks per wavefront per tile
@@ -294,18 +313,18 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
     // row tile first: under the causal mask later rows see more suffix keys,
     // and dispatching the longest tiles first keeps them out of the tail
     const int xcd = wg & 7, local = wg >> 3;
-    const int gamma = (local / p.m_tiles) * 8 + xcd;
-    if (gamma >= p.n_groups) return;
-    const int mt = p.m_tiles - 1 - local % p.m_tiles;
-    const int g = gamma / p.n_split, split = gamma - g * p.n_split;
+    const int gamma = (local / m_tiles) * 8 + xcd;
+    if (gamma >= n_groups) return;
+    const int mt = m_tiles - 1 - local % m_tiles;
+    const int g = gamma / n_split, split = gamma - g * n_split;
 
-    const int64_t row = (int64_t)mt * TILE_ROWS + wave * WAVE_ROWS + col;
-    const bool row_ok = row < p.rows;
-    const int tok = row_ok ? (int)(row / p.grp) : 0;
+    const int row = mt * TILE_ROWS + wave * WAVE_ROWS + col;
+    const bool row_ok = row < rows;
+    const int tok = row_ok ? row / grp : 0;
     bf16x8 qop[D / 16];
     {
-        const int head = g * p.grp + (row_ok ? (int)(row % p.grp) : 0);
-        const uint16_t *qr = p.q + ((int64_t)tok * p.nq + head) * D + half * 8;
+        const int head = g * grp + (row_ok ? row % grp : 0);
+        const uint16_t *qr = q_in + ((int64_t)tok * nq + head) * D + half * 8;
 #pragma unroll
         for (int ds = 0; ds < D / 16; ++ds) {
             u32x4 v = row_ok ? *reinterpret_cast<const u32x4 *>(qr + ds * 16) : u32x4{0, 0, 0, 0};
@@ -313,16 +332,16 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
         }
     }
 
-    int64_t b0 = (int64_t)split * p.blocks_per_split;
-    int64_t b1 = b0 + p.blocks_per_split;
-    if (b1 > p.n_blocks) b1 = p.n_blocks;
+    const int b0 = split * blocks_per_split;
+    int b1 = b0 + blocks_per_split;
+    if (b1 > n_blocks) b1 = n_blocks;
     {   // causal clip: no row of this tile sees suffix keys past its last token
-        int64_t row_hi = ((int64_t)mt + 1) * TILE_ROWS - 1;
-        if (row_hi > p.rows - 1) row_hi = p.rows - 1;
-        const int64_t last_page = p.n_pre_pages + (row_hi / p.grp) / PAGE;
+        int row_hi = (mt + 1) * TILE_ROWS - 1;
+        if (row_hi > rows - 1) row_hi = rows - 1;
+        const int last_page = n_pre_pages + (row_hi / grp) / PAGE;
         if (b1 > last_page / 4 + 1) b1 = last_page / 4 + 1;
     }
-    const int64_t full_pre_pages = p.Tp / PAGE;
+    const int full_pre_pages = Tp / PAGE;
     const int64_t head_block = (int64_t)PAGE * D;      // elements of one (page, head) block
 
     // ---- global -> LDS copy of one 64-key block (4 pages) ----
@@ -333,16 +352,10 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
     // chunks of each tile.  The base pointers stay in registers, and the page
     // ids of a block are loaded (scalar loads through the constant address
     // space) one block ahead of its copy, so no copy waits on a lookup.
-    const uint16_t *const pool_k = p.pool_k, *const pool_v = p.pool_v;
-    const uint16_t *const k_new = p.k_new, *const v_new = p.v_new;
-    const int64_t n_pre_pages = p.n_pre_pages, Ts = p.Ts;
-    const int nkv = p.nkv;
-    const __attribute__((address_space(4))) int32_t *pages_c =
-        (const __attribute__((address_space(4))) int32_t *)p.pages;
-    auto load_pids = [&](int64_t b, int32_t (&pid)[CPW]) {
+    auto load_pids = [&](int b, int32_t (&pid)[CPW]) {
 #pragma unroll
         for (int u = 0; u < CPW; ++u) {
-            const int64_t v = b * 4 + (u * WAVES + wave) / CPP;
+            const int v = b * 4 + (u * WAVES + wave) / CPP;
             pid[u] = v < n_pre_pages ? pages_c[v] : 0;
         }
     };
@@ -360,22 +373,23 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
         klane[u] = (uint32_t)(r * D + ck * 8) * 2;
         vlane[u] = (uint32_t)(r * D + cv * 8) * 2;
     }
-    auto issue_block = [&](int64_t b, int buf, const int32_t (&pid)[CPW]) {
+    auto issue_block = [&](int b, int buf, const int32_t (&pid)[CPW]) {
         uint16_t *kt_lds = lds + buf * 2 * TILE;
         uint16_t *vt_lds = kt_lds + TILE;
 #pragma unroll
         for (int u = 0; u < CPW; ++u) {
             const int q = u * WAVES + wave;                   // chunk index, uniform per wavefront
-            const int64_t v = b * 4 + q / CPP;                // page of the key sequence
+            const int v = b * 4 + q / CPP;                    // page of the key sequence
             if (v < n_pre_pages) {
                 const int64_t blk = ((int64_t)pid[u] * nkv + g) * head_block;
                 dma16(pool_k + blk, klane[u], kt_lds + q * 512);
                 dma16(pool_v + blk, vlane[u], vt_lds + q * 512);
             } else {
                 // suffix token; rows past the last one repeat it (finite, and masked)
-                int64_t T = (v - n_pre_pages) * PAGE + rr[u];
+                int T = (v - n_pre_pages) * PAGE + rr[u];
                 if (T > Ts - 1) T = Ts - 1;
-                const uint32_t rw = (uint32_t)((T * nkv + g) * D - rr[u] * D) * 2;
+                // below 2^31: the host limits T_s * n_kv * d * 2 bytes
+                const uint32_t rw = ((uint32_t)(T * nkv + g) * D - (uint32_t)rr[u] * D) * 2;
                 dma16(k_new, rw + klane[u], kt_lds + q * 512);
                 dma16(v_new, rw + vlane[u], vt_lds + q * 512);
             }
@@ -410,10 +424,10 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
     // dropped the kept value).
     // (The limits are shifted by this half-wave's key offset so that each
     // comparison is against a constant: no per-lane key index stays live.)
-    auto mask_block = [&](int64_t b) {
+    auto mask_block = [&](int b) {
         const int sh = 8 * half;
-        const int pe = (int)(p.Tp - b * KB) - sh;
-        const int ps = (int)(p.n_pre_pages * PAGE - b * KB) - sh;
+        const int pe = Tp - b * KB - sh;
+        const int ps = n_pre_pages * PAGE - b * KB - sh;
         const int lim = tok + ps;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
@@ -427,7 +441,7 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
     // Q operands are in registers before the key loop starts (a wait the
     // compiler sees, so it places none of its own inside the loop)
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-    const int nb = (int)(b1 > b0 ? b1 - b0 : 0);
+    const int nb = b1 > b0 ? b1 - b0 : 0;
     int32_t pid[CPW];
     if (nb > 0) {
         load_pids(b0, pid);
@@ -457,29 +471,29 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
         lds_barrier();
         if (j + 2 < nb) issue_block(b0 + j + 2, (j + 2) % NBUF, pid);
         if (j + 3 < nb) load_pids(b0 + j + 3, pid);
-        const int64_t b = b0 + j;
-        if (j < nb && (b + 1) * 4 > full_pre_pages && b * 4 <= full_pre_pages && full_pre_pages < p.n_pre_pages) {
+        const int b = b0 + j;
+        if (j < nb && (b + 1) * 4 > full_pre_pages && b * 4 <= full_pre_pages && full_pre_pages < n_pre_pages) {
             // last, partial prefix page: its slots past Tp may hold anything;
             // zero them so masked keys contribute exactly nothing (the V
             // tile is first read after the next barrier)
             uint16_t *V = lds + (j % NBUF) * 2 * TILE + TILE;
-            const int pg = (int)(full_pre_pages - b * 4), k0 = (int)(p.Tp % PAGE);
+            const int pg = full_pre_pages - b * 4, k0 = Tp % PAGE;
             for (int idx = tid; idx < D * (PAGE - k0); idx += THREADS) V[(pg * PAGE + k0) * D + idx] = 0;
         }
     };
     // A block needs the mask only if it holds slots of the prefix's partial
     // last page, or suffix keys that some row of this wavefront does not see
     // yet (the wavefront's rows start at token tok_min).
-    const int tok_min = (int)(((int64_t)mt * TILE_ROWS + wave * WAVE_ROWS) / p.grp);
+    const int tok_min = (mt * TILE_ROWS + wave * WAVE_ROWS) / grp;
     auto softmax_block = [&](int j) {
-        const int64_t b = b0 + j;
+        const int b = b0 + j;
         if ((b + 1) * 4 > full_pre_pages) {
-            const int64_t ps = p.n_pre_pages * PAGE - b * KB, pe = p.Tp - b * KB;
-            const bool partial_prefix = ps > 0 && pe < (ps < KB ? ps : (int64_t)KB);
+            const int ps = n_pre_pages * PAGE - b * KB, pe = Tp - b * KB;
+            const bool partial_prefix = ps > 0 && pe < (ps < KB ? ps : KB);
             const bool unseen_suffix = ps < KB && KB - 1 - ps > tok_min;
             if (partial_prefix || unseen_suffix) mask_block(b);
         }
-        softmax_phase<D>(w, p.scale_log2);
+        softmax_phase<D>(w, scale_log2);
     };
     // Each group runs its own copy of the loop (one straight path each, so
     // the accumulators keep their registers); both execute the same barriers.
@@ -522,10 +536,10 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
 
     const float l_tot = half_swap_sum(w.l);
     if (!row_ok) return;
-    if (p.n_split == 1) {
+    if (n_split == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        const int head = g * p.grp + (int)(row % p.grp);
-        uint16_t *orow = p.out + ((int64_t)tok * p.nq + head) * D;
+        const int head = g * grp + row % grp;
+        uint16_t *orow = out_ptr + ((int64_t)tok * nq + head) * D;
 #pragma unroll
         for (int et = 0; et < D / 32; ++et)
 #pragma unroll
@@ -534,8 +548,8 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
                 *reinterpret_cast<bf16x4 *>(orow + et * 32 + vq * 8 + half * 4) = __builtin_convertvector(o4 * inv, bf16x4);
             }
     } else {
-        const int64_t prow = ((int64_t)split * p.nkv + g) * p.rows_pad + row;
-        float *orow = p.o_part + prow * D;
+        const int64_t prow = ((int64_t)split * nkv + g) * rows_pad + row;
+        float *orow = o_part + prow * D;
 #pragma unroll
         for (int et = 0; et < D / 32; ++et)
 #pragma unroll
@@ -544,8 +558,8 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
                 *reinterpret_cast<f32x4 *>(orow + et * 32 + vq * 8 + half * 4) = o4;
             }
         if (half == 0) {
-            p.ml_part[prow * 2 + 0] = w.m;
-            p.ml_part[prow * 2 + 1] = l_tot;
+            ml_part[prow * 2 + 0] = w.m;
+            ml_part[prow * 2 + 1] = l_tot;
         }
     }
 }

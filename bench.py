@@ -345,7 +345,7 @@ def write_path(oc, wl, layout, pool, reqs, passes):
     return out
 
 
-def ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev):
+def ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev, sweep=True):
     """TTFT of the four modes (HBM-resident and device-staged trials given),
     added TTFT at the cap, the eq. (3) floor and the device-staged gate."""
     L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
@@ -370,8 +370,11 @@ def ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev):
                "arrival_floor_ms": round(L * layer_bytes / args.cap * 1e3, 3)}
     res["gates"] = {"device_staged_over_hbm": round((ttft["device_staged"][0] - ttft["hbm_resident"][0]) /
                                                     ttft["hbm_resident"][0], 4)}
-    if not args.no_producer and args.sweep_rates:
+    if not args.no_producer and args.sweep_rates and sweep:
         res["delivery_sweep"] = delivery_sweep(oc, wl, layout, pool, reqs, args, ttft["device_staged"][0] / L)
+        sens = bandwidth_sensitivity(res["delivery_sweep"])
+        if sens:
+            res["bandwidth_sensitivity"] = sens
     return ttft, res
 
 
@@ -387,14 +390,16 @@ def delivery_sweep(oc, wl, layout, pool, reqs, args, c_layer_ms):
     / rate, C_l = the measured device-staged time per layer."""
     L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
     layer_bytes = sum(wl.prefix_tokens) * b
-    trials = max(2, args.trials // 2)
     out = []
     for gbs in [float(x) for x in args.sweep_rates.split(",")]:
         rate = gbs * 1e9
-        if rate > 0 and L * layer_bytes / rate > args.sweep_max_s:
+        trial_s = L * layer_bytes / rate if rate > 0 else 0.0
+        if trial_s > args.sweep_max_s:
             out.append({"rate_GBps": gbs, "skipped": f"over {args.sweep_max_s} s per trial"})
             continue
-        row = {"rate_GBps": gbs if rate > 0 else "uncapped"}
+        # rates whose trial takes seconds: one timed trial after the discarded first
+        trials = 2 if trial_s > 2.0 else max(2, args.trials // 2)
+        row = {"rate_GBps": gbs if rate > 0 else "uncapped", "timed_trials": trials - 1}
         for name in ("layerwise", "chunkwise"):
             runs = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, trials, rate_bytes_per_s=rate,
                             delivery=name)
@@ -406,6 +411,17 @@ def delivery_sweep(oc, wl, layout, pool, reqs, args, c_layer_ms):
         out.append(row)
         log(f"[bench] {wl.name} delivery sweep {gbs} GB/s done")
     return out
+
+
+def bandwidth_sensitivity(sweep, low=1.25, high=12.5):
+    """Relative TTFT increase at `low` GB/s over `high` GB/s (10 over 100
+    Gbps: the paper's bandwidth-sensitivity comparison), per delivery."""
+    rows = {r["rate_GBps"]: r for r in sweep if "skipped" not in r}
+    if low not in rows or high not in rows:
+        return None
+    return {"rates_GBps": [low, high],
+            **{f"{name}_increase": round(rows[low][f"{name}_ms"][0] / rows[high][f"{name}_ms"][0] - 1.0, 4)
+               for name in ("layerwise", "chunkwise")}}
 
 
 POLICIES = ["fifo", "equal", "kv_prop", "bw_prop", "stall_opt", "cal_stall_opt"]
@@ -519,7 +535,6 @@ def canonical_cells(args):
     chunkwise closed form with X_l = layer bytes / cap and C_l measured."""
     import torch
     import kvgen
-    import oracle.model as model
     import paper_2605_22850_amd as oc
     torch.cuda.set_device(0)
     L, nq, nkv, d, F, Ps, G = 32, 32, 8, 128, 14336, 16, args.cells_chunk
@@ -580,8 +595,8 @@ def canonical_cells(args):
         res["ttft_ms"] = {k: round(v, 2) for k, v in ttft.items()}
         res["compute_ms_per_layer"] = round(float(np.mean(c_ms)), 3)
         res["transfer_ms_per_layer_at_cap"] = round(x_ms[0], 3)
-        res["eq3_ms"] = round(model.layerwise_ttft(x_ms, c_ms), 2)
-        res["chunkwise_model_ms"] = round(model.chunkwise_ttft(x_ms, c_ms), 2)
+        res["eq3_ms"] = round(layerwise_floor(x_ms, c_ms), 2)
+        res["chunkwise_model_ms"] = round(chunkwise_floor(x_ms, c_ms), 2)
         base = ttft["hbm_resident"]
         res["added_over_hbm_pct"] = {k: round((v - base) / base * 100, 2) for k, v in ttft.items()
                                      if k != "hbm_resident"}
@@ -591,12 +606,53 @@ def canonical_cells(args):
         res["attention_gflop_per_layer"] = round(flops / 1e9, 1)
         res["gemm_gflop_per_layer"] = round(2 * ts * sum(K * N for K, N in shapes) / 1e9, 1)
         res["layer_tflops"] = round((flops + 2 * ts * sum(K * N for K, N in shapes)) / (np.mean(c_ms) / 1e3) / 1e12, 1)
+        # the overlap requirement of Section 5.3: the rate at which a layer's
+        # transfer takes exactly its compute window
+        res["required_GBps"] = round(tp * b / (np.mean(c_ms) / 1e3) / 1e9, 3)
+        if args.cells_rates:
+            sweep = []
+            for gbs in [float(x) for x in args.cells_rates.split(",")]:
+                rate = gbs * 1e9
+                row = {"rate_GBps": gbs}
+                for name in ("layerwise", "chunkwise"):
+                    if gbs * 1e9 == args.cap:
+                        key = f"capped_{name}"
+                        row[f"{name}_ms"] = round(ttft[key], 2)
+                        continue
+                    runs_r = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_PRODUCER, 2, rate_bytes_per_s=rate,
+                                      delivery=name, **kw)
+                    row[f"{name}_ms"] = round(float(runs_r[1][1][0]["ttft_ms"]), 2)
+                xr = [tp * b / rate * 1e3] * L
+                row["eq3_ms"] = round(layerwise_floor(xr, c_ms), 2)
+                row["chunkwise_model_ms"] = round(chunkwise_floor(xr, c_ms), 2)
+                sweep.append(row)
+            res["rate_sweep"] = sweep
+            res["bandwidth_sensitivity"] = bandwidth_sensitivity(
+                [{"rate_GBps": r["rate_GBps"], "layerwise_ms": [r["layerwise_ms"]],
+                  "chunkwise_ms": [r["chunkwise_ms"]]} for r in sweep], 1.25, args.cap / 1e9)
         out["cells"].append(res)
         log(f"[bench] cell {ctx_len} @ {hit}: ttft {res['ttft_ms']} eq3 {res['eq3_ms']} "
             f"C/layer {res['compute_ms_per_layer']} ms X/layer {res['transfer_ms_per_layer_at_cap']} ms")
         del pool, table, q, kn, vn, outt, reqs, runs
         torch.cuda.empty_cache()
     return out
+
+
+def cpu_model():
+    """The host CPU's model name as lscpu reports it (else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in out.splitlines():
+            if ln.strip().startswith("Model name:"):
+                return ln.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "unknown")
+    except OSError:
+        return "unknown"
 
 
 def cpu_baseline(wl, objs_all, tables, budget_s):
@@ -608,11 +664,12 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
     n = objs.shape[0]
     tp = wl.prefix_tokens[0]
     pool = np.zeros(oracle.pool_shape(1, wl.pool_pages, nkv, Ps, d), dtype=np.uint16)
+    threads = min(16, len(os.sched_getaffinity(0)))     # the host share of one GPU
     layers, secs = 0, 0.0
     while layers < L and (layers == 0 or secs < budget_s * 0.5):
         staging = np.ascontiguousarray(objs[:, layers, :]).reshape(-1)
         t = time.perf_counter()
-        oracle.ingest_layer(staging, n, G, nkv, d, Ps, table, pool, 0)
+        oracle.ingest_layer(staging, n, G, nkv, d, Ps, table, pool, 0, threads=threads)
         secs += time.perf_counter() - t
         layers += 1
     ingest_gbs = 2.0 * layers * tp * 2 * nkv * d * 2 / secs / 1e9
@@ -624,7 +681,6 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
     vn = kvgen.suffix_tensor(wl.seed, kvgen.KIND_VNEW, 0, 0, (ts, nkv, d))
     chunks = [np.ascontiguousarray(objs[j]).reshape(-1) for j in range(n)]
     k, v = oracle.logical_kv(chunks, G, nkv, d, 0)
-    threads = len(os.sched_getaffinity(0))
     rows, flops, asecs = [], 0.0, 0.0
     step = max(1, ts // 64)
     for i in range(ts - 1, -1, -step):
@@ -635,18 +691,13 @@ def cpu_baseline(wl, objs_all, tables, budget_s):
         asecs += time.perf_counter() - t
         rows.append(i)
         flops += 4.0 * nq * d * (tp + i + 1)
-    cpu = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu)
-    except OSError:
-        pass
+    cpu = cpu_model()
     rate = flops / asecs                                    # flop/s of the sampled rows
     layer_flops = attn_flops(nq, d, tp, ts)
     return {
-        "value": round(ingest_gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle", "cpu": cpu,
-        "sample": f"oracle byte-loop ingest (single thread) of {layers} of {L} layer payloads of request 0 "
-                  f"({layers * tp} tokens x {2 * nkv * d * 2} B, read + written)",
+        "value": round(ingest_gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle", "cpu": cpu,
+        "sample": f"oracle byte-loop ingest ({threads} threads over the chunks) of {layers} of {L} layer "
+                  f"payloads of request 0 ({layers * tp} tokens x {2 * nkv * d * 2} B, read + written)",
         "attention": {"gflops": round(rate / 1e9, 4), "cores": threads, "rows": len(rows),
                       "sample": f"float64 attention of {len(rows)} suffix rows x {nq} heads of layer 0 over "
                                 f"{tp} prefix keys, {threads} threads",
@@ -689,6 +740,69 @@ def zero_kv(args):
                      "attention_ms_per_layer": round(ms, 4)}
         log(f"[bench] {name} pool: {out[name]}")
     return {"workload": wl.name, "trials": trials - 1, **out}
+
+
+def step_ingest(stats_all, wl):
+    """In-step ingest of timed pipeline runs: algorithmic bytes (read + write
+    of every layer payload) over the summed time between each layer's landed
+    and ingested events on the copy stream."""
+    L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
+    ingest_ms, n = 0.0, 0
+    for st in stats_all:
+        for rst in st:
+            for l in range(L):
+                ingest_ms += rst["ingested_ms"][l] - rst["landed_ms"][l]
+                n += 1
+    nbytes = 2.0 * sum(wl.prefix_tokens) * b * L * len(stats_all)
+    gbs = nbytes / (ingest_ms / 1e3) / 1e9
+    return {"value": round(gbs, 2), "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "launches": n,
+            "mean_launch_us": round(ingest_ms / n * 1e3, 3), "bytes_per_launch": nbytes / n}
+
+
+def workload_legs(oc, name, args):
+    """One more workload, every figure the main one reports: timed
+    device-staged steps (in-step ingest), the four TTFT modes with the gates,
+    the attention rate and the isolated ingest.  Frees its device memory."""
+    import torch
+    import kvgen
+    wl = kvgen.workload(name)
+    L, nq, d, R = wl.num_layers, wl.num_q_heads, wl.head_dim, wl.n_requests
+    layout, pool, reqs, _, _ = setup(wl)
+    buf = torch.empty(1 << 27, dtype=torch.int16, device="cuda")
+    warm_device(torch.cuda.current_stream(), lambda: buf.fill_(1))
+    del buf
+    run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, 2)
+    ctx = oc.oc_context_create(pool, layout, oc.OC_MODE_DEVICE_STAGED, max(wl.prefix_tokens),
+                               max(wl.suffix_tokens), **RUN_OPTS)
+    steps = max(2, args.other_steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    stats_all = [oc.oc_pipeline_run(ctx, reqs, L) for _ in range(steps)]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    oc.oc_context_destroy(ctx)
+    out = {"workload": wl.name, "layers": L, "q_heads": nq, "kv_heads": wl.num_kv_heads, "head_dim": d,
+           "prefix_tokens": wl.prefix_tokens if R > 1 else wl.prefix_tokens[0],
+           "suffix_tokens": wl.suffix_tokens if R > 1 else wl.suffix_tokens[0],
+           "steps": steps, "ms_per_step": round(wall / steps * 1e3, 3),
+           "ingest_in_step": step_ingest(stats_all, wl)}
+    trials = max(2, args.trials)
+    hbm = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_HBM_RESIDENT, trials)
+    dev = run_mode(oc, pool, layout, wl, reqs, oc.OC_MODE_DEVICE_STAGED, trials)
+    tflops, op_ms = attention_rate(wl, hbm[1:])
+    out["attention"] = {"roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": BF16_PEAK_TFLOPS,
+                                     "unit": "TFLOP/s", "frac": round(tflops / BF16_PEAK_TFLOPS, 4)},
+                        "op_ms_per_layer": round(op_ms, 4),
+                        "launch": "one per layer for all requests" if R > 1 and not RUN_OPTS.get(
+                            "attention_per_request") else "one per request and layer"}
+    out["ttft_ms"], res = ttft_legs(oc, wl, layout, pool, reqs, args, hbm, dev, sweep=False)
+    out.update(res)
+    if args.isolated_passes > 0:
+        out["ingest_isolated"] = isolated_ingest(oc, wl, layout, pool, reqs, max(2, args.isolated_passes))
+    del pool, reqs, hbm, dev
+    torch.cuda.empty_cache()
+    log(f"[bench] {wl.name} legs done")
+    return out
 
 
 def run_bench(args):
@@ -785,19 +899,7 @@ def run_bench(args):
     line.update(res)
     if args.policy_sweep:
         line["policy_sweep"] = policy_sweep(oc, wl, layout, pool, reqs, args, hbm)
-    if args.second_workload and args.second_workload != wl.name:
-        wl2 = kvgen.workload(args.second_workload)
-        del hbm, dev
-        lay2, pool2, reqs2, _, _ = setup(wl2)
-        hbm2 = run_mode(oc, pool2, lay2, wl2, reqs2, oc.OC_MODE_HBM_RESIDENT, trials)
-        dev2 = run_mode(oc, pool2, lay2, wl2, reqs2, oc.OC_MODE_DEVICE_STAGED, trials)
-        t2, res2 = ttft_legs(oc, wl2, lay2, pool2, reqs2, args, hbm2, dev2)
-        line["second_workload"] = {"workload": wl2.name, "ttft_ms": t2, **res2}
-        if args.isolated_passes > 0:
-            line["second_workload"]["ingest_isolated"] = isolated_ingest(oc, wl2, lay2, pool2, reqs2,
-                                                                         max(4, args.isolated_passes))
-        del pool2, reqs2
-        log(f"[bench] {wl2.name} ttft legs done")
+    del hbm, dev
     if args.isolated_passes > 0:
         line["ingest_isolated"] = isolated_ingest(oc, wl, layout, pool, reqs, args.isolated_passes)
         log("[bench] isolated ingest done")
@@ -809,6 +911,12 @@ def run_bench(args):
             del pool3, reqs3
         line["write_path"] = write_path(oc, wl, layout, pool, reqs, args.isolated_passes)
         log("[bench] write path done")
+    # the other workloads, one at a time (the main one's device memory freed first)
+    others = [w for w in args.other_workloads.split(",") if w and w != wl.name]
+    if others:
+        del pool, reqs
+        torch.cuda.empty_cache()
+        line["workloads"] = {w: workload_legs(oc, w, args) for w in others}
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
         line["cpu_baseline"] = cpu_baseline(wl, objs_all, tables, args.cpu_budget)
@@ -962,7 +1070,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep-rates", default="1.25,12.5,50,0",
                     help="producer rates (GB/s, 0 = uncapped) of the layerwise/chunkwise sweep; empty: skip")
-    ap.add_argument("--sweep-max-s", type=float, default=2.0, help="skip sweep rates whose payload takes longer")
+    ap.add_argument("--sweep-max-s", type=float, default=8.0, help="skip sweep rates whose payload takes longer")
     ap.add_argument("--policy-sweep", action="store_true",
                     help="run every bandwidth allocation policy under the cap (meant for --workload batch8)")
     ap.add_argument("--scheduler-workloads", default="",
@@ -973,10 +1081,15 @@ def main():
                     help="run the end-to-end TTFT cells (4K/64K x 12.5/50/87.5%% hits) with the whole layer's "
                          "compute instead")
     ap.add_argument("--cells-chunk", type=int, default=64, help="chunk tokens G of the canonical cells")
+    ap.add_argument("--cells-rates", default="1.25,2.5,5,12.5,25,50",
+                    help="producer rates (GB/s) of the canonical cells' layerwise/chunkwise sweep ('' to skip); "
+                         "one timed trial each after a discarded first")
     ap.add_argument("--policy-margin", type=float, default=0.625e9,
                     help="Calibrated Stall-opt margin, bytes/s (0.625e9 = 5 Gbps)")
-    ap.add_argument("--second-workload", default="8b-4k",
-                    help="workload whose TTFT legs are reported beside the main one ('' to skip)")
+    ap.add_argument("--other-workloads", default="8b-4k,batch8,70b-32k",
+                    help="workloads whose steps, TTFT legs, attention and isolated ingest are reported beside "
+                         "the main one, comma-separated ('' to skip)")
+    ap.add_argument("--other-steps", type=int, default=5, help="timed device-staged steps of each other workload")
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"{CALIB_COPIES} plain {CALIB_BYTES >> 20} MiB device copies before the steps")
     ap.add_argument("--attention-per-request", action="store_true",

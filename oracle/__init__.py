@@ -46,6 +46,8 @@ def _load():
         lib.oco_logical_kv.restype = None
         lib.oco_ingest_layer.argtypes = [P, I64, I32, I32, I32, I32, P, I64, P, I64, I32]
         lib.oco_ingest_layer.restype = ctypes.c_int
+        lib.oco_ingest_layer_mt.argtypes = [P, I64, I32, I32, I32, I32, P, I64, P, I64, I32, I32]
+        lib.oco_ingest_layer_mt.restype = ctypes.c_int
         lib.oco_gather_layer.argtypes = [P, I64, I32, P, I64, I64, I32, I32, I32, I32, P]
         lib.oco_gather_layer.restype = ctypes.c_int
         lib.oco_append_suffix.argtypes = [P, P, I64, I32, I32, I32, P, I64, I64, P, I64, I32]
@@ -102,8 +104,10 @@ def pool_shape(L: int, P: int, n_kv: int, Ps: int, d: int):
 
 
 def ingest_layer(staging: np.ndarray, n_chunks: int, G: int, n_kv: int, d: int, Ps: int,
-                 table: np.ndarray, pool: np.ndarray, layer: int) -> None:
-    """Scatter a staging payload into ``pool`` (uint16, shape pool_shape) in place."""
+                 table: np.ndarray, pool: np.ndarray, layer: int, threads: int = 1) -> None:
+    """Scatter a staging payload into ``pool`` (uint16, shape pool_shape) in
+    place; with threads > 1 the chunks are divided over that many threads
+    (same result for a table of distinct page ids)."""
     lib = _load()
     staging = _u16(staging.view(np.uint16) if staging.dtype == np.uint8 else staging)
     table = np.ascontiguousarray(table, dtype=np.int32)
@@ -112,8 +116,12 @@ def ingest_layer(staging: np.ndarray, n_chunks: int, G: int, n_kv: int, d: int, 
     P = pool.shape[2]
     if staging.size != n_chunks * 2 * G * n_kv * d:
         raise ValueError("staging size does not match n_chunks * S")
-    rc = lib.oco_ingest_layer(_ptr(staging), n_chunks, G, n_kv, d, Ps, _ptr(table), table.size,
-                              _ptr(pool), P, layer)
+    if threads > 1:
+        rc = lib.oco_ingest_layer_mt(_ptr(staging), n_chunks, G, n_kv, d, Ps, _ptr(table), table.size,
+                                     _ptr(pool), P, layer, threads)
+    else:
+        rc = lib.oco_ingest_layer(_ptr(staging), n_chunks, G, n_kv, d, Ps, _ptr(table), table.size,
+                                  _ptr(pool), P, layer)
     if rc != 0:
         raise ValueError("block table entry out of range or too short")
 

@@ -75,11 +75,11 @@ static int64_t pool_index(int32_t l, int32_t m, int64_t page, int32_t h, int32_t
  * chunk objects, prefix order) into the pool.  Token T = j*G + t of the prefix
  * lands in page table[T / Ps], slot T % Ps.  Returns 0, or -1 when a table
  * entry is outside [0, P). */
-int oco_ingest_layer(const uint16_t *staging, int64_t n_chunks, int32_t G, int32_t n_kv, int32_t d,
-                     int32_t Ps, const int32_t *table, int64_t table_len, uint16_t *pool, int64_t P,
-                     int32_t layer) {
+static int ingest_chunk_range(const uint16_t *staging, int64_t j0, int64_t j1, int32_t G, int32_t n_kv,
+                              int32_t d, int32_t Ps, const int32_t *table, int64_t table_len, uint16_t *pool,
+                              int64_t P, int32_t layer) {
     int64_t slice = 2LL * G * n_kv * d;
-    for (int64_t j = 0; j < n_chunks; ++j)
+    for (int64_t j = j0; j < j1; ++j)
         for (int32_t m = 0; m < 2; ++m)
             for (int32_t t = 0; t < G; ++t)
                 for (int32_t h = 0; h < n_kv; ++h)
@@ -94,6 +94,57 @@ int oco_ingest_layer(const uint16_t *staging, int64_t n_chunks, int32_t G, int32
                             staging[src];
                     }
     return 0;
+}
+
+int oco_ingest_layer(const uint16_t *staging, int64_t n_chunks, int32_t G, int32_t n_kv, int32_t d,
+                     int32_t Ps, const int32_t *table, int64_t table_len, uint16_t *pool, int64_t P,
+                     int32_t layer) {
+    return ingest_chunk_range(staging, 0, n_chunks, G, n_kv, d, Ps, table, table_len, pool, P, layer);
+}
+
+/* The same scatter with the chunks divided into `threads` contiguous ranges,
+ * one thread each.  Chunks write distinct pool elements as long as the page
+ * ids are distinct (the block table's contract), so the result equals
+ * oco_ingest_layer's. */
+struct ingest_job {
+    const uint16_t *staging;
+    int64_t j0, j1;
+    int32_t G, n_kv, d, Ps, layer;
+    const int32_t *table;
+    int64_t table_len, P;
+    uint16_t *pool;
+    int rc;
+};
+
+static void *ingest_worker(void *arg) {
+    struct ingest_job *J = (struct ingest_job *)arg;
+    J->rc = ingest_chunk_range(J->staging, J->j0, J->j1, J->G, J->n_kv, J->d, J->Ps, J->table, J->table_len,
+                               J->pool, J->P, J->layer);
+    return NULL;
+}
+
+int oco_ingest_layer_mt(const uint16_t *staging, int64_t n_chunks, int32_t G, int32_t n_kv, int32_t d,
+                        int32_t Ps, const int32_t *table, int64_t table_len, uint16_t *pool, int64_t P,
+                        int32_t layer, int32_t threads) {
+    if (threads < 1) threads = 1;
+    if (threads > 256) threads = 256;
+    if (threads > n_chunks) threads = n_chunks > 0 ? (int32_t)n_chunks : 1;
+    struct ingest_job jobs[256];
+    pthread_t tid[256];
+    for (int32_t i = 0; i < threads; ++i) {
+        struct ingest_job J = {staging, n_chunks * i / threads, n_chunks * (i + 1) / threads, G, n_kv, d, Ps,
+                               layer, table, table_len, P, pool, 0};
+        jobs[i] = J;
+    }
+    for (int32_t i = 1; i < threads; ++i)
+        if (pthread_create(&tid[i], NULL, ingest_worker, &jobs[i]) != 0) jobs[i].rc = -2;
+    ingest_worker(&jobs[0]);
+    int rc = jobs[0].rc;
+    for (int32_t i = 1; i < threads; ++i) {
+        if (jobs[i].rc != -2) pthread_join(tid[i], NULL);
+        if (jobs[i].rc != 0) rc = jobs[i].rc;
+    }
+    return rc;
 }
 
 /* Inverse of the scatter: read the layer back out of the pool into the

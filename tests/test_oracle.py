@@ -117,6 +117,12 @@ def test_ingest_matches_numpy_formulation(G, Ps, n_chunks, nkv, d):
     # gather undoes scatter
     back = oracle.gather_layer(pool, layer, table, n_chunks, G, nkv, d, Ps)
     assert np.array_equal(back, staging)
+    # the threaded form (the CPU baseline's) gives the same pool, for thread
+    # counts that split the chunks evenly, unevenly and beyond their number
+    for threads in (2, 3, 8):
+        mt = np.full(oracle.pool_shape(L, P, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+        oracle.ingest_layer(staging, n_chunks, G, nkv, d, Ps, table, mt, layer, threads=threads)
+        assert np.array_equal(mt, ref), threads
 
 
 def test_paged_read_returns_logical_token():
@@ -154,9 +160,10 @@ def test_ingest_copies_nan_and_denormal_bits():
 
 def test_ingest_rejects_out_of_range_page():
     pool = np.zeros(oracle.pool_shape(1, 4, 1, 16, 8), dtype=np.uint16)
-    with pytest.raises(ValueError):
-        oracle.ingest_layer(np.zeros(2 * 16 * 8, np.uint16), 1, 16, 1, 8, 16,
-                            np.array([4], np.int32), pool, 0)
+    for threads in (1, 2):
+        with pytest.raises(ValueError):
+            oracle.ingest_layer(np.zeros(2 * 2 * 16 * 8, np.uint16), 2, 16, 1, 8, 16,
+                                np.array([1, 4], np.int32), pool, 0, threads=threads)
 
 
 # ---------------------------------------------------------------------------

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define OC_ABI_VERSION 4
+#define OC_ABI_VERSION 5
 
 typedef enum {
     OC_OK = 0,
@@ -256,9 +256,12 @@ int oc_rest_of_layer(const void *attn_out, int64_t tokens, const oc_layout *layo
  * (appendix pseudocode "layerwise GET"), paced to a byte rate, and signals
  * layer-ready.  With several requests sharing one rate (OC_ALLOC_FIFO),
  * layers are delivered layer-major, request-minor (round-robin); with an
- * allocation policy each request gets its own rate for the run (one
- * scheduling epoch) and the producer dispatches their payload pieces by
- * weighted deficit round robin (Section 3.6 and its appendix pseudocode).
+ * allocation policy each request gets its own rate, fixed from its admission
+ * until its deliveries end: requests that arrive at the start share one
+ * scheduling epoch, later ones are admitted at later boundaries with the
+ * budget then free (oc_epoch_schedule), and the producer dispatches the
+ * admitted requests' payload pieces by weighted deficit round robin
+ * (Section 3.6 and its appendix pseudocode).
  * A request delivered chunkwise (eq. (2)) instead receives its whole chunk
  * objects in prefix order, as many per staging slot as fit; each group is
  * landed and ingested with oc_kv_chunks_ingest, and its L layers' attention
@@ -289,6 +292,24 @@ typedef enum {
 int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes,
                           const double *layer_compute_s, double budget_bytes_per_s,
                           double margin_bytes_per_s, double *rates_out);
+
+/* Host-only: the scheduling epochs of Section 3.6 for requests that arrive
+ * over time.  Request i arrives at arrival_s[i] (seconds, >= 0) and moves
+ * num_layers payloads of layer_bytes[i].  At each epoch boundary the requests
+ * that have arrived and wait are admitted together; they share, under
+ * `policy` (as oc_bandwidth_allocate), the budget the admitted requests still
+ * in flight do not hold.  An admitted request keeps its rate until its
+ * deliveries end (admission + num_layers * layer_bytes[i] / rate); the rate it
+ * then releases goes to requests admitted at a later boundary, never to one
+ * already in flight.  Boundaries are the multiples of epoch_s (> 0), or, with
+ * epoch_s == 0, every arrival and every end of a delivery.  Outputs:
+ * rates_out[i] (bytes/s) and admit_s_out[i] (the boundary at which request i
+ * was admitted).  Same argument rules as oc_bandwidth_allocate, plus
+ * num_layers >= 1, finite arrival_s >= 0 and epoch_s >= 0; OC_EINVAL
+ * otherwise.  Arrays are caller-owned; nothing is retained. */
+int oc_epoch_schedule(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
+                      int32_t num_layers, const double *arrival_s, double budget_bytes_per_s,
+                      double margin_bytes_per_s, double epoch_s, double *rates_out, double *admit_s_out);
 
 typedef enum {
     OC_MODE_HBM_RESIDENT = 0,  /* pool already holds the prefix: attention only          */
@@ -352,6 +373,9 @@ typedef struct {
                                   stream, so each layer's window C_l is the whole layer's
                                   compute; the struct is copied at context creation, the
                                   weights must outlive the context                        */
+    double epoch_s;            /* with an allocation policy: scheduling epoch length for
+                                  requests with arrival_s > 0 (oc_epoch_schedule); 0 = an
+                                  epoch begins at every arrival and end of a delivery    */
 } oc_pipeline_opts;
 
 /* One request.  Device arrays are [L][...] stacks of the per-layer tensors. */
@@ -370,6 +394,10 @@ typedef struct {
     double layer_compute_s;               /* c_i for the allocation policies (seconds per
                                              layer), and the emulated window with
                                              emulate_compute; otherwise ignored             */
+    double arrival_s;                     /* seconds after the run starts at which the
+                                             request arrives; > 0 only with an allocation
+                                             policy (its rate and admission then follow
+                                             oc_epoch_schedule)                             */
 } oc_request;
 
 /* Per-request timings (milliseconds from the start of the run, all on one
@@ -377,13 +405,15 @@ typedef struct {
  * For a request delivered chunkwise, produced/landed/ingested of every layer
  * are those of its last chunk group (the time every layer became usable). */
 typedef struct {
-    double ttft_ms;            /* start -> this request's last layer done          */
+    double ttft_ms;            /* arrival -> this request's last layer done        */
     double *produced_ms;       /* host: layer payload fully in its pinned slot     */
     double *landed_ms;         /* device: payload in HBM (layer-ready)             */
     double *ingested_ms;       /* device: ingest kernel finished                   */
     double *done_ms;           /* device: attention finished                       */
     double rate_bytes_per_s;   /* the request's allocated rate (0 under FIFO)      */
     int32_t delivery;          /* the delivery the request got (oc_delivery)       */
+    double admitted_ms;        /* the epoch boundary at which the request was
+                                  admitted (its deliveries are paced from there)  */
 } oc_request_stats;
 
 /* Create a context on `device` for one pool.  Allocates the streams, events,

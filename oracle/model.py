@@ -12,7 +12,10 @@ Closed forms written from the paper:
   * Section 3.6, eq. (4): per-layer stall and the zero-stall rate r* = s/c;
   * Section 3.6, eqs. (5)-(7) and the evaluation's baselines: per-request
     bandwidth under a shared cap B -- Equal, KV-prop, BW-prop, Stall-opt and
-    Calibrated Stall-opt.
+    Calibrated Stall-opt;
+  * Section 3.6, the scheduling-epoch rule: rates stay fixed while a
+    request's KV loads, and a finished request's rate returns to the pool
+    for the next epoch only.
 """
 from __future__ import annotations
 
@@ -144,3 +147,69 @@ def alloc_cal_stall_opt(B: float, s: Sequence[float], c: Sequence[float], delta:
 def total_stall(s: Sequence[float], c: Sequence[float], r: Sequence[float]) -> float:
     """Sum of the per-layer stalls of eq. (4)."""
     return sum(per_layer_stall(a, x, b) for a, b, x in zip(s, c, r))
+
+
+# ---------------------------------------------------------------------------
+# scheduling epochs (Section 3.6).  Requests arrive over time; in each
+# scheduling epoch the requests that have arrived and are not yet served are
+# admitted as one batch under the budget not held by requests still loading,
+# with the batch's policy.  A request keeps its rate until its L layer
+# payloads are delivered; the rate it frees goes back to the pool and is only
+# handed out at a later epoch, never to a request already loading.  Reading
+# taken where the paper gives no epoch length: with epoch > 0, epochs begin
+# at the multiples of `epoch`; with epoch == 0, an epoch begins whenever a
+# request arrives or finishes its delivery.
+# ---------------------------------------------------------------------------
+
+def epoch_schedule(policy: str, s: Sequence[float], c, L: int, arrival: Sequence[float], B: float,
+                   delta: float = 0.0, epoch: float = 0.0):
+    """(rates, admission times) of requests with per-layer bytes s[i],
+    per-layer compute c[i] (the policies that use it), L layers and arrival
+    times arrival[i], under budget B.  policy: equal, kv_prop, bw_prop,
+    stall_opt or cal_stall_opt (margin delta)."""
+    n = len(s)
+
+    def allocate(budget, idx):
+        ss = [s[i] for i in idx]
+        cc = [c[i] for i in idx] if c is not None else None
+        if policy == "equal":
+            return alloc_equal(budget, len(idx))
+        if policy == "kv_prop":
+            return alloc_kv_prop(budget, ss)
+        if policy == "bw_prop":
+            return alloc_bw_prop(budget, ss, cc)
+        if policy == "stall_opt":
+            return alloc_stall_opt(budget, ss, cc)
+        if policy == "cal_stall_opt":
+            return alloc_cal_stall_opt(budget, ss, cc, delta)
+        raise ValueError(policy)
+
+    rate, admit = [None] * n, [None] * n
+
+    def end(i):                       # when request i's last payload byte goes out
+        return admit[i] + L * s[i] / rate[i]
+
+    def epoch_start(t):               # the first epoch beginning at or after t
+        if epoch == 0:
+            return t
+        k = -(-t // epoch)            # ceil
+        while k * epoch < t:
+            k += 1
+        return k * epoch
+
+    t = epoch_start(0.0)
+    while any(a is None for a in admit):
+        loading = [i for i in range(n) if admit[i] is not None and end(i) > t]
+        free = B - sum(rate[i] for i in loading)
+        batch = [i for i in range(n) if admit[i] is None and arrival[i] <= t]
+        if batch and free > 1e-9 * B:
+            for i, r in zip(batch, allocate(free, batch)):
+                rate[i], admit[i] = r, t
+        # the next epoch: after the next arrival or end of a delivery
+        later = [arrival[i] for i in range(n) if admit[i] is None and arrival[i] > t]
+        later += [end(i) for i in range(n) if admit[i] is not None and end(i) > t]
+        if any(a is None for a in admit):
+            if not later:
+                raise RuntimeError("requests wait while nothing loads")
+            t = epoch_start(min(later))
+    return rate, admit

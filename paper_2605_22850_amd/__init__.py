@@ -9,5 +9,5 @@ from ._lib import (  # noqa: F401
     oc_block_table_check, oc_context_create, oc_context_destroy, oc_kv_layer_gather, oc_kv_layer_ingest,
     oc_pipeline_last_ms, oc_pipeline_run, oc_suffix_prefill_layer, oc_bandwidth_allocate, ALLOC_POLICIES,
     DELIVERIES, oc_kv_chunks_ingest, oc_kv_chunks_gather, oc_kv_suffix_append, LayerWeights, oc_rest_of_layer,
-    oc_suffix_prefill_layer_noalloc, OC_NOALLOC_WORKSPACE_BYTES,
+    oc_suffix_prefill_layer_noalloc, OC_NOALLOC_WORKSPACE_BYTES, oc_epoch_schedule,
 )

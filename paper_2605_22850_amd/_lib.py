@@ -29,6 +29,7 @@ EXPORTS = [
     "oc_kv_layer_gather", "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_rest_of_layer",
     "oc_attention_workspace_bytes", "oc_suffix_prefill_layer", "oc_context_create", "oc_pipeline_run",
     "oc_pipeline_last_ms", "oc_context_destroy", "oc_bandwidth_allocate", "oc_suffix_prefill_layer_noalloc",
+    "oc_epoch_schedule",
 ]
 OC_NOALLOC_WORKSPACE_BYTES = 65 << 20
 
@@ -63,7 +64,7 @@ class c_pipeline_opts(ctypes.Structure):
                 ("fault", c_int32), ("fault_layer", c_int32), ("alloc_policy", c_int32),
                 ("margin_bytes_per_s", c_double), ("delivery", c_int32), ("theta_bytes", c_double),
                 ("emulate_compute", c_int32), ("append_suffix", c_int32), ("attention_per_request", c_int32),
-                ("layer_weights", c_void_p)]
+                ("layer_weights", c_void_p), ("epoch_s", c_double)]
 
 
 class c_layer_weights(ctypes.Structure):
@@ -78,13 +79,14 @@ class c_layer_buffers(ctypes.Structure):
 class c_request(ctypes.Structure):
     _fields_ = [("prefix_tokens", c_int64), ("suffix_tokens", c_int64), ("block_table", POINTER(c_block_table)),
                 ("chunk_objects", POINTER(c_void_p)), ("device_payload", c_void_p), ("q", c_void_p),
-                ("k_new", c_void_p), ("v_new", c_void_p), ("out", c_void_p), ("layer_compute_s", c_double)]
+                ("k_new", c_void_p), ("v_new", c_void_p), ("out", c_void_p), ("layer_compute_s", c_double),
+                ("arrival_s", c_double)]
 
 
 class c_request_stats(ctypes.Structure):
     _fields_ = [("ttft_ms", c_double), ("produced_ms", POINTER(c_double)), ("landed_ms", POINTER(c_double)),
                 ("ingested_ms", POINTER(c_double)), ("done_ms", POINTER(c_double)),
-                ("rate_bytes_per_s", c_double), ("delivery", c_int32)]
+                ("rate_bytes_per_s", c_double), ("delivery", c_int32), ("admitted_ms", c_double)]
 
 
 _lib = None
@@ -130,9 +132,12 @@ def lib():
             L.oc_context_destroy.restype = None
         L.oc_bandwidth_allocate.argtypes = [c_int32, c_int32, POINTER(c_double), POINTER(c_double), c_double, c_double,
                                             POINTER(c_double)]
+        L.oc_epoch_schedule.argtypes = [c_int32, c_int32, POINTER(c_double), POINTER(c_double), c_int32,
+                                        POINTER(c_double), c_double, c_double, c_double, POINTER(c_double),
+                                        POINTER(c_double)]
         for name in ("oc_block_table_check", "oc_kv_layer_ingest", "oc_kv_chunks_ingest", "oc_kv_layer_gather",
                      "oc_kv_chunks_gather", "oc_kv_suffix_append", "oc_rest_of_layer", "oc_suffix_prefill_layer",
-                     "oc_suffix_prefill_layer_noalloc", "oc_bandwidth_allocate"):
+                     "oc_suffix_prefill_layer_noalloc", "oc_bandwidth_allocate", "oc_epoch_schedule"):
             getattr(L, name).restype = c_int
         _lib = L
     return _lib
@@ -314,6 +319,7 @@ class Request:
     chunk_objects: object = None       # host numpy uint16 [N][L * S/2], one chunk object per row
     device_payload: object = None      # device [L][Tp * b] bytes, layer payloads back to back
     layer_compute_s: float = 0.0       # per-layer compute window for the allocation policies
+    arrival_s: float = 0.0             # arrival after the run starts (allocation policies only)
 
 
 def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, max_suffix_tokens: int,
@@ -322,12 +328,12 @@ def oc_context_create(pool, layout: Layout, mode: int, max_prefix_tokens: int, m
                       fault_layer: int = 0, device: int = 0, alloc_policy="fifo", margin_bytes_per_s: float = 0.0,
                       delivery="layerwise", theta_bytes: float = 0.0, emulate_compute: bool = False,
                       append_suffix: bool = False, layer_weights: Optional[LayerWeights] = None,
-                      attention_per_request: bool = False):
+                      attention_per_request: bool = False, epoch_s: float = 0.0):
     pol = ALLOC_POLICIES[alloc_policy] if isinstance(alloc_policy, str) else int(alloc_policy)
     dv = DELIVERIES[delivery] if isinstance(delivery, str) else int(delivery)
     opts = c_pipeline_opts(mode, rate_bytes_per_s, piece_bytes, slots, producer_threads, timeout_ms, fault,
                            fault_layer, pol, margin_bytes_per_s, dv, theta_bytes, int(bool(emulate_compute)),
-                           int(bool(append_suffix)), int(bool(attention_per_request)), None)
+                           int(bool(append_suffix)), int(bool(attention_per_request)), None, epoch_s)
     lw = layer_weights.c() if layer_weights is not None else None
     if lw is not None:
         opts.layer_weights = ctypes.cast(ctypes.pointer(lw), c_void_p)     # copied by the library
@@ -366,17 +372,18 @@ def oc_pipeline_run(ctx, requests: Sequence[Request], num_layers: int):
             keep.append(objs)
         creqs[i] = c_request(r.prefix_tokens, r.suffix_tokens, ctypes.pointer(bt), objs,
                              _ptr(r.device_payload), _ptr(r.q), _ptr(r.k_new), _ptr(r.v_new), _ptr(r.out),
-                             r.layer_compute_s)
+                             r.layer_compute_s, r.arrival_s)
         per = [(c_double * num_layers)() for _ in range(4)]
         arrays.append(per)
-        stats[i] = c_request_stats(0.0, *per, 0.0, 0)
+        stats[i] = c_request_stats(0.0, *per, 0.0, 0, 0.0)
     _check(lib().oc_pipeline_run(ctx, creqs, n, stats))
     out = []
     for i in range(n):
         p = arrays[i]
         out.append({"ttft_ms": stats[i].ttft_ms, "produced_ms": list(p[0]), "landed_ms": list(p[1]),
                     "ingested_ms": list(p[2]), "done_ms": list(p[3]), "rate_bytes_per_s": stats[i].rate_bytes_per_s,
-                    "delivery": {v: k for k, v in DELIVERIES.items()}[stats[i].delivery]})
+                    "delivery": {v: k for k, v in DELIVERIES.items()}[stats[i].delivery],
+                    "admitted_ms": stats[i].admitted_ms})
     return out
 
 
@@ -391,3 +398,18 @@ def oc_bandwidth_allocate(policy, layer_bytes, layer_compute_s, budget_bytes_per
     out = (c_double * n)()
     _check(lib().oc_bandwidth_allocate(pol, n, s, c, budget_bytes_per_s, margin_bytes_per_s, out))
     return list(out)
+
+
+def oc_epoch_schedule(policy, layer_bytes, layer_compute_s, num_layers: int, arrival_s, budget_bytes_per_s: float,
+                      margin_bytes_per_s: float = 0.0, epoch_s: float = 0.0):
+    """(rates in bytes/s, admission times in s) of requests arriving at
+    arrival_s under scheduling epochs; `policy` as in oc_bandwidth_allocate."""
+    pol = ALLOC_POLICIES.get(policy, -1) if isinstance(policy, str) else int(policy)
+    n = len(layer_bytes)
+    s = (c_double * n)(*layer_bytes)
+    c = (c_double * n)(*layer_compute_s) if layer_compute_s is not None else None
+    a = (c_double * n)(*arrival_s)
+    rates, admit = (c_double * n)(), (c_double * n)()
+    _check(lib().oc_epoch_schedule(pol, n, s, c, num_layers, a, budget_bytes_per_s, margin_bytes_per_s, epoch_s,
+                                   rates, admit))
+    return list(rates), list(admit)

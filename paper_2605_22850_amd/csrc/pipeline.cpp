@@ -14,6 +14,7 @@
 #include <algorithm>
 #include <atomic>
 #include <chrono>
+#include <cmath>
 #include <condition_variable>
 #include <cstring>
 #include <deque>
@@ -296,11 +297,12 @@ struct Producer {
 };
 
 // ---- per-request rates (allocation policies) --------------------------------
-// Each request is paced by its own clock at its allocated rate for the whole
-// run -- one scheduling epoch: a request that finishes early does not pass
-// its rate on.  The dispatcher hands out payload pieces by weighted deficit
-// round robin to the copy threads, which copy each piece once its release
-// time has come.  A request's credit grows with elapsed time at its rate (the
+// Each request is paced by its own clock at its allocated rate, from its
+// admission (the epoch boundary oc_epoch_schedule gives it) to its last
+// byte: a request that finishes early does not pass its rate on to the
+// others in flight; later admissions get it.  The dispatcher hands out
+// payload pieces by weighted deficit round robin to the copy threads, which
+// copy each piece once its release time has come.  A request's credit grows with elapsed time at its rate (the
 // weight), not by a fixed amount per round: rounds are uneven in length, and
 // a per-round quantum would hold a slow request below its rate whenever its
 // share of a round is smaller than the round's length times its rate.  A request
@@ -315,6 +317,7 @@ struct RateProducer {
     int64_t S;
     Clock::time_point t0;
     std::vector<double> rate;                // bytes/s per request
+    std::vector<double> admit;               // seconds after t0 at which each request's pacing starts
     std::vector<double> *produced_ms;        // per item k = layer * n_reqs + request
     std::vector<hipEvent_t> *landed;         // per item
 
@@ -479,7 +482,7 @@ struct RateProducer {
                     const int64_t j0 = piece[r] * cpp, j1 = std::min(N[r], j0 + cpp);
                     const double bytes = (double)(j1 - j0) * S;
                     if (deficit[r] < bytes) break;
-                    const double release = (cum[r] + bytes) / rate[r];
+                    const double release = admit[r] + (cum[r] + bytes) / rate[r];
                     if (release > now_s() + lookahead_s) break;
                     const int64_t k = item_of(layer[r], r);
                     if (piece[r] == 0) {
@@ -543,6 +546,10 @@ static int validate_requests(Context *c, const oc_request *reqs, int32_t n) {
         if (r.prefix_tokens % l.chunk_tokens) return fail(OC_ESHAPE, who + "prefix is not a whole number of chunks");
         if (r.prefix_tokens > c->max_prefix || r.suffix_tokens > c->max_suffix)
             return fail(OC_ERANGE, who + "longer than the context was created for");
+        if (!(r.arrival_s >= 0.0) || !std::isfinite(r.arrival_s))
+            return fail(OC_EINVAL, who + "arrival_s must be >= 0 and finite");
+        if (r.arrival_s > 0.0 && !(mode == OC_MODE_PRODUCER && c->opts.alloc_policy != OC_ALLOC_FIFO))
+            return fail(OC_EINVAL, who + "arrival_s > 0 needs the producer mode with an allocation policy");
         const int64_t need = (r.prefix_tokens + l.page_size - 1) / l.page_size;
         if (r.block_table->num_entries < need) return fail(OC_ERANGE, who + "block table too short");
         if (need > 0 && !r.block_table->pages) return fail(OC_EINVAL, who + "NULL block table pages");
@@ -771,22 +778,31 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         for (int32_t i = 0; i < n_reqs; ++i) batch_grid += attention_grid(bplan[i]);
     const bool batched = !c->opts.attention_per_request && !emu && !by_rate && n_cw == 0 && n_reqs >= 2 &&
                          n_reqs <= MAX_ATTN_BATCH && batch_grid <= attention_max_grid();
-    std::vector<double> req_rate(n_reqs, 0.0);
+    std::vector<double> req_rate(n_reqs, 0.0), req_admit(n_reqs, 0.0);
     if (by_rate) {
-        std::vector<double> s_i, c_i;
+        // rates and admissions by scheduling epoch; with every arrival at
+        // the start this is one epoch, oc_bandwidth_allocate over all of them
+        std::vector<double> s_i, c_i, a_i;
         std::vector<int32_t> who;
-        for (int32_t r = 0; r < n_reqs; ++r)
+        for (int32_t r = 0; r < n_reqs; ++r) {
+            req_admit[r] = reqs[r].arrival_s;      // nothing to deliver: admitted on arrival
             if (reqs[r].prefix_tokens > 0) {
                 who.push_back(r);
                 s_i.push_back((double)reqs[r].prefix_tokens * (double)b_tok);
                 c_i.push_back(reqs[r].layer_compute_s);
+                a_i.push_back(reqs[r].arrival_s);
             }
+        }
         if (!who.empty()) {
-            std::vector<double> out(who.size());
-            const int rc = oc_bandwidth_allocate(c->opts.alloc_policy, (int32_t)who.size(), s_i.data(), c_i.data(),
-                                                 c->opts.rate_bytes_per_s, c->opts.margin_bytes_per_s, out.data());
+            std::vector<double> out(who.size()), adm(who.size());
+            const int rc = oc_epoch_schedule(c->opts.alloc_policy, (int32_t)who.size(), s_i.data(), c_i.data(), L,
+                                             a_i.data(), c->opts.rate_bytes_per_s, c->opts.margin_bytes_per_s,
+                                             c->opts.epoch_s, out.data(), adm.data());
             if (rc) return rc;
-            for (size_t i = 0; i < who.size(); ++i) req_rate[who[i]] = out[i];
+            for (size_t i = 0; i < who.size(); ++i) {
+                req_rate[who[i]] = out[i];
+                req_admit[who[i]] = adm[i];
+            }
         }
     }
 
@@ -810,6 +826,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
         rprod.S = S;
         rprod.t0 = t0;
         rprod.rate = req_rate;
+        rprod.admit = req_admit;
         rprod.produced_ms = &produced;
         rprod.landed = &landed;
         producer_thread = std::thread([&rprod] { rprod.run(); });
@@ -1061,13 +1078,14 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             const int64_t k = deliv[r] == OC_DELIVERY_CHUNKWISE ? last_group[r] : item_of[(size_t)r * L + layer];
             const int64_t k_marker = batched && mode == OC_MODE_HBM_RESIDENT ? item_of[(size_t)layer] : k;
             oc_request_stats &st = stats[r];
-            if (layer == L - 1) st.ttft_ms = t_done;
+            if (layer == L - 1) st.ttft_ms = t_done - reqs[r].arrival_s * 1e3;
             if (st.produced_ms) st.produced_ms[layer] = produced[k];
             if (st.landed_ms) st.landed_ms[layer] = mode == OC_MODE_HBM_RESIDENT ? 0.0 : ev_ms(ev_start, landed[k]);
             if (st.ingested_ms) st.ingested_ms[layer] = ev_ms(ev_start, ingested[k_marker]);
             if (st.done_ms) st.done_ms[layer] = t_done;
             st.rate_bytes_per_s = req_rate[r];
             st.delivery = deliv[r];
+            st.admitted_ms = req_admit[r] * 1e3;
         }
     c->last_ms = last;
     return OC_OK;

@@ -99,3 +99,80 @@ int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes, 
             return fail(OC_EINVAL, "unknown allocation policy");
     }
 }
+
+// Scheduling epochs (Section 3.6): the rates of oc_bandwidth_allocate for
+// requests that arrive over time.  At each epoch boundary the requests that
+// have arrived and wait are admitted together and share the budget that the
+// requests in flight do not hold, under the policy; a request keeps its rate
+// until its payloads are delivered (its last byte at admission + L s_i / r_i),
+// and the rate it then releases is handed out at the next boundary, never to
+// a request already in flight.  Boundaries are the multiples of epoch_s, or
+// with epoch_s == 0 every arrival and every completion.
+int oc_epoch_schedule(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
+                      int32_t num_layers, const double *arrival_s, double budget_bytes_per_s,
+                      double margin_bytes_per_s, double epoch_s, double *rates_out, double *admit_s_out) {
+    oc::clear_error();
+    if (n < 1 || !layer_bytes || !arrival_s || !rates_out || !admit_s_out)
+        return fail(OC_EINVAL, "need n >= 1 requests and non-NULL arrays");
+    if (num_layers < 1) return fail(OC_EINVAL, "num_layers must be >= 1");
+    if (!(epoch_s >= 0.0) || !std::isfinite(epoch_s)) return fail(OC_EINVAL, "epoch_s must be >= 0 and finite");
+    for (int i = 0; i < n; ++i)
+        if (!(arrival_s[i] >= 0.0) || !std::isfinite(arrival_s[i]))
+            return fail(OC_EINVAL, "arrival_s must be >= 0 and finite");
+    // the per-call checks of oc_bandwidth_allocate, on all requests at once
+    {
+        std::vector<double> probe(n);
+        const int rc = oc_bandwidth_allocate(policy, n, layer_bytes, layer_compute_s, budget_bytes_per_s,
+                                             margin_bytes_per_s, probe.data());
+        if (rc) return rc;
+    }
+    const double B = budget_bytes_per_s;
+    const double tiny = 1e-9 * B;                 // a budget residue admits nobody
+    std::vector<char> admitted(n, 0);
+    std::vector<double> finish(n, 0.0);
+    int left = n;
+    double t = 0.0;
+    for (bool first = true; left > 0; first = false) {
+        if (!first) {
+            // the next event after t: an arrival or the end of a delivery
+            double nx = INFINITY;
+            for (int i = 0; i < n; ++i) {
+                if (!admitted[i] && arrival_s[i] > t) nx = std::min(nx, arrival_s[i]);
+                if (admitted[i] && finish[i] > t) nx = std::min(nx, finish[i]);
+            }
+            if (!std::isfinite(nx)) return fail(OC_EINVAL, "epoch schedule: requests wait with nothing in flight");
+            t = nx;
+        }
+        if (epoch_s > 0.0) {      // the first boundary at or after the event
+            double bnd = std::ceil(t / epoch_s) * epoch_s;
+            if (bnd < t) bnd += epoch_s;
+            t = bnd;
+        }
+        double held = 0.0;
+        std::vector<int32_t> waiting;
+        for (int i = 0; i < n; ++i) {
+            if (admitted[i] && finish[i] > t) held += rates_out[i];
+            if (!admitted[i] && arrival_s[i] <= t) waiting.push_back(i);
+        }
+        const double free_bw = B - held;
+        if (waiting.empty() || free_bw <= tiny) continue;
+        const int m = (int)waiting.size();
+        std::vector<double> s(m), c(m), r(m);
+        for (int k = 0; k < m; ++k) {
+            s[k] = layer_bytes[waiting[k]];
+            c[k] = layer_compute_s ? layer_compute_s[waiting[k]] : 0.0;
+        }
+        const int rc = oc_bandwidth_allocate(policy, m, s.data(), layer_compute_s ? c.data() : nullptr, free_bw,
+                                             margin_bytes_per_s, r.data());
+        if (rc) return rc;
+        for (int k = 0; k < m; ++k) {
+            const int i = waiting[k];
+            admitted[i] = 1;
+            rates_out[i] = r[k];
+            admit_s_out[i] = t;
+            finish[i] = t + num_layers * layer_bytes[i] / r[k];
+            --left;
+        }
+    }
+    return OC_OK;
+}

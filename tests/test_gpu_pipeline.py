@@ -329,3 +329,56 @@ def test_layerwise_ingest_chunk_sizes(G, chunks, d):
         out = _outs(rs)[0]
         for l in range(rs.L):
             assert_attention_close(out[l], rs.expected_out(0, l), f"{name} G={G} layer {l}")
+
+
+@pytest.mark.timeout(120)
+def test_scheduling_epochs_admit_late_requests_with_released_bandwidth():
+    # Section 3.6's epoch rule on the GPU pipeline: two requests share the
+    # budget from the start; a third arrives mid-run and is admitted at the
+    # first epoch boundary after the short request has finished, with the
+    # rate that request released -- the long request's rate never changes.
+    # Each request's TTFT (from its arrival) follows eq. (3) at its own rate
+    # from its admission; the pool and every output match the oracle.
+    import paper_2605_22850_amd as oc
+    from oracle import model
+    print("[pipeline] scheduling epochs", flush=True)
+    L, nq, nkv, d = 4, 8, 2, 64
+    pre, suf = [2048, 8192, 4096], [24, 24, 24]
+    rs = RequestSet(L, nq, nkv, d, pre, suf, 1024, seed=19).upload(with_payload=True)
+    arrival = [0.0, 0.0, 0.02]
+    for req, a in zip(rs.reqs, arrival):
+        req.arrival_s = a
+    B, epoch = 100e6, 0.05
+    s = [tp * 2 * nkv * d * 2 for tp in pre]
+    want_r, want_t = model.epoch_schedule("equal", s, None, L, arrival, B, epoch=epoch)
+    # hand-checked: 50 MB/s each; the short request ends at 4 MiB / 50 MB/s =
+    # 84 ms, so the late one is admitted at the 100 ms boundary
+    assert want_r == pytest.approx([50e6] * 3) and want_t == pytest.approx([0.0, 0.0, 0.1])
+    stats = _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=B, alloc_policy="equal", epoch_s=epoch, slots=6)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool()), "pool"
+    outs = _outs(rs)
+    for r in range(3):
+        for l in range(L):
+            assert_attention_close(outs[r][l], rs.expected_out(r, l), f"request {r} layer {l}")
+    for r, st in enumerate(stats):
+        assert st["rate_bytes_per_s"] == pytest.approx(want_r[r], rel=1e-12)
+        assert st["admitted_ms"] == pytest.approx(want_t[r] * 1e3, abs=1e-9)
+        # eq. (3) from the admission, with X = layer bytes / rate and C the
+        # measured compute window of each layer; TTFT counts from arrival
+        X = [s[r] / want_r[r] * 1e3] * L
+        C = [st["done_ms"][l] - max(st["ingested_ms"][l], st["done_ms"][l - 1] if l else 0.0) for l in range(L)]
+        model_ms = (want_t[r] - arrival[r]) * 1e3 + model.layerwise_ttft(X, C)
+        print(f"  request {r}: admitted {st['admitted_ms']:.1f} ms, ttft {st['ttft_ms']:.2f} ms "
+              f"(eq. (3) {model_ms:.2f} ms)", flush=True)
+        assert model_ms * 0.99 - 0.5 <= st["ttft_ms"] <= model_ms * 1.05 + 3.0, r
+        # no payload of the late request before its admission
+        assert min(st["produced_ms"]) >= want_t[r] * 1e3 + X[0] * 0.9
+
+
+def test_arrivals_need_an_allocation_policy():
+    import paper_2605_22850_amd as oc
+    rs = RequestSet(2, 4, 2, 64, [256, 256], [8, 8], 64, seed=20).upload(with_payload=True)
+    rs.reqs[1].arrival_s = 0.01
+    with pytest.raises(oc.OcError) as e:
+        _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=1e8)
+    assert "arrival_s" in str(e.value)

@@ -10,6 +10,7 @@ from itertools import groupby
 import numpy as np
 import pytest
 
+import paper_2605_22850_amd as oc
 from oracle import model
 from tests.conftest import golden_rows
 
@@ -159,3 +160,98 @@ def test_library_allocator_rejects_bad_input():
         oc.oc_bandwidth_allocate("no_such_policy", [1.0], [1.0], 1.0, 0.0)
     out = (ctypes.c_double * 1)()
     assert oc.lib().oc_bandwidth_allocate(0, 0, None, None, 1.0, 0.0, out) == L.OC_EINVAL
+
+
+# ---------------------------------------------------------------------------
+# scheduling epochs
+# ---------------------------------------------------------------------------
+
+def _epoch_cases():
+    cases = {}
+    for row in golden_rows("epoch_schedule.txt"):
+        if row[0] == "case":
+            cases[row[1]] = {"policy": row[2], "B": float(row[3]), "L": int(row[4]), "epoch": float(row[5]),
+                             "reqs": []}
+        else:
+            cases[row[1]]["reqs"].append([float(x) for x in row[2:7]])
+    return cases
+
+
+@pytest.mark.parametrize("name", ["periodic", "event", "kvprop", "leftover"])
+def test_epoch_schedule_hand_worked_cases(name):
+    cs = _epoch_cases()[name]
+    s, c, a, want_r, want_t = (list(col) for col in zip(*cs["reqs"]))
+    rates, admit = model.epoch_schedule(cs["policy"], s, c, cs["L"], a, cs["B"], epoch=cs["epoch"])
+    assert rates == pytest.approx(want_r, rel=1e-12) and admit == pytest.approx(want_t, abs=1e-12)
+    rates, admit = oc.oc_epoch_schedule(cs["policy"], s, c, cs["L"], a, cs["B"], epoch_s=cs["epoch"])
+    assert rates == pytest.approx(want_r, rel=1e-12) and admit == pytest.approx(want_t, abs=1e-12)
+
+
+def _check_epoch_rule(policy, s, c, L, a, B, epoch, rates, admit):
+    """The rule, checked on a finished schedule: admissions at or after
+    arrival and on a boundary; at every boundary the rates of the requests
+    still loading fit the budget; a request waits past a boundary only if
+    nobody was admitted there and no budget was free."""
+    n = len(s)
+    end = [admit[i] + L * s[i] / rates[i] for i in range(n)]
+    assert all(rates[i] > 0 and admit[i] >= a[i] - 1e-12 for i in range(n))
+    if epoch > 0:
+        assert all(abs(t / epoch - round(t / epoch)) < 1e-9 for t in admit)
+    for t in set(admit):
+        loading = sum(rates[j] for j in range(n) if admit[j] <= t + 1e-12 and end[j] > t + 1e-12)
+        assert loading <= B * (1 + 1e-9)
+    # boundaries a request waited through
+    events = sorted(set(a) | set(end) | set(admit))
+    bounds = set()
+    for e in events:
+        bounds.add(e if epoch == 0 else math.ceil(e / epoch - 1e-12) * epoch)
+    for i in range(n):
+        for b in bounds:
+            if a[i] <= b < admit[i] - 1e-12:
+                assert not any(abs(admit[j] - b) < 1e-12 for j in range(n)), (i, b)
+                held = sum(rates[j] for j in range(n) if admit[j] < b - 1e-12 and end[j] > b + 1e-12)
+                assert B - held <= 1e-9 * B * 10 + 1e-12, (i, b, B - held)
+
+
+@pytest.mark.parametrize("policy", ["equal", "kv_prop", "bw_prop", "stall_opt", "cal_stall_opt"])
+def test_epoch_schedule_library_matches_oracle_and_rule(policy):
+    rng = np.random.default_rng(11)
+    for trial in range(60):
+        n = int(rng.integers(1, 9))
+        L = int(rng.integers(1, 40))
+        s = list(rng.uniform(1e6, 5e8, n))
+        c = list(rng.uniform(1e-3, 0.2, n))
+        a = [0.0 if rng.random() < 0.3 else float(rng.uniform(0, 3.0)) for _ in range(n)]
+        B = float(rng.uniform(1e9, 2e10))
+        epoch = 0.0 if trial % 2 else float(rng.choice([0.01, 0.1, 0.5]))
+        delta = 0.625e9
+        r_o, t_o = model.epoch_schedule(policy, s, c, L, a, B, delta=delta, epoch=epoch)
+        r_l, t_l = oc.oc_epoch_schedule(policy, s, c, L, a, B, delta, epoch)
+        assert r_l == pytest.approx(r_o, rel=1e-9), (trial, r_l, r_o)
+        assert t_l == pytest.approx(t_o, abs=1e-9), (trial, t_l, t_o)
+        _check_epoch_rule(policy, s, c, L, a, B, epoch, r_l, t_l)
+
+
+def test_epoch_schedule_with_every_arrival_at_start_is_one_allocation():
+    rng = np.random.default_rng(12)
+    for policy in ("equal", "kv_prop", "bw_prop", "stall_opt", "cal_stall_opt"):
+        n = 6
+        s = list(rng.uniform(1e6, 5e8, n))
+        c = list(rng.uniform(1e-3, 0.2, n))
+        one = oc.oc_bandwidth_allocate(policy, s, c, 1e10, 0.625e9)
+        for epoch in (0.0, 0.25):
+            rates, admit = oc.oc_epoch_schedule(policy, s, c, 32, [0.0] * n, 1e10, 0.625e9, epoch)
+            assert rates == pytest.approx(one, rel=1e-12) and admit == [0.0] * n
+
+
+def test_epoch_schedule_rejects_bad_input():
+    with pytest.raises(oc.OcError):
+        oc.oc_epoch_schedule("equal", [1.0], None, 0, [0.0], 1.0)
+    with pytest.raises(oc.OcError):
+        oc.oc_epoch_schedule("equal", [1.0], None, 1, [-1.0], 1.0)
+    with pytest.raises(oc.OcError):
+        oc.oc_epoch_schedule("equal", [1.0], None, 1, [0.0], 1.0, 0.0, -0.5)
+    with pytest.raises(oc.OcError):
+        oc.oc_epoch_schedule("stall_opt", [1.0], None, 1, [0.0], 1.0)
+    with pytest.raises(oc.OcError):
+        oc.oc_epoch_schedule("fifo", [1.0], None, 1, [0.0], 1.0)

@@ -638,6 +638,45 @@ def canonical_cells(args):
     return out
 
 
+def cells_summary(path):
+    """Markdown of a `--canonical-cells` JSON line (the file holds the
+    script's stdout): per cell the four modes beside eq. (3) and the
+    chunkwise form, then the layerwise/chunkwise rate sweep with the overlap
+    requirement, then the 10-over-100 Gbps sensitivity."""
+    with open(path) as f:
+        d = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1])["canonical_cells"]
+    cap = d["cap_GBps"]
+    out = [f"Llama-3-8B shape, random weights, G = {d['chunk_tokens']}, FFN {d['ffn_dim']}, cap {cap} GB/s.", "",
+           "| C | hit | T_p / T_s | C_l (ms) | X_l (ms) | layer TFLOP/s | HBM | uncapped | capped LW | eq. (3) | "
+           "capped CW | CW model | LW added over HBM |", "|" + "---|" * 13]
+    name = {4096: "4K", 65536: "64K"}
+    for c in d["cells"]:
+        t = c["ttft_ms"]
+        out.append(f"| {name.get(c['context'], c['context'])} | {c['hit'] * 100:g} % | {c['prefix_tokens']} / "
+                   f"{c['suffix_tokens']} | {c['compute_ms_per_layer']} | {c['transfer_ms_per_layer_at_cap']} | "
+                   f"{c['layer_tflops']} | {t['hbm_resident']} | {t['producer_uncapped']} | {t['capped_layerwise']} | "
+                   f"{c['eq3_ms']} | {t['capped_chunkwise']} | {c['chunkwise_model_ms']} | "
+                   f"{c['added_over_hbm_pct']['capped_layerwise']} % |")
+    if any("rate_sweep" in c for c in d["cells"]):
+        out += ["", "Rate sweep (ms; one timed trial per rate after a discarded first; B_req = layer bytes / C_l, "
+                "the rate at which a layer's transfer equals its compute):", "",
+                "| C | hit | B_req (GB/s) | rate (GB/s) | layerwise | eq. (3) | LW / eq. (3) | chunkwise | CW model |",
+                "|" + "---|" * 9]
+        for c in d["cells"]:
+            for r in c.get("rate_sweep", []):
+                out.append(f"| {name.get(c['context'], c['context'])} | {c['hit'] * 100:g} % | {c['required_GBps']} | "
+                           f"{r['rate_GBps']} | {r['layerwise_ms']} | {r['eq3_ms']} | "
+                           f"{r['layerwise_ms'] / r['eq3_ms']:.3f} | {r['chunkwise_ms']} | {r['chunkwise_model_ms']} |")
+        out += ["", "Bandwidth sensitivity: TTFT at 1.25 GB/s (10 Gbps) over 12.5 GB/s (100 Gbps), minus one:", "",
+                "| C | hit | B_req (GB/s) | layerwise | chunkwise |", "|---|---|---|---|---|"]
+        for c in d["cells"]:
+            sens = c.get("bandwidth_sensitivity")
+            if sens:
+                out.append(f"| {name.get(c['context'], c['context'])} | {c['hit'] * 100:g} % | {c['required_GBps']} | "
+                           f"+{sens['layerwise_increase'] * 100:.1f} % | +{sens['chunkwise_increase'] * 100:.1f} % |")
+    return "\n".join(out)
+
+
 def cpu_model():
     """The host CPU's model name as lscpu reports it (else /proc/cpuinfo)."""
     import subprocess
@@ -1096,12 +1135,17 @@ def main():
                     help="one attention launch per request and layer, not one per layer for all requests")
     ap.add_argument("--zero-kv", action="store_true",
                     help="HBM-resident runs over an all-zero pool, then over the ingested N(0,1) pool")
+    ap.add_argument("--cells-summary", metavar="JSON",
+                    help="print a markdown summary of a saved --canonical-cells output line (no GPU needed)")
     ap.add_argument("--profile-summary", nargs="+", metavar="DB",
                     help="print a markdown summary of rocprofv3 databases of a run of this script")
     args = ap.parse_args()
 
     if args.profile_summary:
         print(profile_summary(args.profile_summary, args.workload, args.warmup, args.steps))
+        return
+    if args.cells_summary:
+        print(cells_summary(args.cells_summary))
         return
     if args.attention_per_request:
         RUN_OPTS["attention_per_request"] = True

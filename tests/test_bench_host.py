@@ -3,6 +3,7 @@ chunkwise floors it reports beside the measured TTFT (against the oracle's
 model), the attention FLOP count (against a brute-force count of the
 unmasked query-key pairs), and the arithmetic that turns rocprofv3 counter
 databases into the HBM-traffic figure (on a synthetic database)."""
+import json
 import os
 import sqlite3
 import subprocess
@@ -87,3 +88,27 @@ def test_cpu_baseline_reports_its_sample():
     a = r["attention"]
     assert a["rows"] == wl.suffix_tokens[0] and a["gflops"] > 0
     assert a["all_layers_s_extrapolated"] == pytest.approx(wl.num_layers * a["layer_s_extrapolated"], abs=0.1)
+
+
+def test_cells_summary_formats_sweep_and_sensitivity(tmp_path):
+    cell = {"context": 65536, "hit": 0.5, "prefix_tokens": 32768, "suffix_tokens": 32768,
+            "compute_ms_per_layer": 35.0, "transfer_ms_per_layer_at_cap": 10.7, "layer_tflops": 1100.0,
+            "ttft_ms": {"hbm_resident": 1130.0, "producer_uncapped": 1140.0, "capped_layerwise": 1150.0,
+                        "capped_chunkwise": 1480.0},
+            "eq3_ms": 1146.0, "chunkwise_model_ms": 1479.0, "added_over_hbm_pct": {"capped_layerwise": 1.77},
+            "required_GBps": 3.83,
+            "rate_sweep": [{"rate_GBps": 1.25, "layerwise_ms": 3470.0, "chunkwise_ms": 4580.0, "eq3_ms": 3468.0,
+                            "chunkwise_model_ms": 4570.0},
+                           {"rate_GBps": 12.5, "layerwise_ms": 1150.0, "chunkwise_ms": 1480.0, "eq3_ms": 1146.0,
+                            "chunkwise_model_ms": 1479.0}],
+            "bandwidth_sensitivity": bench.bandwidth_sensitivity(
+                [{"rate_GBps": 1.25, "layerwise_ms": [3470.0], "chunkwise_ms": [4580.0]},
+                 {"rate_GBps": 12.5, "layerwise_ms": [1150.0], "chunkwise_ms": [1480.0]}])}
+    p = tmp_path / "cells.json"
+    p.write_text("noise\n" + json.dumps({"canonical_cells": {"cap_GBps": 12.5, "chunk_tokens": 64, "ffn_dim": 14336,
+                                                             "cells": [cell]}}) + "\n")
+    text = bench.cells_summary(str(p))
+    assert "| 64K | 50 % | 32768 / 32768 | 35.0 | 10.7 |" in text
+    assert "| 64K | 50 % | 3.83 | 1.25 | 3470.0 | 3468.0 | 1.001 |" in text
+    # 3470 / 1150 - 1 and 4580 / 1480 - 1
+    assert "| 64K | 50 % | 3.83 | +201.7 % | +209.5 % |" in text

@@ -781,6 +781,65 @@ def zero_kv(args):
     return {"workload": wl.name, "trials": trials - 1, **out}
 
 
+def ingest_tables(args):
+    """The isolated ingest of the main workload with its own (seeded random)
+    block table and with the identity table (prefix page j in pool page j),
+    same payloads and launch shape, beside a plain device copy of the same
+    bytes: what the table's page placement costs the kernel.  `--tables`
+    picks the tables (one per counter run)."""
+    import torch
+    import kvgen
+    import paper_2605_22850_amd as oc
+    torch.cuda.set_device(0)
+    wl = kvgen.workload(args.workload)
+    layout, pool, reqs, _, _ = setup(wl)
+    L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
+    out = {"workload": wl.name, "tables": {}}
+    for name in args.tables.split(","):
+        if name == "identity":
+            for rq in reqs:
+                rq.pages = torch.arange(rq.pages.numel(), dtype=torch.int32, device="cuda")
+        elif name != "random":
+            raise SystemExit(f"unknown table {name}")
+        out["tables"][name] = isolated_ingest(oc, wl, layout, pool, reqs, args.isolated_passes)
+        log(f"[bench] ingest with the {name} table: {out['tables'][name]['value']} GB/s")
+    # plain copy of the same bytes per launch (payload layer -> a buffer), layers rotated
+    s = torch.cuda.Stream()
+    tp = wl.prefix_tokens[0]
+    dst = torch.empty(tp * b // 2, dtype=torch.int16, device="cuda")
+    launches = [(lambda l=l: dst.copy_(reqs[0].device_payload[l * tp * b // 2:(l + 1) * tp * b // 2]),
+                 2.0 * tp * b) for l in range(L)]
+    with torch.cuda.stream(s):
+        warm_device(s, lambda: [fn() for fn, _ in launches])
+        evs, _ = gated_passes(s, launches, args.isolated_passes)
+    out["plain_copy"] = _rate(evs, "device-to-device copy of each layer payload (torch copy_), same bytes")
+    return out
+
+
+def ingest_tables_summary(paths):
+    """Markdown of rocprofv3 counter databases of `--ingest-tables` runs, one
+    table per run: mean per ingest dispatch of every counter collected."""
+    import sqlite3
+    out = ["| run | dispatches | mean us | counter | mean per dispatch |", "|---|---|---|---|---|"]
+    for path in paths:
+        c = sqlite3.connect(path)
+        rows = list(c.execute("select dispatch_id,kernel_name,counter_name,value,start,end "
+                              "from counters_collection order by start"))
+        by_disp = {}
+        for disp, name, cn, val, st, en in rows:
+            if "kv_ingest" not in name:
+                continue
+            e = by_disp.setdefault(disp, {"dur": en - st, "c": {}})
+            e["c"][cn] = e["c"].get(cn, 0.0) + val
+        disp = list(by_disp.values())
+        label = os.path.basename(os.path.dirname(path)) or os.path.basename(path)
+        dur = np.mean([e["dur"] for e in disp]) / 1e3 if disp else float("nan")
+        for cn in sorted({k for e in disp for k in e["c"]}):
+            out.append(f"| {label} | {len(disp)} | {dur:.1f} | {cn} | "
+                       f"{np.mean([e['c'][cn] for e in disp if cn in e['c']]):.4g} |")
+    return "\n".join(out)
+
+
 def step_ingest(stats_all, wl):
     """In-step ingest of timed pipeline runs: algorithmic bytes (read + write
     of every layer payload) over the summed time between each layer's landed
@@ -1125,7 +1184,8 @@ def main():
                          "one timed trial each after a discarded first")
     ap.add_argument("--policy-margin", type=float, default=0.625e9,
                     help="Calibrated Stall-opt margin, bytes/s (0.625e9 = 5 Gbps)")
-    ap.add_argument("--other-workloads", default="8b-4k,batch8,70b-32k",
+    ap.add_argument("--other-workloads", "--second-workload", dest="other_workloads",
+                    default="8b-4k,batch8,70b-32k",
                     help="workloads whose steps, TTFT legs, attention and isolated ingest are reported beside "
                          "the main one, comma-separated ('' to skip)")
     ap.add_argument("--other-steps", type=int, default=5, help="timed device-staged steps of each other workload")
@@ -1135,6 +1195,10 @@ def main():
                     help="one attention launch per request and layer, not one per layer for all requests")
     ap.add_argument("--zero-kv", action="store_true",
                     help="HBM-resident runs over an all-zero pool, then over the ingested N(0,1) pool")
+    ap.add_argument("--tables", default="",
+                    help="isolated ingest of the workload with these block tables instead (random,identity)")
+    ap.add_argument("--ingest-tables-summary", nargs="+", metavar="DB",
+                    help="print a markdown summary of rocprofv3 counter databases of --tables runs")
     ap.add_argument("--cells-summary", metavar="JSON",
                     help="print a markdown summary of a saved --canonical-cells output line (no GPU needed)")
     ap.add_argument("--profile-summary", nargs="+", metavar="DB",
@@ -1147,6 +1211,9 @@ def main():
     if args.cells_summary:
         print(cells_summary(args.cells_summary))
         return
+    if args.ingest_tables_summary:
+        print(ingest_tables_summary(args.ingest_tables_summary))
+        return
     if args.attention_per_request:
         RUN_OPTS["attention_per_request"] = True
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -1158,6 +1225,10 @@ def main():
         print(json.dumps({"metric": "TTFT with the whole layer's compute, end-to-end cells", "unit": "ms",
                           "higher_is_better": False, "data": "synthetic: random weights and KV", "n_gpus": 1,
                           "canonical_cells": res}), flush=True)
+        return
+    if args.tables:
+        print(json.dumps({"metric": "isolated ingest by block table", "unit": "GB/s", "higher_is_better": True,
+                          "data": "synthetic", "n_gpus": 1, "ingest_tables": ingest_tables(args)}), flush=True)
         return
     if args.zero_kv:
         print(json.dumps({"metric": "attention per layer over zero vs N(0,1) K/V", "unit": "TFLOP/s",

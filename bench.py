@@ -1032,6 +1032,84 @@ def _short(name):
     return n.split("(")[0]
 
 
+def marker_summary(paths):
+    """Markdown summary of a rocprofv3 --marker-trace --kernel-trace database:
+    the library's roctx ranges (each pipeline run, each layer's enqueue) and
+    marks (each payload the producer completes), set against the kernels.
+    Per run: the host time of the run and of its layer enqueues; with a
+    producer, the gap between payload marks (the delivery interval) and the
+    lag from a mark to the start of the first ingest launch after it."""
+    import sqlite3
+
+    def message(extdata):
+        try:
+            return json.loads(extdata or "{}").get("message", "")
+        except ValueError:
+            return ""
+
+    out = []
+    for path in paths:
+        c = sqlite3.connect(path)
+        # ranges are regions, marks are samples; the roctx message is in extdata
+        regs = [(message(x), tid, st, en) for x, tid, st, en in
+                c.execute("select extdata,tid,start,end from regions order by start")]
+        marks = [(message(x), tid, ts) for x, tid, ts in
+                 c.execute("select extdata,tid,timestamp from samples order by timestamp")]
+        kern = list(c.execute("select name,start,end from kernels order by start"))
+        # host-to-device copies, when the trace has them (--memory-copy-trace)
+        copies = [(st, en, size) for st, en, size, kind in
+                  c.execute("select start,end,size,src_agent_type from memory_copies order by start")
+                  if kind == "CPU"]
+        out.append(f"### Markers: `{os.path.basename(path)}`\n")
+        kinds = {}
+        for msg, *_ in regs:
+            key = ("range", msg.split(" ")[0])
+            kinds[key] = kinds.get(key, 0) + 1
+        for msg, *_ in marks:
+            key = ("mark", msg.split(" ")[0])
+            kinds[key] = kinds.get(key, 0) + 1
+        out.append("| roctx | message starts | count |\n|---|---|---|")
+        for (kind, head), n in sorted(kinds.items()):
+            out.append(f"| {kind} | `{head}` | {n} |")
+        out.append("")
+        runs = [r for r in regs if r[0] == "oc_pipeline_run"]
+        ing = [st for name, st, en in kern if "kv_ingest" in name]
+        split = {}
+        out.append("| run | host ms | layer enqueues | mean enqueue us | payload marks | mean mark gap ms | "
+                   "mean mark -> ingest start us | max |\n|---|---|---|---|---|---|---|---|")
+        for i, (_, tid, st, en) in enumerate(runs):
+            lay = [r for r in regs if st <= r[2] <= en and r[1] == tid and r[0].startswith("layer ")]
+            ts = [m[2] for m in marks if st <= m[2] <= en and m[0].startswith("ready ")]
+            row = f"| {i} | {(en - st) / 1e6:.2f} | {len(lay)} | "
+            row += f"{np.mean([r[3] - r[2] for r in lay]) / 1e3:.1f} | " if lay else "- | "
+            row += f"{len(ts)} | "
+            row += f"{np.mean(np.diff(ts)) / 1e6:.3f} | " if len(ts) >= 2 else "- | "
+            lags = []
+            for m in ts:
+                nxt = next((k for k in ing if k >= m), None)
+                if nxt is not None and nxt <= en:
+                    lags.append(nxt - m)
+            row += f"{np.mean(lags) / 1e3:.1f} | {max(lags) / 1e3:.1f} |" if lags else "- | - |"
+            out.append(row)
+            # the lag split: mark -> copy start, the copy itself, copy end -> ingest start
+            for m in ts:
+                cp = next((x for x in copies if x[0] >= m), None)
+                nxt = next((k for k in ing if cp is not None and k >= cp[1]), None)
+                if cp is not None and nxt is not None and nxt <= en:
+                    split.setdefault(i, []).append((cp[0] - m, cp[1] - cp[0], cp[2], nxt - cp[1]))
+        out.append("")
+        if split:
+            out.append("| run | marks | mark -> DMA start us | DMA us | DMA MiB | DMA GB/s | DMA end -> ingest "
+                       "start us |\n|---|---|---|---|---|---|---|")
+            for i, v in sorted(split.items()):
+                a = np.array(v, dtype=float)
+                out.append(f"| {i} | {len(v)} | {a[:, 0].mean() / 1e3:.1f} | {a[:, 1].mean() / 1e3:.1f} | "
+                           f"{a[:, 2].mean() / 2**20:.1f} | {a[:, 2].sum() / a[:, 1].sum():.1f} | "
+                           f"{a[:, 3].mean() / 1e3:.1f} |")
+            out.append("")
+    return "\n".join(out)
+
+
 def profile_summary(paths, workload, warmup, steps):
     import sqlite3
     import kvgen
@@ -1201,10 +1279,15 @@ def main():
                     help="print a markdown summary of rocprofv3 counter databases of --tables runs")
     ap.add_argument("--cells-summary", metavar="JSON",
                     help="print a markdown summary of a saved --canonical-cells output line (no GPU needed)")
+    ap.add_argument("--marker-summary", nargs="+", metavar="DB",
+                    help="print a markdown summary of the roctx ranges and marks in rocprofv3 databases")
     ap.add_argument("--profile-summary", nargs="+", metavar="DB",
                     help="print a markdown summary of rocprofv3 databases of a run of this script")
     args = ap.parse_args()
 
+    if args.marker_summary:
+        print(marker_summary(args.marker_summary))
+        return
     if args.profile_summary:
         print(profile_summary(args.profile_summary, args.workload, args.warmup, args.steps))
         return

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define OC_ABI_VERSION 5
+#define OC_ABI_VERSION 6
 
 typedef enum {
     OC_OK = 0,
@@ -48,7 +48,8 @@ typedef enum {
     OC_EHIP = -5,      /* the HIP runtime reported an error                */
     OC_ETIMEOUT = -6,  /* a layer did not arrive within the timeout        */
     OC_ENOMEM = -7,    /* host/pinned/device allocation failed (contexts)  */
-    OC_EABORT = -8     /* the producer stopped before delivering a layer   */
+    OC_EABORT = -8,    /* the producer stopped before delivering a layer   */
+    OC_ESHORT = -9     /* a delivered payload is shorter than the layer    */
 } oc_status;
 
 /* Model and paging layout (Section 2.1, eq. (1); Table "ObjectCache request
@@ -320,7 +321,9 @@ typedef enum {
 typedef enum {
     OC_FAULT_NONE = 0,
     OC_FAULT_STALL = 1,        /* producer stops delivering at fault_layer (tests timeouts) */
-    OC_FAULT_ABORT = 2         /* producer gives up at fault_layer (tests error paths)      */
+    OC_FAULT_ABORT = 2,        /* producer gives up at fault_layer (tests error paths)      */
+    OC_FAULT_SHORT_WRITE = 3   /* producer's payload for fault_layer ends half a chunk slice
+                                  early (a torn object read); tests the length check        */
 } oc_fault;
 
 /* Delivery of a request's cached prefix (eq. (2), Section 3.4).  The
@@ -428,6 +431,15 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
 /* Run the pipeline over n_reqs requests for all L layers; synchronous.
  * stats (optional) has n_reqs entries.  On OC_ETIMEOUT / OC_EABORT the run is
  * stopped, all enqueued GPU work is drained and the context stays usable.
+ * Before a delivered payload is landed, the byte count the producer reports
+ * for it is checked against the layer's size (prefix_tokens * 2 * n_kv * d *
+ * 2, or the chunk group's objects): a short payload is never copied to HBM
+ * or ingested; the run stops with OC_ESHORT, drained, the context usable.
+ * Layers landed before it stay ingested in the pool.  With the library built
+ * against roctx, each run and each layer's enqueue on the driver thread is a
+ * named range ("oc_pipeline_run", "layer <l> req <r>"), and the producer
+ * marks each payload it completes ("ready layer <l> req <r>"), so a
+ * rocprofv3 --marker-trace timeline shows delivery against the kernels.
  * The run's GPU work starts after all work enqueued so far on the device's
  * null (legacy default) stream; work on other streams that writes the pool,
  * tables or tensors of reqs must be complete before the call. */

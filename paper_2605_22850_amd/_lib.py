@@ -17,10 +17,10 @@ from typing import Optional, Sequence
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libobjectcache.so")
 
-OC_OK, OC_EINVAL, OC_ESHAPE, OC_EALIGN, OC_ERANGE, OC_EHIP, OC_ETIMEOUT, OC_ENOMEM, OC_EABORT = \
-    0, -1, -2, -3, -4, -5, -6, -7, -8
+OC_OK, OC_EINVAL, OC_ESHAPE, OC_EALIGN, OC_ERANGE, OC_EHIP, OC_ETIMEOUT, OC_ENOMEM, OC_EABORT, OC_ESHORT = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8, -9
 OC_MODE_HBM_RESIDENT, OC_MODE_DEVICE_STAGED, OC_MODE_PRODUCER = 0, 1, 2
-OC_FAULT_NONE, OC_FAULT_STALL, OC_FAULT_ABORT = 0, 1, 2
+OC_FAULT_NONE, OC_FAULT_STALL, OC_FAULT_ABORT, OC_FAULT_SHORT_WRITE = 0, 1, 2, 3
 ALLOC_POLICIES = {"fifo": 0, "equal": 1, "kv_prop": 2, "bw_prop": 3, "stall_opt": 4, "cal_stall_opt": 5}
 DELIVERIES = {"layerwise": 0, "chunkwise": 1, "auto": 2}
 

@@ -24,6 +24,8 @@
 #include <thread>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "common.hpp"
 
 namespace oc {
@@ -55,6 +57,15 @@ struct Context {
     double last_ms = 0.0;
 };
 
+// A roctx range for a scope of the calling thread (a no-op without a tool
+// attached): the run and each layer's enqueue show on a rocprofv3 timeline.
+struct TraceRange {
+    explicit TraceRange(const std::string &name) { roctxRangePushA(name.c_str()); }
+    ~TraceRange() { roctxRangePop(); }
+    TraceRange(const TraceRange &) = delete;
+    TraceRange &operator=(const TraceRange &) = delete;
+};
+
 // ---- shared state between the driver and the producer ----------------------
 struct RunShared {
     std::mutex mu;
@@ -65,7 +76,21 @@ struct RunShared {
     int producer_status = OC_OK;  // producer -> driver
     std::string producer_msg;
     std::deque<int64_t> reported; // rate producer -> driver: items complete in a pinned slot
+    std::vector<int64_t> delivered; // per item: bytes the producer put in its pinned slot,
+                                    // set before the item is published as ready or reported
 };
+
+// The injected short write: the copy of item `it`'s last chunk stops half
+// way, as a torn read of an object would.  Returns the bytes to copy of a
+// unit that is the `j`-th of [.., last).
+static inline int64_t copy_len(const oc_pipeline_opts &o, int32_t layer, int64_t j, int64_t last, int64_t unit) {
+    return o.fault == OC_FAULT_SHORT_WRITE && layer == o.fault_layer && j == last - 1 ? unit / 2 : unit;
+}
+
+// Stall and abort stop delivery at fault_layer; a short write still delivers.
+static inline bool stops_at(const oc_pipeline_opts &o, int32_t layer) {
+    return (o.fault == OC_FAULT_STALL || o.fault == OC_FAULT_ABORT) && layer == o.fault_layer;
+}
 
 // A unit of delivery: one layer payload of a request (layerwise), or a
 // group of whole chunk objects j0..j1-1 of a request (chunkwise, layer 0 for
@@ -86,6 +111,7 @@ static int fill_defaults(oc_pipeline_opts &o) {
     if (o.producer_threads > 64) return fail(OC_EINVAL, "producer_threads must be <= 64");
     if (o.mode < OC_MODE_HBM_RESIDENT || o.mode > OC_MODE_PRODUCER) return fail(OC_EINVAL, "unknown mode");
     if (o.rate_bytes_per_s < 0) return fail(OC_EINVAL, "negative rate");
+    if (o.fault < OC_FAULT_NONE || o.fault > OC_FAULT_SHORT_WRITE) return fail(OC_EINVAL, "unknown fault");
     if (o.alloc_policy < OC_ALLOC_FIFO || o.alloc_policy > OC_ALLOC_CAL_STALL_OPT)
         return fail(OC_EINVAL, "unknown allocation policy");
     if (o.alloc_policy != OC_ALLOC_FIFO && !(o.rate_bytes_per_s > 0))
@@ -156,6 +182,7 @@ struct Producer {
     std::mutex wmu;
     std::condition_variable wcv;
     int64_t cur_item = -1, next_piece = 0, n_pieces = 0, pieces_done = 0, chunks_per_piece = 1;
+    int64_t bytes_done = 0;             // bytes the current item's pieces copied
     double cum_before = 0.0;            // bytes delivered before the current item
     bool stop = false;
 
@@ -207,13 +234,17 @@ struct Producer {
                 }
             }
             unsigned char *dst = static_cast<unsigned char *>(c->slots[item % c->slots.size()].pinned);
+            int64_t copied = 0;
             for (int64_t j = j0; j < j1 && !skip; ++j) {
                 const unsigned char *obj = static_cast<const unsigned char *>(r.chunk_objects[j]);
-                std::memcpy(dst + (j - first) * unit, obj + src_off, (size_t)unit);
+                const int64_t len = copy_len(c->opts, it.layer, j, last, unit);
+                std::memcpy(dst + (j - first) * unit, obj + src_off, (size_t)len);
+                copied += len;
             }
             {
                 std::lock_guard<std::mutex> g(wmu);
                 ++pieces_done;
+                bytes_done += copied;
             }
             wcv.notify_all();
         }
@@ -238,7 +269,7 @@ struct Producer {
         const int64_t nslots = (int64_t)c->slots.size();
         for (int64_t k = 0; k < n_items; ++k) {
             const Item it = (*items)[k];
-            if (c->opts.fault != OC_FAULT_NONE && it.layer == c->opts.fault_layer) {
+            if (stops_at(c->opts, it.layer)) {
                 if (c->opts.fault == OC_FAULT_ABORT) {
                     set_error(OC_EABORT, "producer aborted (injected fault)");
                     break;
@@ -270,19 +301,24 @@ struct Producer {
                 n_pieces = (N + chunks_per_piece - 1) / chunks_per_piece;
                 next_piece = 0;
                 pieces_done = 0;
+                bytes_done = 0;
                 cum_before = cum;
                 cur_item = k;
             }
             wcv.notify_all();
+            int64_t delivered;
             {
                 std::unique_lock<std::mutex> lk(wmu);
                 wcv.wait(lk, [&] { return pieces_done == n_pieces; });
                 cur_item = -1;
+                delivered = bytes_done;
             }
             cum += (double)N * unit;
             (*produced_ms)[k] = std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
+            roctxMarkA(("ready layer " + std::to_string(it.layer) + " req " + std::to_string(it.req)).c_str());
             {
                 std::lock_guard<std::mutex> g(sh->mu);
+                sh->delivered[k] = delivered;
                 sh->ready = k + 1;
             }
             sh->cv.notify_all();
@@ -335,6 +371,7 @@ struct RateProducer {
     std::priority_queue<Piece, std::vector<Piece>, Later> heap;
     bool stop = false;
     std::vector<int64_t> pieces_left;        // per item
+    std::vector<int64_t> bytes_of;           // per item: bytes its pieces copied
     std::vector<char> complete;              // per item
     std::vector<int32_t> next_report;        // per request: the layer to report next
     std::vector<int> slot_of;                // per item; written before the item is reported
@@ -367,6 +404,8 @@ struct RateProducer {
         while (next_report[r] < L && complete[item_of(next_report[r], r)]) {
             const int64_t k = item_of(next_report[r], r);
             (*produced_ms)[k] = std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
+            roctxMarkA(("ready layer " + std::to_string(next_report[r]) + " req " + std::to_string(r)).c_str());
+            sh->delivered[k] = bytes_of[k];
             sh->reported.push_back(k);
             ++next_report[r];
         }
@@ -406,12 +445,17 @@ struct RateProducer {
                 }
             }
             const int32_t layer = (int32_t)(pc.item / n_reqs), r = (int32_t)(pc.item % n_reqs);
+            const int64_t N = reqs[r].prefix_tokens / c->pool.layout.chunk_tokens;
             unsigned char *dst = static_cast<unsigned char *>(c->slots[pc.slot].pinned);
+            int64_t copied = 0;
             for (int64_t j = pc.j0; j < pc.j1; ++j) {
                 const unsigned char *obj = static_cast<const unsigned char *>(reqs[r].chunk_objects[j]);
-                std::memcpy(dst + j * S, obj + (int64_t)layer * S, (size_t)S);
+                const int64_t len = copy_len(c->opts, layer, j, N, S);
+                std::memcpy(dst + j * S, obj + (int64_t)layer * S, (size_t)len);
+                copied += len;
             }
             std::lock_guard<std::mutex> g(wmu);
+            bytes_of[pc.item] += copied;
             if (--pieces_left[pc.item] == 0) {
                 complete[pc.item] = 1;
                 report_ready(r);
@@ -424,6 +468,7 @@ struct RateProducer {
         const int64_t n_items = (int64_t)n_reqs * L;
         const int64_t cpp = std::max<int64_t>(1, c->opts.piece_bytes / S);     // chunks per piece
         pieces_left.assign(n_items, 0);
+        bytes_of.assign(n_items, 0);
         complete.assign(n_items, 0);
         next_report.assign(n_reqs, 0);
         slot_of.assign(n_items, -1);
@@ -467,7 +512,7 @@ struct RateProducer {
             for (int32_t r = 0; r < n_reqs; ++r) {
                 if (layer[r] >= L) continue;
                 all_done = false;
-                if (c->opts.fault != OC_FAULT_NONE && layer[r] == c->opts.fault_layer && piece[r] == 0) {
+                if (stops_at(c->opts, layer[r]) && piece[r] == 0) {
                     if (c->opts.fault == OC_FAULT_ABORT) {
                         set_error(OC_EABORT, "producer aborted (injected fault)");
                     } else {      // injected stall: deliver nothing more until the driver gives up
@@ -580,6 +625,7 @@ static double ev_ms(hipEvent_t a, hipEvent_t b) {
 
 static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
     const DeviceScope on_device(c->device);
+    const TraceRange trace_run("oc_pipeline_run");
     const oc_layout &l = c->pool.layout;
     const int32_t L = l.num_layers;
     const int mode = c->opts.mode;
@@ -807,6 +853,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     }
 
     RunShared sh;
+    sh.delivered.assign(n_items, 0);
     Producer prod{};
     RateProducer rprod{};
     std::thread producer_thread;
@@ -846,8 +893,17 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
 
     int status = OC_OK;
     std::string msg;
+    // a payload shorter than its item is never landed: the run stops there
+    auto short_payload = [&](const Item &it, int64_t got, int64_t want) {
+        const std::string what = it.chunks ? "chunks " + std::to_string(it.j0) + ".." + std::to_string(it.j1 - 1)
+                                           : "layer " + std::to_string(it.layer);
+        status = OC_ESHORT;
+        msg = what + " of request " + std::to_string(it.req) + ": the producer delivered " + std::to_string(got) +
+              " of " + std::to_string(want) + " bytes";
+    };
     for (int64_t step = 0; step < n_items && status == OC_OK; ++step) {
         int64_t k = step;
+        int64_t got = 0;   // bytes the producer reports for item k
         if (by_rate) {     // the next layer any request has ready, in the order they became ready
             std::unique_lock<std::mutex> lk(sh.mu);
             const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
@@ -864,8 +920,12 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             }
             k = sh.reported.front();
             sh.reported.pop_front();
+            got = sh.delivered[k];
         }
         const Item it = items[k];
+        const TraceRange trace_item(it.chunks ? "chunks " + std::to_string(it.j0) + ".." + std::to_string(it.j1 - 1) +
+                                                    " req " + std::to_string(it.req)
+                                              : "layer " + std::to_string(it.layer) + " req " + std::to_string(it.req));
         const oc_request &r = reqs[it.req];
         const int64_t layer_bytes = r.prefix_tokens * b_tok;
         const int64_t N = r.prefix_tokens / l.chunk_tokens;
@@ -889,6 +949,11 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                           " ms";
                     break;
                 }
+                got = sh.delivered[k];
+            }
+            if (got != (it.j1 - it.j0) * obj_bytes) {
+                short_payload(it, got, (it.j1 - it.j0) * obj_bytes);
+                break;
             }
             Slot &s = c->slots[k % c->slots.size()];
             hipError_t e = hipMemcpyAsync(s.device, s.pinned, (size_t)((it.j1 - it.j0) * obj_bytes),
@@ -920,6 +985,10 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
             continue;
         }
         if (by_rate) {
+            if (got != layer_bytes) {
+                short_payload(it, got, layer_bytes);
+                break;
+            }
             if (layer_bytes > 0) {
                 const int slot = rprod.slot_of[k];
                 Slot &s = c->slots[slot];
@@ -959,7 +1028,12 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                       " did not arrive within " + std::to_string(c->opts.timeout_ms) + " ms";
                 break;
             }
+            got = sh.delivered[k];
             lk.unlock();
+            if (got != layer_bytes) {
+                short_payload(it, got, layer_bytes);
+                break;
+            }
             Slot &s = c->slots[k % c->slots.size()];
             hipError_t e = layer_bytes ? hipMemcpyAsync(s.device, s.pinned, (size_t)layer_bytes,
                                                         hipMemcpyHostToDevice, c->copy)

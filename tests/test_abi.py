@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert oc.oc_abi_version() == 5
+    assert oc.oc_abi_version() == 6
 
 
 def _layout(**kw):

@@ -2,7 +2,7 @@
 (pool bit-exact, attention in tolerance) and the modes agree bit for bit;
 slot recycling under a racing producer; several requests sharing a pool and
 a rate; pacing and timestamps; injected producer stalls and aborts end in an
-error, never a hang."""
+error, never a hang; a short payload is caught before it is landed."""
 import time
 
 import numpy as np
@@ -238,6 +238,54 @@ def test_injected_abort_reports_error():
     with pytest.raises(oc.OcError) as e:
         _run(rs, oc.OC_MODE_PRODUCER, fault=oc.OC_FAULT_ABORT, fault_layer=2)
     assert e.value.status == oc._lib.OC_EABORT
+
+
+def _short_write_rejected(rs, **kw):
+    import paper_2605_22850_amd as oc
+    with pytest.raises(oc.OcError) as e:
+        _run(rs, oc.OC_MODE_PRODUCER, fault=oc.OC_FAULT_SHORT_WRITE, **kw)
+    assert e.value.status == oc._lib.OC_ESHORT
+    assert "the producer delivered" in str(e.value)
+    return str(e.value)
+
+
+def test_injected_short_write_is_never_landed():
+    # layer 1's payload of request 0 ends half a chunk slice early: the run
+    # stops before landing it, so layer 0 of every request is in the pool and
+    # no later layer was touched; the context's next run is whole
+    import paper_2605_22850_amd as oc
+    print("[pipeline] short write, layerwise", flush=True)
+    rs = RequestSet(4, 8, 2, 128, [256, 160], [8, 5], 64, seed=7).upload()
+    S = 2 * rs.G * 2 * 128 * 2
+    msg = _short_write_rejected(rs, fault_layer=1, piece_bytes=3 * S)
+    assert f"layer 1 of request 0: the producer delivered {16 * S - S // 2} of {16 * S} bytes" in msg
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool(layers=[0]))
+    _run(rs, oc.OC_MODE_PRODUCER)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
+
+
+def test_injected_short_write_chunkwise_and_paced():
+    import paper_2605_22850_amd as oc
+    print("[pipeline] short write, chunkwise", flush=True)
+    rs = RequestSet(3, 8, 2, 128, [256, 96], [8, 4], 48, seed=8).upload()
+    msg = _short_write_rejected(rs, fault_layer=0, delivery="chunkwise")
+    assert "chunks 0.." in msg and "of request 0" in msg
+    # chunk groups come first and the first one is torn: nothing was landed
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool(layers=[]))
+    print("[pipeline] short write, paced by policy", flush=True)
+    total = sum(tp * 2 * 2 * 128 * 2 for tp in rs.prefix) * rs.L
+    _short_write_rejected(rs, fault_layer=2, alloc_policy="equal", rate_bytes_per_s=total / 0.03,
+                          piece_bytes=16384)
+    _run(rs, oc.OC_MODE_PRODUCER, alloc_policy="equal", rate_bytes_per_s=total / 0.03, piece_bytes=16384)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
+
+
+def test_unknown_fault_rejected():
+    import paper_2605_22850_amd as oc
+    rs = RequestSet(2, 8, 2, 128, [64], [4], 8, seed=9).upload()
+    with pytest.raises(oc.OcError) as e:
+        rs.context(oc.OC_MODE_PRODUCER, fault=4)
+    assert e.value.status == oc._lib.OC_EINVAL
 
 
 def test_bad_request_rejected_before_running():

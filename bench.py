@@ -678,18 +678,26 @@ def cells_summary(path):
 
 
 def cpu_model():
-    """The host CPU's model name as lscpu reports it (else /proc/cpuinfo)."""
+    """The host CPU as lscpu reports it: the model name, then the family,
+    model and stepping numbers and the CPU count (a virtual machine may show
+    only a generic model name); else /proc/cpuinfo's model name."""
     import subprocess
     try:
         out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        f = {}
         for ln in out.splitlines():
-            if ln.strip().startswith("Model name:"):
-                return ln.split(":", 1)[1].strip()
+            if ":" in ln:
+                k, v = ln.split(":", 1)
+                f.setdefault(k.strip(), v.strip())
+        if f.get("Model name"):
+            ids = ", ".join(f"{k.lower()} {f[k]}" for k in ("CPU family", "Model", "Stepping") if f.get(k))
+            extra = "; ".join(x for x in (ids, f"{f['CPU(s)']} CPUs" if f.get("CPU(s)") else "") if x)
+            return f"{f['Model name']} ({extra})" if extra else f["Model name"]
     except (OSError, subprocess.SubprocessError):
         pass
     try:
-        with open("/proc/cpuinfo") as f:
-            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "unknown")
+        with open("/proc/cpuinfo") as fh:
+            return next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "unknown")
     except OSError:
         return "unknown"
 
@@ -1073,40 +1081,40 @@ def marker_summary(paths):
             out.append(f"| {kind} | `{head}` | {n} |")
         out.append("")
         runs = [r for r in regs if r[0] == "oc_pipeline_run"]
-        ing = [st for name, st, en in kern if "kv_ingest" in name]
-        split = {}
-        out.append("| run | host ms | layer enqueues | mean enqueue us | payload marks | mean mark gap ms | "
-                   "mean mark -> ingest start us | max |\n|---|---|---|---|---|---|---|---|")
+        out.append("| run | host ms | layer ranges | mean layer range us | payload marks | mean mark gap ms | "
+                   "DMA spans per layer | DMA GB/s | mark -> last span landed us | last span -> ingest start us | "
+                   "mark -> ingest start us (max) |\n|---|---|---|---|---|---|---|---|---|---|---|")
         for i, (_, tid, st, en) in enumerate(runs):
             lay = [r for r in regs if st <= r[2] <= en and r[1] == tid and r[0].startswith("layer ")]
             ts = [m[2] for m in marks if st <= m[2] <= en and m[0].startswith("ready ")]
+            cps = [x for x in copies if st <= x[0] <= en]
+            ing = [k[1] for k in kern if st <= k[1] <= en and "kv_ingest" in k[0]]
             row = f"| {i} | {(en - st) / 1e6:.2f} | {len(lay)} | "
             row += f"{np.mean([r[3] - r[2] for r in lay]) / 1e3:.1f} | " if lay else "- | "
             row += f"{len(ts)} | "
             row += f"{np.mean(np.diff(ts)) / 1e6:.3f} | " if len(ts) >= 2 else "- | "
-            lags = []
-            for m in ts:
-                nxt = next((k for k in ing if k >= m), None)
-                if nxt is not None and nxt <= en:
-                    lags.append(nxt - m)
-            row += f"{np.mean(lags) / 1e3:.1f} | {max(lags) / 1e3:.1f} |" if lags else "- | - |"
+            # one request delivered in layer order: the i-th payload mark and
+            # the i-th ingest launch are one layer's, and the copy stream runs
+            # that layer's DMA spans between the previous ingest and its own
+            if ts and cps and len(ts) == len(ing):
+                spans, land, to_ing, lag, prev = [], [], [], [], -1
+                for m, k0 in zip(ts, ing):
+                    mine = [x for x in cps if prev < x[1] <= k0]
+                    prev = k0
+                    if not mine:
+                        continue
+                    spans.append(len(mine))
+                    land.append(mine[-1][1] - m)
+                    to_ing.append(k0 - mine[-1][1])
+                    lag.append(k0 - m)
+                nb = float(sum(x[2] for x in cps))
+                dma = float(sum(x[1] - x[0] for x in cps))
+                row += (f"{np.mean(spans):.1f} | {nb / dma:.1f} | {np.mean(land) / 1e3:.1f} | "
+                        f"{np.mean(to_ing) / 1e3:.1f} | {np.mean(lag) / 1e3:.1f} ({np.max(lag) / 1e3:.1f}) |")
+            else:
+                row += "- | - | - | - | - |"
             out.append(row)
-            # the lag split: mark -> copy start, the copy itself, copy end -> ingest start
-            for m in ts:
-                cp = next((x for x in copies if x[0] >= m), None)
-                nxt = next((k for k in ing if cp is not None and k >= cp[1]), None)
-                if cp is not None and nxt is not None and nxt <= en:
-                    split.setdefault(i, []).append((cp[0] - m, cp[1] - cp[0], cp[2], nxt - cp[1]))
         out.append("")
-        if split:
-            out.append("| run | marks | mark -> DMA start us | DMA us | DMA MiB | DMA GB/s | DMA end -> ingest "
-                       "start us |\n|---|---|---|---|---|---|---|")
-            for i, v in sorted(split.items()):
-                a = np.array(v, dtype=float)
-                out.append(f"| {i} | {len(v)} | {a[:, 0].mean() / 1e3:.1f} | {a[:, 1].mean() / 1e3:.1f} | "
-                           f"{a[:, 2].mean() / 2**20:.1f} | {a[:, 2].sum() / a[:, 1].sum():.1f} | "
-                           f"{a[:, 3].mean() / 1e3:.1f} |")
-            out.append("")
     return "\n".join(out)
 
 

@@ -431,11 +431,14 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
 /* Run the pipeline over n_reqs requests for all L layers; synchronous.
  * stats (optional) has n_reqs entries.  On OC_ETIMEOUT / OC_EABORT the run is
  * stopped, all enqueued GPU work is drained and the context stays usable.
- * Before a delivered payload is landed, the byte count the producer reports
- * for it is checked against the layer's size (prefix_tokens * 2 * n_kv * d *
- * 2, or the chunk group's objects): a short payload is never copied to HBM
- * or ingested; the run stops with OC_ESHORT, drained, the context usable.
- * Layers landed before it stay ingested in the pool.  With the library built
+ * Once the producer completes a payload, the byte count it reports is
+ * checked against the layer's size (prefix_tokens * 2 * n_kv * d * 2, or the
+ * chunk group's objects): a short payload is never ingested (its leading
+ * pieces may have been copied to the HBM staging slot); the run stops with
+ * OC_ESHORT, drained, the context usable.  Layers ingested before it stay in
+ * the pool.  With OC_ALLOC_FIFO and a rate cap, a layer payload is copied to
+ * HBM in spans (an eighth of the layer, at least 8 MiB) as its leading bytes
+ * complete; the ingest waits for the whole layer.  With the library built
  * against roctx, each run and each layer's enqueue on the driver thread is a
  * named range ("oc_pipeline_run", "layer <l> req <r>"), and the producer
  * marks each payload it completes ("ready layer <l> req <r>"), so a

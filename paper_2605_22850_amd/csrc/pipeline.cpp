@@ -3,7 +3,9 @@
 // pseudocode): for each layer, in prefix order, the producer copies that
 // layer's slice of every matched chunk object into a pinned slot, paced to a
 // byte rate, and then signals layer-ready.  The driver thread lands the slot
-// in HBM with an asynchronous DMA on the copy stream and ingests it there;
+// in HBM with asynchronous DMAs on the copy stream -- from a paced in-order
+// producer, span by span as the leading bytes of the slot complete, so the
+// copy overlaps the production -- and, once the whole layer is in, ingests it;
 // the compute stream waits on the layer's ingested event and runs that
 // layer's attention.  So layer l+1 lands and is ingested while layer l
 // computes, and every hand-off is a HIP event, never a device-wide sync.
@@ -78,6 +80,10 @@ struct RunShared {
     std::deque<int64_t> reported; // rate producer -> driver: items complete in a pinned slot
     std::vector<int64_t> delivered; // per item: bytes the producer put in its pinned slot,
                                     // set before the item is published as ready or reported
+    // producer -> driver, layerwise items of the in-order producer: the
+    // leading bytes of item part_item's slot that are complete (whole
+    // pieces, in slot order); never decreases for an item
+    int64_t part_item = -1, part_bytes = 0;
 };
 
 // The injected short write: the copy of item `it`'s last chunk stops half
@@ -85,6 +91,18 @@ struct RunShared {
 // unit that is the `j`-th of [.., last).
 static inline int64_t copy_len(const oc_pipeline_opts &o, int32_t layer, int64_t j, int64_t last, int64_t unit) {
     return o.fault == OC_FAULT_SHORT_WRITE && layer == o.fault_layer && j == last - 1 ? unit / 2 : unit;
+}
+
+// A layer payload of the in-order, rate-capped producer lands in HBM in spans
+// of about this many bytes as its leading pieces complete: an eighth of the
+// layer, at least 8 MiB and a piece.  Each copy costs the driver thread about
+// 50 us, which must stay well below a span's time on the host link (8 MiB:
+// about 150 us).  The producer wakes the driver only when a span boundary is
+// passed.  Uncapped, the producer outruns the host link and each layer's DMA
+// already overlaps the next layer's production: the layer lands whole.
+static inline int64_t landing_span(const oc_pipeline_opts &o, int64_t layer_bytes) {
+    if (!(o.rate_bytes_per_s > 0)) return std::max<int64_t>(layer_bytes, 1);
+    return std::max<int64_t>({o.piece_bytes, layer_bytes / 8, (int64_t)8 << 20});
 }
 
 // Stall and abort stop delivery at fault_layer; a short write still delivers.
@@ -183,6 +201,8 @@ struct Producer {
     std::condition_variable wcv;
     int64_t cur_item = -1, next_piece = 0, n_pieces = 0, pieces_done = 0, chunks_per_piece = 1;
     int64_t bytes_done = 0;             // bytes the current item's pieces copied
+    std::vector<char> piece_done;       // per piece of the current item
+    int64_t prefix_pieces = 0;          // leading pieces of the current item that are done
     double cum_before = 0.0;            // bytes delivered before the current item
     bool stop = false;
 
@@ -241,12 +261,32 @@ struct Producer {
                 std::memcpy(dst + (j - first) * unit, obj + src_off, (size_t)len);
                 copied += len;
             }
+            int64_t prefix = -1;      // complete leading bytes of a layer payload's slot
             {
                 std::lock_guard<std::mutex> g(wmu);
                 ++pieces_done;
                 bytes_done += copied;
+                if (!skip) {
+                    piece_done[p] = 1;
+                    while (prefix_pieces < n_pieces && piece_done[prefix_pieces]) ++prefix_pieces;
+                    if (!it.chunks) prefix = std::min(prefix_pieces * cpp, last - first) * unit;
+                }
             }
             wcv.notify_all();
+            if (prefix >= 0) {
+                const int64_t span = landing_span(c->opts, (last - first) * unit);
+                bool wake = false;
+                {
+                    std::lock_guard<std::mutex> g(sh->mu);
+                    if (item > sh->part_item || (item == sh->part_item && prefix > sh->part_bytes)) {
+                        const int64_t before = item == sh->part_item ? sh->part_bytes : 0;
+                        wake = prefix / span > before / span;
+                        sh->part_item = item;
+                        sh->part_bytes = prefix;
+                    }
+                }
+                if (wake) sh->cv.notify_all();
+            }
         }
     }
 
@@ -302,6 +342,8 @@ struct Producer {
                 next_piece = 0;
                 pieces_done = 0;
                 bytes_done = 0;
+                piece_done.assign(n_pieces, 0);
+                prefix_pieces = 0;
                 cum_before = cum;
                 cur_item = k;
             }
@@ -1014,30 +1056,51 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
                 }
             }
         } else if (mode == OC_MODE_PRODUCER) {
-            std::unique_lock<std::mutex> lk(sh.mu);
-            const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
-            const bool ok = sh.cv.wait_until(lk, deadline, [&] { return sh.ready > k || sh.producer_status != OC_OK; });
-            if (sh.producer_status != OC_OK) {
-                status = sh.producer_status;
-                msg = sh.producer_msg;
-                break;
-            }
-            if (!ok) {
-                status = OC_ETIMEOUT;
-                msg = "layer " + std::to_string(it.layer) + " of request " + std::to_string(it.req) +
-                      " did not arrive within " + std::to_string(c->opts.timeout_ms) + " ms";
-                break;
-            }
-            got = sh.delivered[k];
-            lk.unlock();
-            if (got != layer_bytes) {
-                short_payload(it, got, layer_bytes);
-                break;
-            }
+            // land the payload in spans as the producer completes its leading
+            // bytes, so the copy of a layer overlaps its production; the
+            // ingest still waits for the whole layer
             Slot &s = c->slots[k % c->slots.size()];
-            hipError_t e = layer_bytes ? hipMemcpyAsync(s.device, s.pinned, (size_t)layer_bytes,
-                                                        hipMemcpyHostToDevice, c->copy)
-                                       : hipSuccess;
+            const int64_t span = landing_span(c->opts, layer_bytes);
+            const unsigned char *src = static_cast<const unsigned char *>(s.pinned);
+            unsigned char *dst = static_cast<unsigned char *>(s.device);
+            const auto deadline = Clock::now() + std::chrono::milliseconds(c->opts.timeout_ms);
+            int64_t sent = 0;
+            bool whole = false;
+            hipError_t e = hipSuccess;
+            while (!whole && e == hipSuccess) {
+                int64_t avail;
+                {
+                    std::unique_lock<std::mutex> lk(sh.mu);
+                    const bool ok = sh.cv.wait_until(lk, deadline, [&] {
+                        return sh.ready > k ||
+                               (sh.part_item == k && sh.part_bytes >= std::min(layer_bytes, (sent / span + 1) * span)) ||
+                               sh.producer_status != OC_OK;
+                    });
+                    if (sh.producer_status != OC_OK) {
+                        status = sh.producer_status;
+                        msg = sh.producer_msg;
+                        break;
+                    }
+                    if (!ok) {
+                        status = OC_ETIMEOUT;
+                        msg = "layer " + std::to_string(it.layer) + " of request " + std::to_string(it.req) +
+                              " did not arrive within " + std::to_string(c->opts.timeout_ms) + " ms";
+                        break;
+                    }
+                    whole = sh.ready > k;
+                    got = sh.delivered[k];
+                    avail = whole ? layer_bytes : sh.part_bytes;
+                }
+                if (whole && got != layer_bytes) {
+                    short_payload(it, got, layer_bytes);     // landed in part, never ingested
+                    break;
+                }
+                if (avail > sent) {
+                    e = hipMemcpyAsync(dst + sent, src + sent, (size_t)(avail - sent), hipMemcpyHostToDevice, c->copy);
+                    sent = avail;
+                }
+            }
+            if (status != OC_OK) break;
             if (e == hipSuccess) e = hipEventRecord(landed[k], c->copy);
             {
                 std::lock_guard<std::mutex> g(sh.mu);

@@ -112,3 +112,36 @@ def test_cells_summary_formats_sweep_and_sensitivity(tmp_path):
     assert "| 64K | 50 % | 3.83 | 1.25 | 3470.0 | 3468.0 | 1.001 |" in text
     # 3470 / 1150 - 1 and 4580 / 1480 - 1
     assert "| 64K | 50 % | 3.83 | +201.7 % | +209.5 % |" in text
+
+
+def test_marker_summary_splits_each_layers_delivery(tmp_path):
+    # one run, two layers: marks at 1000 and 3000 ns; layer 0 lands in two
+    # spans (ending 1500 and 2000) and is ingested at 2100, layer 1 in one
+    # span (ending 3500), ingested at 3600
+    db = tmp_path / "m.db"
+    c = sqlite3.connect(db)
+    c.execute("create table regions (extdata text, tid int, start int, end int)")
+    c.execute("create table samples (extdata text, tid int, timestamp int)")
+    c.execute("create table kernels (name text, start int, end int)")
+    c.execute("create table memory_copies (start int, end int, size int, src_agent_type text)")
+    msg = lambda m: json.dumps({"message": m})  # noqa: E731
+    c.executemany("insert into regions values (?,?,?,?)",
+                  [(msg("oc_pipeline_run"), 7, 0, 100000), (msg("layer 0 req 0"), 7, 10, 2050),
+                   (msg("layer 1 req 0"), 7, 2060, 3550), (msg("layer 0 req 0"), 8, 20, 30)])
+    c.executemany("insert into samples values (?,?,?)", [(msg("ready layer 0 req 0"), 9, 1000),
+                                                         (msg("ready layer 1 req 0"), 9, 3000)])
+    c.executemany("insert into kernels values (?,?,?)",
+                  [("oc::kv_ingest_src_kernel<true>", 2100, 2200), ("oc::attn_fwd_kernel<128>", 2200, 2900),
+                   ("oc::kv_ingest_rows_kernel", 3600, 3700)])
+    c.executemany("insert into memory_copies values (?,?,?,?)",
+                  [(1000, 1500, 1000, "CPU"), (1500, 2000, 1000, "CPU"), (3000, 3500, 1000, "CPU"),
+                   (50000, 50100, 99, "GPU")])
+    c.commit()
+    c.close()
+    out = bench.marker_summary([str(db)])
+    assert "| range | `layer` | 3 |" in out and "| mark | `ready` | 2 |" in out
+    row = next(ln for ln in out.splitlines() if ln.startswith("| 0 |"))
+    cells = [x.strip() for x in row.strip("|").split("|")]
+    # run, host ms, layer ranges (driver thread only), mean range us, marks, mark gap ms,
+    # spans per layer, DMA GB/s, mark -> last span, last span -> ingest, mark -> ingest (max)
+    assert cells == ["0", "0.10", "2", "1.8", "2", "0.002", "1.5", "2.0", "0.8", "0.1", "0.8 (1.1)"]

@@ -280,6 +280,28 @@ def test_injected_short_write_chunkwise_and_paced():
     assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
 
 
+def test_layer_lands_in_spans_while_produced():
+    # 25 MiB layers land in 8 MiB spans as the paced producer's leading
+    # pieces complete (3 threads finish pieces out of order; the last piece
+    # is ragged); every layer must reach the pool whole, and a short layer
+    # whose first spans were already landed must still never be ingested
+    import paper_2605_22850_amd as oc
+    print("[pipeline] spans: 25 MiB layers, 256 KiB pieces", flush=True)
+    rs = RequestSet(3, 8, 8, 128, [6160], [12], 512, seed=10).upload()
+    kw = dict(rate_bytes_per_s=1.0e9, piece_bytes=256 << 10, producer_threads=3)
+    _run(rs, oc.OC_MODE_PRODUCER, **kw)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
+    out = _outs(rs)[0]
+    for l in range(rs.L):
+        assert_attention_close(out[l], rs.expected_out(0, l), f"layer {l}")
+    rs.d_pool.fill_(np.int16(np.uint16(SENTINEL).view(np.int16)))
+    layer = 6160 * 2 * 8 * 128 * 2
+    S = 2 * 16 * 8 * 128 * 2
+    msg = _short_write_rejected(rs, fault_layer=1, **kw)
+    assert f"layer 1 of request 0: the producer delivered {layer - S // 2} of {layer} bytes" in msg
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool(layers=[0]))
+
+
 def test_unknown_fault_rejected():
     import paper_2605_22850_amd as oc
     rs = RequestSet(2, 8, 2, 128, [64], [4], 8, seed=9).upload()

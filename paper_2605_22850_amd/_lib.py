@@ -15,7 +15,9 @@ from dataclasses import dataclass
 from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libobjectcache.so")
+# OC_LIBRARY names another build of the same library (the sanitizer build of
+# its host code, say); by default the in-tree one
+LIB_PATH = os.environ.get("OC_LIBRARY") or os.path.join(_HERE, "libobjectcache.so")
 
 OC_OK, OC_EINVAL, OC_ESHAPE, OC_EALIGN, OC_ERANGE, OC_EHIP, OC_ETIMEOUT, OC_ENOMEM, OC_EABORT, OC_ESHORT = \
     0, -1, -2, -3, -4, -5, -6, -7, -8, -9

@@ -147,7 +147,7 @@ struct DeviceScope {
     int prev = -1;
     explicit DeviceScope(int dev) {
         if (hipGetDevice(&prev) != hipSuccess) prev = -1;
-        hipSetDevice(dev);
+        (void)hipSetDevice(dev);
     }
     ~DeviceScope() {
         if (prev >= 0) hipSetDevice(prev);

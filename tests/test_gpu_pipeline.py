@@ -302,6 +302,46 @@ def test_layer_lands_in_spans_while_produced():
     assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool(layers=[0]))
 
 
+def test_two_contexts_run_from_two_threads_at_once():
+    # the library from two host threads at the same time, each with its own
+    # context and pool: a paced producer (three runs) and device-staged
+    # delivery (twenty runs); both pools and every layer's output must come
+    # out as when each runs alone
+    import threading
+    import paper_2605_22850_amd as oc
+    print("[pipeline] two contexts, two threads", flush=True)
+    a = RequestSet(4, 8, 2, 128, [512, 96], [16, 7], 96, seed=11).upload()
+    b = RequestSet(3, 16, 4, 64, [320], [33], 64, seed=12).upload(with_payload=True)
+    layer_bytes_a = (512 + 96) * 2 * 2 * 128 * 2
+    ctx_a = a.context(oc.OC_MODE_PRODUCER, rate_bytes_per_s=layer_bytes_a * 4 / 0.05, piece_bytes=16384)
+    ctx_b = b.context(oc.OC_MODE_DEVICE_STAGED)
+    errors = []
+
+    def run(ctx, rs, reps):
+        try:
+            for _ in range(reps):
+                oc.oc_pipeline_run(ctx, rs.reqs, rs.L)
+        except Exception as e:          # reported below, from the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=run, args=(ctx_a, a, 3)), threading.Thread(target=run, args=(ctx_b, b, 20))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=60)
+    # a context still in use by a live thread is left alone, not destroyed
+    assert not any(t.is_alive() for t in threads), "a pipeline run did not return"
+    oc.oc_context_destroy(ctx_a)
+    oc.oc_context_destroy(ctx_b)
+    assert not errors, errors
+    for rs in (a, b):
+        assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
+        for r in range(len(rs.reqs)):
+            out = from_dev(rs.reqs[r].out)
+            for l in range(rs.L):
+                assert_attention_close(out[l], rs.expected_out(r, l), f"request {r} layer {l}")
+
+
 def test_unknown_fault_rejected():
     import paper_2605_22850_amd as oc
     rs = RequestSet(2, 8, 2, 128, [64], [4], 8, seed=9).upload()

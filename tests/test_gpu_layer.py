@@ -210,3 +210,46 @@ def test_pool_beyond_two_billion_elements():
 def oracle_pool_shape(P, nkv, Ps, d):
     import oracle
     return oracle.pool_shape(1, P, nkv, Ps, d)
+
+
+def _random_cases(n, seed):
+    # seeded shapes across the supported space: GQA groups 1-8 (odd ones
+    # too), head_dim 64 / 128, chunk sizes that divide a page, fill it or
+    # straddle pages, empty and ragged prefixes, suffixes of 1-299 tokens
+    # (several row tiles and a ragged last one), pools with or without free
+    # pages, any layer of 1-3; kept to sizes the oracle computes in well
+    # under a second
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        nkv = int(rng.choice([1, 2, 4, 8]))
+        grp = int(rng.choice([1, 2, 3, 4, 5, 8]))
+        nq, d = nkv * grp, int(rng.choice([64, 128]))
+        G = int(rng.choice([8, 16, 24, 32, 64]))
+        n_chunks = 0 if rng.random() < 0.1 else int(rng.integers(1, 4096 // G + 1))
+        Ts = int(rng.integers(1, 300))
+        if 4 * nq * d * Ts * (n_chunks * G + Ts) > 3e9:
+            continue
+        need = -(-n_chunks * G // 16)
+        P = max(1, need + (0 if rng.random() < 0.2 else int(rng.integers(1, 2 * need + 4))))
+        L = int(rng.integers(1, 4))
+        cases.append((nq, nkv, d, G, 16, n_chunks, Ts, P, L, int(rng.integers(0, L))))
+    return cases
+
+
+RANDOM_CASES = _random_cases(40, 2605)
+
+
+@pytest.mark.parametrize("i", range(len(RANDOM_CASES)))
+def test_random_shapes_ingest_and_attention(i):
+    # whole pool bit-exact after the ingest, every output row in tolerance
+    import torch
+    nq, nkv, d, G, Ps, n, Ts, P, L, layer = RANDOM_CASES[i]
+    print(f"[random {i}] nq {nq} nkv {nkv} d {d} G {G} chunks {n} Ts {Ts} P {P} L {L} layer {layer}", flush=True)
+    c = LayerCase(nq, nkv, d, G, Ps, n, Ts, P, L, layer, seed=100 + i).upload()
+    if n:
+        c.run_ingest()
+    out = c.run_attention()
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(c.d_pool).reshape(c.pool_shape()), c.expected_pool())
+    assert_attention_close(from_dev(out), c.expected_attention(), f"random {i}")

@@ -492,3 +492,59 @@ def test_arrivals_need_an_allocation_policy():
     with pytest.raises(oc.OcError) as e:
         _run(rs, oc.OC_MODE_PRODUCER, rate_bytes_per_s=1e8)
     assert "arrival_s" in str(e.value)
+
+
+def _random_pipeline_cases(n, seed):
+    # seeded pipelines: 1-5 requests (some with no cached prefix) sharing a
+    # pool, GQA groups 1-8, d 64/128, chunks of 8-64 tokens, 2-4 layers;
+    # device-staged, or the producer with 2-4 slots, 1-4 threads, pieces
+    # that do or do not divide into chunk slices, layerwise / chunkwise /
+    # eq. (2) delivery, FIFO or an allocation policy, capped or not; one
+    # launch per layer or per request
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        nkv, grp = int(rng.choice([1, 2, 4, 8])), int(rng.choice([1, 2, 4, 5, 8]))
+        d, G, L = int(rng.choice([64, 128])), int(rng.choice([8, 16, 32, 64])), int(rng.integers(2, 5))
+        nr = int(rng.integers(1, 6))
+        prefix = [0 if rng.random() < 0.15 else G * int(rng.integers(1, 1024 // G + 1)) for _ in range(nr)]
+        suffix = [int(rng.integers(1, 80)) for _ in range(nr)]
+        if sum(4 * nkv * grp * d * ts * (tp + ts) for tp, ts in zip(prefix, suffix)) * L > 2e9:
+            continue
+        need = sum(-(-tp // 16) for tp in prefix)
+        P = need + int(rng.integers(1, need + 8))
+        b = 2 * nkv * d * 2
+        kw = {"attention_per_request": bool(rng.random() < 0.3)}
+        if rng.random() < 0.3:
+            mode = "staged"
+        else:
+            mode = "producer"
+            kw.update(slots=int(rng.integers(2, 5)), producer_threads=int(rng.integers(1, 5)),
+                      piece_bytes=int(2 * G * b * int(rng.integers(1, 5)) + (0 if rng.random() < 0.5 else 1000)))
+            delivery = str(rng.choice(["layerwise", "layerwise", "chunkwise", "auto"]))
+            policy = str(rng.choice(["fifo", "equal", "kv_prop"])) if delivery == "layerwise" else "fifo"
+            total = max(1, sum(prefix) * b * L)
+            rate = 0.0 if policy == "fifo" and rng.random() < 0.4 else total / float(rng.uniform(0.01, 0.04))
+            kw.update(delivery=delivery, alloc_policy=policy, rate_bytes_per_s=rate)
+            if delivery == "auto":
+                kw["theta_bytes"] = float(rng.choice(prefix)) * b * L + 1.0
+        cases.append((L, nkv * grp, nkv, d, prefix, suffix, P, G, mode, kw))
+    return cases
+
+
+RANDOM_PIPELINES = _random_pipeline_cases(16, 2605)
+
+
+@pytest.mark.parametrize("i", range(len(RANDOM_PIPELINES)))
+def test_random_pipelines_match_oracle(i):
+    import paper_2605_22850_amd as oc
+    L, nq, nkv, d, prefix, suffix, P, G, mode, kw = RANDOM_PIPELINES[i]
+    print(f"[pipeline random {i}] L {L} nq {nq} nkv {nkv} d {d} G {G} prefix {prefix} suffix {suffix} P {P} "
+          f"{mode} {kw}", flush=True)
+    rs = RequestSet(L, nq, nkv, d, prefix, suffix, P, seed=200 + i, G=G).upload(with_payload=mode == "staged")
+    _run(rs, oc.OC_MODE_DEVICE_STAGED if mode == "staged" else oc.OC_MODE_PRODUCER, **kw)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
+    for r in range(len(prefix)):
+        out = from_dev(rs.reqs[r].out)
+        for l in range(L):
+            assert_attention_close(out[l], rs.expected_out(r, l), f"request {r} layer {l}")

@@ -494,13 +494,14 @@ def test_arrivals_need_an_allocation_policy():
     assert "arrival_s" in str(e.value)
 
 
-def _random_pipeline_cases(n, seed):
+def _random_pipeline_cases(n, seed, scheduled=False):
     # seeded pipelines: 1-5 requests (some with no cached prefix) sharing a
     # pool, GQA groups 1-8, d 64/128, chunks of 8-64 tokens, 2-4 layers;
     # device-staged, or the producer with 2-4 slots, 1-4 threads, pieces
     # that do or do not divide into chunk slices, layerwise / chunkwise /
-    # eq. (2) delivery, FIFO or an allocation policy, capped or not; one
-    # launch per layer or per request
+    # eq. (2) delivery, FIFO or an allocation policy (with arrivals during the
+    # run and scheduling epochs), capped or not; one launch per layer or per
+    # request
     rng = np.random.default_rng(seed)
     cases = []
     while len(cases) < n:
@@ -515,24 +516,31 @@ def _random_pipeline_cases(n, seed):
         P = need + int(rng.integers(1, need + 8))
         b = 2 * nkv * d * 2
         kw = {"attention_per_request": bool(rng.random() < 0.3)}
-        if rng.random() < 0.3:
+        if scheduled and nr < 2:
+            continue
+        if rng.random() < 0.3 and not scheduled:
             mode = "staged"
         else:
             mode = "producer"
             kw.update(slots=int(rng.integers(2, 5)), producer_threads=int(rng.integers(1, 5)),
                       piece_bytes=int(2 * G * b * int(rng.integers(1, 5)) + (0 if rng.random() < 0.5 else 1000)))
-            delivery = str(rng.choice(["layerwise", "layerwise", "chunkwise", "auto"]))
-            policy = str(rng.choice(["fifo", "equal", "kv_prop"])) if delivery == "layerwise" else "fifo"
+            delivery = "layerwise" if scheduled else str(rng.choice(["layerwise", "layerwise", "chunkwise", "auto"]))
+            policy = (str(rng.choice(["equal", "kv_prop"])) if scheduled else
+                      str(rng.choice(["fifo", "equal", "kv_prop"])) if delivery == "layerwise" else "fifo")
             total = max(1, sum(prefix) * b * L)
             rate = 0.0 if policy == "fifo" and rng.random() < 0.4 else total / float(rng.uniform(0.01, 0.04))
             kw.update(delivery=delivery, alloc_policy=policy, rate_bytes_per_s=rate)
             if delivery == "auto":
                 kw["theta_bytes"] = float(rng.choice(prefix)) * b * L + 1.0
+            if scheduled:
+                # requests arriving during the run, admitted by scheduling epochs
+                kw["epoch_s"] = float(rng.choice([0.0, 0.004]))
+                kw["arrivals"] = [0.0] + [float(rng.uniform(0.0, 0.02)) for _ in range(nr - 1)]
         cases.append((L, nkv * grp, nkv, d, prefix, suffix, P, G, mode, kw))
     return cases
 
 
-RANDOM_PIPELINES = _random_pipeline_cases(16, 2605)
+RANDOM_PIPELINES = _random_pipeline_cases(16, 2605) + _random_pipeline_cases(8, 2606, scheduled=True)
 
 
 @pytest.mark.parametrize("i", range(len(RANDOM_PIPELINES)))
@@ -542,6 +550,9 @@ def test_random_pipelines_match_oracle(i):
     print(f"[pipeline random {i}] L {L} nq {nq} nkv {nkv} d {d} G {G} prefix {prefix} suffix {suffix} P {P} "
           f"{mode} {kw}", flush=True)
     rs = RequestSet(L, nq, nkv, d, prefix, suffix, P, seed=200 + i, G=G).upload(with_payload=mode == "staged")
+    kw = dict(kw)
+    for req, a in zip(rs.reqs, kw.pop("arrivals", [])):
+        req.arrival_s = a
     _run(rs, oc.OC_MODE_DEVICE_STAGED if mode == "staged" else oc.OC_MODE_PRODUCER, **kw)
     assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
     for r in range(len(prefix)):

@@ -935,7 +935,7 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
 
     int status = OC_OK;
     std::string msg;
-    // a payload shorter than its item is never landed: the run stops there
+    // a payload shorter than its item is never ingested: the run stops there
     auto short_payload = [&](const Item &it, int64_t got, int64_t want) {
         const std::string what = it.chunks ? "chunks " + std::to_string(it.j0) + ".." + std::to_string(it.j1 - 1)
                                            : "layer " + std::to_string(it.layer);

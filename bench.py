@@ -845,7 +845,21 @@ def ingest_tables_summary(paths):
         for cn in sorted({k for e in disp for k in e["c"]}):
             out.append(f"| {label} | {len(disp)} | {dur:.1f} | {cn} | "
                        f"{np.mean([e['c'][cn] for e in disp if cn in e['c']]):.4g} |")
+        # average latencies (cycles) where a pass holds both the summed
+        # in-flight level (or latency) and the request count (Little's law)
+        for what, lev, cnt in LATENCY_PAIRS:
+            pairs = [e["c"][lev] / e["c"][cnt] for e in disp if e["c"].get(cnt, 0) > 0 and lev in e["c"]]
+            if pairs:
+                out.append(f"| {label} | {len(disp)} | {dur:.1f} | {what} (= {lev} / {cnt}) | {np.mean(pairs):.4g} |")
     return "\n".join(out)
+
+
+LATENCY_PAIRS = [
+    ("memory-side read latency", "TCC_EA0_RDREQ_LEVEL_sum", "TCC_EA0_RDREQ_sum"),
+    ("memory-side write latency", "TCC_EA0_WRREQ_LEVEL_sum", "TCC_EA0_WRREQ_sum"),
+    ("L1 -> L2 read latency", "TCP_TCC_READ_REQ_LATENCY_sum", "TCP_TCC_READ_REQ_sum"),
+    ("L1 -> L2 write latency", "TCP_TCC_WRITE_REQ_LATENCY_sum", "TCP_TCC_WRITE_REQ_sum"),
+]
 
 
 def step_ingest(stats_all, wl):

@@ -73,10 +73,13 @@ struct KParams {
 };
 
 // One launch serves up to MAX_ATTN_BATCH requests of one layer: workgroup w
-// belongs to the last request whose first workgroup it has reached.
+// belongs to the last request whose first workgroup it has reached (and a
+// block of the split merge, likewise, to the last whose first block it has
+// reached; a request without splits has none).
 struct KBatch {
     int32_t n;
     int32_t first_wg[MAX_ATTN_BATCH];
+    int32_t first_cb[MAX_ATTN_BATCH];
     KParams req[MAX_ATTN_BATCH];
 };
 
@@ -568,39 +571,63 @@ template <int D>
 constexpr size_t attn_lds_bytes() { return (size_t)4 * 2 * KB * D * 2; }
 
 // Merge the splits of each row: weights 2^(m_s - M), normalised by the
-// matching sum of l_s; bf16 out.
+// matching sum of l_s; bf16 out.  Block `blk` of a request's merge covers
+// RPB of its (KV head, row) pairs.
 template <int D>
-__global__ __launch_bounds__(256) void attn_combine_kernel(KParams p) {
+__device__ __forceinline__ void combine_block(const float *ml_part, const float *o_part, uint16_t *out, int nkv,
+                                              int64_t rows, int64_t rows_pad, int n_split, int grp, int nq,
+                                              int64_t blk) {
     constexpr int TPR = D / 4;                 // threads per row, 4 floats each
     constexpr int RPB = 256 / TPR;             // rows per block
-    const int64_t gr = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;   // over nkv * rows
+    const int64_t gr = blk * RPB + threadIdx.x / TPR;   // over nkv * rows
     const int c4 = threadIdx.x % TPR;
-    if (gr >= (int64_t)p.nkv * p.rows) return;
-    const int g = (int)(gr / p.rows);
-    const int64_t row = gr - (int64_t)g * p.rows;
+    if (gr >= (int64_t)nkv * rows) return;
+    const int g = (int)(gr / rows);
+    const int64_t row = gr - (int64_t)g * rows;
     // the splits' partials are independent loads: unrolled, their latencies
     // overlap instead of adding up split after split
-    const int64_t split_stride = (int64_t)p.nkv * p.rows_pad;
-    const int64_t prow0 = (int64_t)g * p.rows_pad + row;
+    const int64_t split_stride = (int64_t)nkv * rows_pad;
+    const int64_t prow0 = (int64_t)g * rows_pad + row;
     float M = -__builtin_inff();
 #pragma unroll 8
-    for (int s = 0; s < p.n_split; ++s) M = fmaxf(M, p.ml_part[(prow0 + s * split_stride) * 2]);
+    for (int s = 0; s < n_split; ++s) M = fmaxf(M, ml_part[(prow0 + s * split_stride) * 2]);
     const float Mu = M == -__builtin_inff() ? 0.f : M;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float L = 0.f;
 #pragma unroll 4
-    for (int s = 0; s < p.n_split; ++s) {
+    for (int s = 0; s < n_split; ++s) {
         const int64_t prow = prow0 + s * split_stride;
-        const float2 ml = *reinterpret_cast<const float2 *>(p.ml_part + prow * 2);
-        const f32x4 o = *reinterpret_cast<const f32x4 *>(p.o_part + prow * D + c4 * 4);
+        const float2 ml = *reinterpret_cast<const float2 *>(ml_part + prow * 2);
+        const f32x4 o = *reinterpret_cast<const f32x4 *>(o_part + prow * D + c4 * 4);
         const float w = __builtin_amdgcn_exp2f(ml.x - Mu);
         L += w * ml.y;
         acc += w * o;
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
-    const int64_t tok = row / p.grp;
-    const int head = g * p.grp + (int)(row % p.grp);
-    *reinterpret_cast<bf16x4 *>(p.out + (tok * p.nq + head) * D + c4 * 4) = __builtin_convertvector(acc * inv, bf16x4);
+    const int64_t tok = row / grp;
+    const int head = g * grp + (int)(row % grp);
+    *reinterpret_cast<bf16x4 *>(out + (tok * nq + head) * D + c4 * 4) = __builtin_convertvector(acc * inv, bf16x4);
+}
+
+// The merge of one request, with its parameters alone as the kernel
+// arguments (a lone request's launch stays short).
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(KParams p) {
+    combine_block<D>(p.ml_part, p.o_part, p.out, p.nkv, p.rows, p.rows_pad, p.n_split, p.grp, p.nq, blockIdx.x);
+}
+
+// The merges of every request of a batch that has splits, in one launch.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_batch_kernel(KBatch batch) {
+    // parameters straight from the kernel-argument segment, as in the
+    // attention kernel
+    typedef const __attribute__((address_space(4))) KBatch *kbatch_ptr;
+    const kbatch_ptr bp = (kbatch_ptr)__builtin_amdgcn_kernarg_segment_ptr();
+    int req = 0;
+    for (int i = 1; i < bp->n; ++i) req += (int)blockIdx.x >= bp->first_cb[i];
+    const __attribute__((address_space(4))) KParams &p = bp->req[req];
+    combine_block<D>(p.ml_part, p.o_part, p.out, p.nkv, p.rows, p.rows_pad, p.n_split, p.grp, p.nq,
+                     (int64_t)blockIdx.x - bp->first_cb[req]);
 }
 
 // ---------------------------------------------------------------------------
@@ -762,13 +789,25 @@ static hipError_t launch_d(const AttnPlan *pl, const AttnArgs *a, int n, hipStre
     });
     if (lds_status[dev] != hipSuccess) return lds_status[dev];
     if (grid > 0) hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3((unsigned)grid), dim3(THREADS), attn_lds_bytes<D>(), s, batch);
-    for (int k = 0; k < n; ++k)
-        if (batch.req[k].n_split > 1) {
-            constexpr int RPB = 256 / (D / 4);
-            const int64_t nrows = (int64_t)batch.req[k].nkv * batch.req[k].rows;
-            hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, s,
-                               batch.req[k]);
-        }
+    // the split merge of every request that has splits, in one launch
+    constexpr int RPB = 256 / (D / 4);
+    int64_t cblocks[MAX_ATTN_BATCH], ctotal = 0;
+    for (int k = 0; k < n; ++k) {
+        cblocks[k] = batch.req[k].n_split > 1 ? ((int64_t)batch.req[k].nkv * batch.req[k].rows + RPB - 1) / RPB : 0;
+        batch.first_cb[k] = (int32_t)std::min<int64_t>(ctotal, INT32_MAX);
+        ctotal += cblocks[k];
+    }
+    const int with_splits = (int)std::count_if(cblocks, cblocks + n, [](int64_t c) { return c > 0; });
+    if (with_splits > 1 && ctotal * 256 <= OC_MAX_GRID_ITEMS) {
+        hipLaunchKernelGGL(attn_combine_batch_kernel<D>, dim3((unsigned)ctotal), dim3(256), 0, s, batch);
+    } else {
+        // one request with splits, or too many rows for one dispatch: one
+        // merge per request (each fits, as the shape checks require)
+        for (int k = 0; k < n; ++k)
+            if (cblocks[k])
+                hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)cblocks[k]), dim3(256), 0, s,
+                                   batch.req[k]);
+    }
     return hipGetLastError();
 }
 

@@ -865,13 +865,14 @@ LATENCY_PAIRS = [
 def step_ingest(stats_all, wl):
     """In-step ingest of timed pipeline runs: algorithmic bytes (read + write
     of every layer payload) over the summed time between each layer's landed
-    and ingested events on the copy stream."""
+    and ingested events on the copy stream.  Requests whose layer is ingested
+    by one launch together report the same pair of events; it counts once."""
     L, b = wl.num_layers, 2 * wl.num_kv_heads * wl.head_dim * 2
     ingest_ms, n = 0.0, 0
     for st in stats_all:
-        for rst in st:
-            for l in range(L):
-                ingest_ms += rst["ingested_ms"][l] - rst["landed_ms"][l]
+        for l in range(L):
+            for t0, t1 in sorted({(rst["landed_ms"][l], rst["ingested_ms"][l]) for rst in st}):
+                ingest_ms += t1 - t0
                 n += 1
     nbytes = 2.0 * sum(wl.prefix_tokens) * b * L * len(stats_all)
     gbs = nbytes / (ingest_ms / 1e3) / 1e9

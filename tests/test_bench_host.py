@@ -145,3 +145,17 @@ def test_marker_summary_splits_each_layers_delivery(tmp_path):
     # run, host ms, layer ranges (driver thread only), mean range us, marks, mark gap ms,
     # spans per layer, DMA GB/s, mark -> last span, last span -> ingest, mark -> ingest (max)
     assert cells == ["0", "0.10", "2", "1.8", "2", "0.002", "1.5", "2.0", "0.8", "0.1", "0.8 (1.1)"]
+
+
+def test_step_ingest_counts_a_shared_launch_once():
+    # two requests of two layers, 400 tokens of 32 bytes per layer: 51200
+    # bytes read + written per run; layer 0 ingested by one launch for both
+    # (the same marker pair), layer 1 by one launch each
+    class W:
+        num_layers, num_kv_heads, head_dim, prefix_tokens = 2, 1, 8, [100, 300]
+    runs = [[{"landed_ms": [0.0, 2.0], "ingested_ms": [1.0, 2.5]},
+             {"landed_ms": [0.0, 2.5], "ingested_ms": [1.0, 3.5]}]]
+    r = bench.step_ingest(runs, W)
+    assert r["launches"] == 3
+    assert r["mean_launch_us"] == pytest.approx(2500.0 / 3)
+    assert r["value"] == pytest.approx(round(51200 / 2.5e-3 / 1e9, 2))

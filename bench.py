@@ -1056,12 +1056,14 @@ def _short(name):
 
 
 def marker_summary(paths):
-    """Markdown summary of a rocprofv3 --marker-trace --kernel-trace database:
-    the library's roctx ranges (each pipeline run, each layer's enqueue) and
-    marks (each payload the producer completes), set against the kernels.
-    Per run: the host time of the run and of its layer enqueues; with a
-    producer, the gap between payload marks (the delivery interval) and the
-    lag from a mark to the start of the first ingest launch after it."""
+    """Markdown summary of a rocprofv3 --marker-trace --kernel-trace
+    (--memory-copy-trace) database: the library's roctx ranges (each pipeline
+    run, each layer's wait and enqueue) and marks (each payload the producer
+    completes), set against the kernels and host-to-device copies.  Per run:
+    the host time of the run and of its layer ranges; with a producer, the gap
+    between payload marks (the delivery interval), the DMA spans of each layer
+    and the lag from a payload's mark to its last span landing and to its
+    ingest launch (one request delivered in layer order)."""
     import sqlite3
 
     def message(extdata):
@@ -1124,6 +1126,7 @@ def marker_summary(paths):
                     lag.append(k0 - m)
                 nb = float(sum(x[2] for x in cps))
                 dma = float(sum(x[1] - x[0] for x in cps))
+            if ts and cps and len(ts) == len(ing) and spans:
                 row += (f"{np.mean(spans):.1f} | {nb / dma:.1f} | {np.mean(land) / 1e3:.1f} | "
                         f"{np.mean(to_ing) / 1e3:.1f} | {np.mean(lag) / 1e3:.1f} ({np.max(lag) / 1e3:.1f}) |")
             else:

@@ -283,12 +283,14 @@ def test_injected_short_write_chunkwise_and_paced():
 def test_layer_lands_in_spans_while_produced():
     # 25 MiB layers land in 8 MiB spans as the paced producer's leading
     # pieces complete (3 threads finish pieces out of order; the last piece
-    # is ragged); every layer must reach the pool whole, and a short layer
-    # whose first spans were already landed must still never be ingested
+    # is ragged), through a ring of two slots, so each slot is refilled and
+    # landed again while the next layer's spans are in flight; every layer
+    # must reach the pool whole, and a short layer whose first spans were
+    # already landed must still never be ingested
     import paper_2605_22850_amd as oc
-    print("[pipeline] spans: 25 MiB layers, 256 KiB pieces", flush=True)
-    rs = RequestSet(3, 8, 8, 128, [6160], [12], 512, seed=10).upload()
-    kw = dict(rate_bytes_per_s=1.0e9, piece_bytes=256 << 10, producer_threads=3)
+    print("[pipeline] spans: 25 MiB layers, 256 KiB pieces, 2 slots", flush=True)
+    rs = RequestSet(5, 8, 8, 128, [6160], [12], 512, seed=10).upload()
+    kw = dict(rate_bytes_per_s=1.0e9, piece_bytes=256 << 10, producer_threads=3, slots=2)
     _run(rs, oc.OC_MODE_PRODUCER, **kw)
     assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool())
     out = _outs(rs)[0]

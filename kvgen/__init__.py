@@ -245,10 +245,20 @@ def workload(name: str, seed: Optional[int] = None) -> Workload:
     if name == "70b-32k":
         return _single("70b-32k", seed or 5, 80, 64, 8, 128, 32768, 512,
                        desc="70B shape (80 layers, 64q/8kv, d128), 32768-token prefix + 512-token suffix")
+    # one GPU's share of 8b-64k split eight ways: by KV head (each GPU holds
+    # one KV head and its four query heads), or by prefix pages (each GPU
+    # holds an eighth of the prefix; the one with the suffix does the most)
+    if name == "8b-64k-tp8":
+        return _single("8b-64k-tp8", seed or 3, 32, 4, 1, 128, 65536, 512,
+                       desc="8b-64k, one of 8 KV-head shards: 4q/1kv, 65536-token prefix + 512-token suffix")
+    if name == "8b-64k-cp8":
+        return _single("8b-64k-cp8", seed or 3, 32, 32, 8, 128, 8192, 512,
+                       desc="8b-64k, one of 8 prefix-page shards: 8192 prefix tokens + the 512-token suffix")
     raise KeyError(name)
 
 
 WORKLOADS = ["tiny", "8b-4k", "8b-64k", "batch8", "70b-32k"]
+SHARD_WORKLOADS = ["8b-64k-tp8", "8b-64k-cp8"]
 
 
 def with_chunk_tokens(wl: Workload, G: int) -> Workload:

@@ -120,7 +120,7 @@ def check_workload(wl):
 
 
 @pytest.mark.timeout(400)
-@pytest.mark.parametrize("name", kvgen.WORKLOADS)
+@pytest.mark.parametrize("name", kvgen.WORKLOADS + kvgen.SHARD_WORKLOADS)
 def test_workload_first_and_last_layer(name):
     check_workload(kvgen.workload(name))
 

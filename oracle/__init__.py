@@ -122,6 +122,8 @@ def ingest_layer(staging: np.ndarray, n_chunks: int, G: int, n_kv: int, d: int, 
     else:
         rc = lib.oco_ingest_layer(_ptr(staging), n_chunks, G, n_kv, d, Ps, _ptr(table), table.size,
                                   _ptr(pool), P, layer)
+    if rc == -2:
+        raise RuntimeError("could not start the ingest threads")
     if rc != 0:
         raise ValueError("block table entry out of range or too short")
 

@@ -105,7 +105,8 @@ int oco_ingest_layer(const uint16_t *staging, int64_t n_chunks, int32_t G, int32
 /* The same scatter with the chunks divided into `threads` contiguous ranges,
  * one thread each.  Chunks write distinct pool elements as long as the page
  * ids are distinct (the block table's contract), so the result equals
- * oco_ingest_layer's. */
+ * oco_ingest_layer's.  Returns -2 when a thread could not be started (its
+ * range is then not copied). */
 struct ingest_job {
     const uint16_t *staging;
     int64_t j0, j1;
@@ -136,12 +137,16 @@ int oco_ingest_layer_mt(const uint16_t *staging, int64_t n_chunks, int32_t G, in
                                layer, table, table_len, P, pool, 0};
         jobs[i] = J;
     }
-    for (int32_t i = 1; i < threads; ++i)
-        if (pthread_create(&tid[i], NULL, ingest_worker, &jobs[i]) != 0) jobs[i].rc = -2;
+    char started[256] = {0};
+    for (int32_t i = 1; i < threads; ++i) started[i] = pthread_create(&tid[i], NULL, ingest_worker, &jobs[i]) == 0;
     ingest_worker(&jobs[0]);
     int rc = jobs[0].rc;
     for (int32_t i = 1; i < threads; ++i) {
-        if (jobs[i].rc != -2) pthread_join(tid[i], NULL);
+        if (!started[i]) {   /* its chunks were not copied */
+            rc = -2;
+            continue;
+        }
+        pthread_join(tid[i], NULL);
         if (jobs[i].rc != 0) rc = jobs[i].rc;
     }
     return rc;

@@ -1,5 +1,6 @@
 // C entry points for single-layer calls: argument validation, then launch.
 // Nothing is enqueued unless every check passes.
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -174,26 +175,34 @@ int oc_abi_version(void) { return OC_ABI_VERSION; }
 
 const char *oc_last_error(void) { return g_err.c_str(); }
 
-int oc_block_table_check(const int32_t *host_pages, int64_t num_entries, int64_t num_tokens, int64_t num_pages,
-                         int32_t page_size) {
+static int block_table_check_body(const int32_t *host_pages, int64_t num_entries, int64_t num_tokens, int64_t num_pages,
+                                  int32_t page_size) {
     clear_error();
     if (page_size < 1 || num_tokens < 0 || num_entries < 0 || num_pages < 1)
         return fail(OC_EINVAL, "bad sizes");
     const int64_t need = (num_tokens + page_size - 1) / page_size;
     if (num_entries < need) return fail(OC_ERANGE, "block table shorter than the prefix needs");
     if (need > 0 && !host_pages) return fail(OC_EINVAL, "pages is NULL");
-    std::vector<unsigned char> seen((size_t)num_pages, 0);
     for (int64_t i = 0; i < need; ++i) {
         const int64_t p = host_pages[i];
         if (p < 0 || p >= num_pages) return fail(OC_ERANGE, "page id " + std::to_string(p) + " out of range");
-        if (seen[(size_t)p]) return fail(OC_ERANGE, "page id " + std::to_string(p) + " repeats");
-        seen[(size_t)p] = 1;
     }
+    // repeats: sorted, equal ids are neighbours (memory follows the table,
+    // not the pool)
+    std::vector<int32_t> ids(host_pages, host_pages + need);
+    std::sort(ids.begin(), ids.end());
+    for (size_t i = 1; i < ids.size(); ++i)
+        if (ids[i] == ids[i - 1]) return fail(OC_ERANGE, "page id " + std::to_string(ids[i]) + " repeats");
     return OC_OK;
 }
 
-int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_table, oc_kv_pool *kv_pool,
-                       int32_t layer, void *stream) {
+int oc_block_table_check(const int32_t *host_pages, int64_t num_entries, int64_t num_tokens, int64_t num_pages,
+                         int32_t page_size) {
+    return guarded([&] { return block_table_check_body(host_pages, num_entries, num_tokens, num_pages, page_size); });
+}
+
+static int kv_layer_ingest_body(const oc_staging *staging, const oc_block_table *block_table, oc_kv_pool *kv_pool,
+                                int32_t layer, void *stream) {
     clear_error();
     if (!staging || !kv_pool) return fail(OC_EINVAL, "staging and kv_pool must not be NULL");
     int rc = check_layout(kv_pool->layout);
@@ -214,8 +223,13 @@ int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_ta
     return OC_OK;
 }
 
-int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc_block_table *block_table,
-                        oc_kv_pool *kv_pool, void *stream) {
+int oc_kv_layer_ingest(const oc_staging *staging, const oc_block_table *block_table, oc_kv_pool *kv_pool,
+                       int32_t layer, void *stream) {
+    return guarded([&] { return kv_layer_ingest_body(staging, block_table, kv_pool, layer, stream); });
+}
+
+static int kv_chunks_ingest_body(const oc_staging *objects, int64_t first_chunk, const oc_block_table *block_table,
+                                 oc_kv_pool *kv_pool, void *stream) {
     clear_error();
     if (!objects || !kv_pool) return fail(OC_EINVAL, "objects and kv_pool must not be NULL");
     int rc = check_layout(kv_pool->layout);
@@ -240,8 +254,13 @@ int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc
     return OC_OK;
 }
 
-int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int32_t layer,
-                       void *staging_out, int64_t num_chunks, int64_t per_layer_chunk_bytes, void *stream) {
+int oc_kv_chunks_ingest(const oc_staging *objects, int64_t first_chunk, const oc_block_table *block_table,
+                        oc_kv_pool *kv_pool, void *stream) {
+    return guarded([&] { return kv_chunks_ingest_body(objects, first_chunk, block_table, kv_pool, stream); });
+}
+
+static int kv_layer_gather_body(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int32_t layer,
+                                void *staging_out, int64_t num_chunks, int64_t per_layer_chunk_bytes, void *stream) {
     clear_error();
     if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
     int rc = check_layout(kv_pool->layout);
@@ -261,8 +280,16 @@ int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_p
     return OC_OK;
 }
 
-int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int64_t first_chunk,
-                        int64_t num_chunks, void *objects_out, void *stream) {
+int oc_kv_layer_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int32_t layer,
+                       void *staging_out, int64_t num_chunks, int64_t per_layer_chunk_bytes, void *stream) {
+    return guarded([&] {
+        return kv_layer_gather_body(block_table, kv_pool, layer, staging_out, num_chunks, per_layer_chunk_bytes,
+                                    stream);
+    });
+}
+
+static int kv_chunks_gather_body(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int64_t first_chunk,
+                                 int64_t num_chunks, void *objects_out, void *stream) {
     clear_error();
     if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
     int rc = check_layout(kv_pool->layout);
@@ -284,8 +311,16 @@ int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_
     return OC_OK;
 }
 
-int oc_rest_of_layer(const void *attn_out, int64_t tokens, const oc_layout *layout, const oc_layer_weights *weights,
-                     int32_t layer, const oc_layer_buffers *buffers, void *stream) {
+int oc_kv_chunks_gather(const oc_block_table *block_table, const oc_kv_pool *kv_pool, int64_t first_chunk,
+                        int64_t num_chunks, void *objects_out, void *stream) {
+    return guarded([&] {
+        return kv_chunks_gather_body(block_table, kv_pool, first_chunk, num_chunks, objects_out, stream);
+    });
+}
+
+static int rest_of_layer_body(const void *attn_out, int64_t tokens, const oc_layout *layout,
+                              const oc_layer_weights *weights, int32_t layer, const oc_layer_buffers *buffers,
+                              void *stream) {
     clear_error();
     if (!layout) return fail(OC_EINVAL, "layout is NULL");
     int rc = check_layout(*layout);
@@ -302,8 +337,13 @@ int oc_rest_of_layer(const void *attn_out, int64_t tokens, const oc_layout *layo
     return launch_rest_of_layer(a, static_cast<hipStream_t>(stream));
 }
 
-int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tokens,
-                        const oc_block_table *block_table, oc_kv_pool *kv_pool, int32_t layer, void *stream) {
+int oc_rest_of_layer(const void *attn_out, int64_t tokens, const oc_layout *layout, const oc_layer_weights *weights,
+                     int32_t layer, const oc_layer_buffers *buffers, void *stream) {
+    return guarded([&] { return rest_of_layer_body(attn_out, tokens, layout, weights, layer, buffers, stream); });
+}
+
+static int kv_suffix_append_body(const void *k_new, const void *v_new, int64_t suffix_tokens,
+                                 const oc_block_table *block_table, oc_kv_pool *kv_pool, int32_t layer, void *stream) {
     clear_error();
     if (!kv_pool) return fail(OC_EINVAL, "kv_pool must not be NULL");
     int rc = check_layout(kv_pool->layout);
@@ -321,6 +361,13 @@ int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tok
     AppendArgs a = append_args(kv_pool, block_table, layer, k_new, v_new, suffix_tokens);
     OC_HIP(launch_append(a, static_cast<hipStream_t>(stream)));
     return OC_OK;
+}
+
+int oc_kv_suffix_append(const void *k_new, const void *v_new, int64_t suffix_tokens,
+                        const oc_block_table *block_table, oc_kv_pool *kv_pool, int32_t layer, void *stream) {
+    return guarded([&] {
+        return kv_suffix_append_body(k_new, v_new, suffix_tokens, block_table, kv_pool, layer, stream);
+    });
 }
 
 size_t oc_attention_workspace_bytes(const oc_layout *layout, int64_t prefix_tokens, int64_t suffix_tokens) {
@@ -384,9 +431,9 @@ static int enqueue_attention(const AttnPlan &p, const void *q, const void *k_new
 
 extern "C" {
 
-int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
-                            const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
-                            void *workspace, size_t workspace_bytes, void *stream) {
+static int suffix_prefill_layer_body(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                                     const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
+                                     void *workspace, size_t workspace_bytes, void *stream) {
     clear_error();
     AttnPlan p;
     int rc = check_attention_call(q, k_new, v_new, suffix_tokens, kv_pool, block_table, layer, out, &p);
@@ -399,9 +446,18 @@ int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
                              static_cast<hipStream_t>(stream));
 }
 
-int oc_suffix_prefill_layer_noalloc(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
-                                    const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer,
-                                    void *out, void *stream) {
+int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                            const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer, void *out,
+                            void *workspace, size_t workspace_bytes, void *stream) {
+    return guarded([&] {
+        return suffix_prefill_layer_body(q, k_new, v_new, suffix_tokens, kv_pool, block_table, layer, out, workspace,
+                                         workspace_bytes, stream);
+    });
+}
+
+static int suffix_prefill_layer_noalloc_body(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                                             const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer,
+                                             void *out, void *stream) {
     clear_error();
     AttnPlan p;
     int rc = check_attention_call(q, k_new, v_new, suffix_tokens, kv_pool, block_table, layer, out, &p);
@@ -414,6 +470,15 @@ int oc_suffix_prefill_layer_noalloc(const void *q, const void *k_new, const void
     if ((rc = scratch_on_current_device(&ws))) return rc;
     return enqueue_attention(p, q, k_new, v_new, kv_pool, block_table, layer, out, ws,
                              static_cast<hipStream_t>(stream));
+}
+
+int oc_suffix_prefill_layer_noalloc(const void *q, const void *k_new, const void *v_new, int64_t suffix_tokens,
+                                    const oc_kv_pool *kv_pool, const oc_block_table *block_table, int32_t layer,
+                                    void *out, void *stream) {
+    return guarded([&] {
+        return suffix_prefill_layer_noalloc_body(q, k_new, v_new, suffix_tokens, kv_pool, block_table, layer, out,
+                                                 stream);
+    });
 }
 
 }  // extern "C"

@@ -5,7 +5,10 @@
 
 #include <cstdint>
 #include <cstdio>
+#include <new>
+#include <stdexcept>
 #include <string>
+#include <system_error>
 
 #include "objectcache.h"
 
@@ -16,6 +19,30 @@ void set_error(const std::string &msg);
 void clear_error();
 int fail(int status, const std::string &msg);
 int hip_fail(hipError_t e, const char *what);
+
+// The body of a C entry point, run so that no C++ exception leaves the
+// library: host memory that cannot be allocated, or a thread that cannot be
+// started, becomes OC_ENOMEM with a message.
+template <class F>
+int guarded(F &&body) noexcept {
+    const char *why;
+    try {
+        return body();
+    } catch (const std::bad_alloc &) {
+        why = "out of host memory";
+    } catch (const std::length_error &) {
+        why = "out of host memory";
+    } catch (const std::system_error &) {
+        why = "could not start a host thread";
+    } catch (...) {
+        why = "unexpected C++ exception";
+    }
+    try {
+        set_error(why);
+    } catch (...) {
+    }
+    return OC_ENOMEM;
+}
 
 #define OC_HIP(call)                                 \
     do {                                             \

@@ -21,6 +21,7 @@
 #include <cstring>
 #include <deque>
 #include <queue>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -103,6 +104,20 @@ static inline int64_t copy_len(const oc_pipeline_opts &o, int32_t layer, int64_t
 static inline int64_t landing_span(const oc_pipeline_opts &o, int64_t layer_bytes) {
     if (!(o.rate_bytes_per_s > 0)) return std::max<int64_t>(layer_bytes, 1);
     return std::max<int64_t>({o.piece_bytes, layer_bytes / 8, (int64_t)8 << 20});
+}
+
+// Starts up to n threads running fn, fewer if the system refuses more;
+// returns how many run.
+template <class F>
+static int start_threads(std::vector<std::thread> &pool, int n, F fn) {
+    for (int i = 0; i < n; ++i) {
+        try {
+            pool.emplace_back(fn);
+        } catch (...) {
+            break;
+        }
+    }
+    return (int)pool.size();
 }
 
 // Stall and abort stop delivery at fault_layer; a short write still delivers.
@@ -300,10 +315,11 @@ struct Producer {
     }
 
     void run() {
-        const int nw = c->opts.producer_threads;
         std::vector<std::thread> pool;
-        pool.reserve(nw);
-        for (int i = 0; i < nw; ++i) pool.emplace_back([this] { worker(); });
+        if (start_threads(pool, c->opts.producer_threads, [this] { worker(); }) == 0) {
+            set_error(OC_ENOMEM, "could not start the producer's copy threads");
+            return;
+        }
         double cum = 0.0;
         const int64_t n_items = (int64_t)items->size();
         const int64_t nslots = (int64_t)c->slots.size();
@@ -538,9 +554,11 @@ struct RateProducer {
                 }
             }
         }
-        const int nw = c->opts.producer_threads;
         std::vector<std::thread> pool;
-        for (int i = 0; i < nw; ++i) pool.emplace_back([this] { worker(); });
+        if (start_threads(pool, c->opts.producer_threads, [this] { worker(); }) == 0) {
+            set_error(OC_ENOMEM, "could not start the producer's copy threads");
+            return;
+        }
         bool failed = false;
         double last_round = now_s();
         for (;;) {
@@ -899,6 +917,21 @@ static int run_pipeline(Context *c, const oc_request *reqs, int32_t n_reqs, oc_r
     Producer prod{};
     RateProducer rprod{};
     std::thread producer_thread;
+    // however the run ends (an exception included), the producer is stopped
+    // and joined before the state it uses goes away
+    struct StopOnExit {
+        std::thread &t;
+        RunShared &sh;
+        ~StopOnExit() {
+            if (!t.joinable()) return;
+            {
+                std::lock_guard<std::mutex> g(sh.mu);
+                sh.abort = true;
+            }
+            sh.cv.notify_all();
+            t.join();
+        }
+    } stop_on_exit{producer_thread, sh};
     const hipStream_t first = mode == OC_MODE_HBM_RESIDENT ? c->compute : c->copy;
     OC_HIP(hipEventRecord(ev_start, first));
     if (mode != OC_MODE_HBM_RESIDENT) OC_HIP(hipStreamWaitEvent(c->compute, ev_start, 0));
@@ -1234,8 +1267,8 @@ using namespace oc;
 
 extern "C" {
 
-int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_opts *opts, int64_t max_prefix_tokens,
-                      int64_t max_suffix_tokens, void **ctx) {
+static int context_create_body(int device, const oc_kv_pool *kv_pool, const oc_pipeline_opts *opts,
+                               int64_t max_prefix_tokens, int64_t max_suffix_tokens, void **ctx) {
     clear_error();
     if (!kv_pool || !ctx) return fail(OC_EINVAL, "kv_pool and ctx must not be NULL");
     *ctx = nullptr;
@@ -1247,20 +1280,16 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
     if (check_copy_pieces(max_prefix_tokens * 2 * l.num_kv_heads * (l.head_dim / 8), "layer payload"))
         return fail(OC_ERANGE, oc_last_error());
     if (!kv_pool->base || !aligned(kv_pool->base, 16)) return fail(OC_EALIGN, "pool base must be 16-byte aligned");
-    Context *c = new Context();
+    // released (streams, events, memory) on every early return
+    std::unique_ptr<Context, void (*)(Context *)> hold(new Context(), release);
+    Context *c = hold.get();
     c->device = device;
     c->pool = *kv_pool;
     c->opts = opts ? *opts : oc_pipeline_opts{};
     int rc = fill_defaults(c->opts);
-    if (rc) {
-        delete c;
-        return rc;
-    }
+    if (rc) return rc;
     if (c->opts.layer_weights) {
-        if ((rc = check_layer_weights(l, c->opts.layer_weights))) {
-            delete c;
-            return rc;
-        }
+        if ((rc = check_layer_weights(l, c->opts.layer_weights))) return rc;
         c->has_layer = true;
         c->lw = *c->opts.layer_weights;
         c->opts.layer_weights = &c->lw;
@@ -1274,49 +1303,49 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
         c->slot_bytes = std::max(c->slot_bytes, obj);
     }
     int n_dev = 0;
-    if (hipGetDeviceCount(&n_dev) != hipSuccess || device < 0 || device >= n_dev) {
-        delete c;
+    if (hipGetDeviceCount(&n_dev) != hipSuccess || device < 0 || device >= n_dev)
         return fail(OC_EINVAL, "no such device");
-    }
     const DeviceScope on_device(device);
     // default-priority, non-blocking streams
     if (hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking) != hipSuccess ||
-        hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking) != hipSuccess) {
-        release(c);
+        hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking) != hipSuccess)
         return fail(OC_EHIP, "stream creation failed");
-    }
-    if (hipEventCreateWithFlags(&c->caller_done, hipEventDisableTiming) != hipSuccess) {
-        release(c);
+    if (hipEventCreateWithFlags(&c->caller_done, hipEventDisableTiming) != hipSuccess)
         return fail(OC_EHIP, "event creation failed");
-    }
     if (c->opts.mode == OC_MODE_PRODUCER && c->slot_bytes > 0) {
         c->slots.resize((size_t)c->opts.slots);
         for (auto &s : c->slots) {
             if (hipHostMalloc(&s.pinned, c->slot_bytes, hipHostMallocDefault) != hipSuccess ||
-                hipMalloc(&s.device, c->slot_bytes) != hipSuccess) {
-                release(c);
+                hipMalloc(&s.device, c->slot_bytes) != hipSuccess)
                 return fail(OC_ENOMEM, "staging slot allocation failed");
-            }
         }
     }
     AttnPlan p;
     plan_attention(l, max_prefix_tokens, max_suffix_tokens, &p);
-    if (hipMalloc(&c->ws, p.total) != hipSuccess) {
-        release(c);
-        return fail(OC_ENOMEM, "attention workspace allocation failed");
-    }
+    if (hipMalloc(&c->ws, p.total) != hipSuccess) return fail(OC_ENOMEM, "attention workspace allocation failed");
     c->ws_bytes = p.total;
-    *ctx = c;
+    *ctx = hold.release();
     return OC_OK;
 }
 
-int oc_pipeline_run(void *ctx, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
+int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_opts *opts, int64_t max_prefix_tokens,
+                      int64_t max_suffix_tokens, void **ctx) {
+    return guarded([&] {
+        return context_create_body(device, kv_pool, opts, max_prefix_tokens, max_suffix_tokens, ctx);
+    });
+}
+
+static int pipeline_run_body(void *ctx, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
     clear_error();
     Context *c = static_cast<Context *>(ctx);
     if (!c || !reqs || n_reqs < 1) return fail(OC_EINVAL, "NULL context/requests or n_reqs < 1");
     int rc = validate_requests(c, reqs, n_reqs);
     if (rc) return rc;
     return run_pipeline(c, reqs, n_reqs, stats);
+}
+
+int oc_pipeline_run(void *ctx, const oc_request *reqs, int32_t n_reqs, oc_request_stats *stats) {
+    return guarded([&] { return pipeline_run_body(ctx, reqs, n_reqs, stats); });
 }
 
 double oc_pipeline_last_ms(void *ctx) { return ctx ? static_cast<Context *>(ctx)->last_ms : 0.0; }

@@ -51,9 +51,10 @@ void water_fill(int n, const double *s, const double *cap, double B, double *r) 
 }  // namespace oc
 
 using oc::fail;
+using oc::guarded;
 
-int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
-                          double budget_bytes_per_s, double margin_bytes_per_s, double *rates_out) {
+static int bandwidth_allocate_body(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
+                                   double budget_bytes_per_s, double margin_bytes_per_s, double *rates_out) {
     oc::clear_error();
     if (n < 1 || !layer_bytes || !rates_out) return fail(OC_EINVAL, "need n >= 1 requests and non-NULL arrays");
     if (!(budget_bytes_per_s > 0.0) || !std::isfinite(budget_bytes_per_s))
@@ -100,6 +101,14 @@ int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes, 
     }
 }
 
+int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
+                          double budget_bytes_per_s, double margin_bytes_per_s, double *rates_out) {
+    return guarded([&] {
+        return bandwidth_allocate_body(policy, n, layer_bytes, layer_compute_s, budget_bytes_per_s,
+                                       margin_bytes_per_s, rates_out);
+    });
+}
+
 // Scheduling epochs (Section 3.6): the rates of oc_bandwidth_allocate for
 // requests that arrive over time.  At each epoch boundary the requests that
 // have arrived and wait are admitted together and share the budget that the
@@ -108,9 +117,9 @@ int oc_bandwidth_allocate(int32_t policy, int32_t n, const double *layer_bytes, 
 // and the rate it then releases is handed out at the next boundary, never to
 // a request already in flight.  Boundaries are the multiples of epoch_s, or
 // with epoch_s == 0 every arrival and every completion.
-int oc_epoch_schedule(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
-                      int32_t num_layers, const double *arrival_s, double budget_bytes_per_s,
-                      double margin_bytes_per_s, double epoch_s, double *rates_out, double *admit_s_out) {
+static int epoch_schedule_body(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
+                               int32_t num_layers, const double *arrival_s, double budget_bytes_per_s,
+                               double margin_bytes_per_s, double epoch_s, double *rates_out, double *admit_s_out) {
     oc::clear_error();
     if (n < 1 || !layer_bytes || !arrival_s || !rates_out || !admit_s_out)
         return fail(OC_EINVAL, "need n >= 1 requests and non-NULL arrays");
@@ -175,4 +184,13 @@ int oc_epoch_schedule(int32_t policy, int32_t n, const double *layer_bytes, cons
         }
     }
     return OC_OK;
+}
+
+int oc_epoch_schedule(int32_t policy, int32_t n, const double *layer_bytes, const double *layer_compute_s,
+                      int32_t num_layers, const double *arrival_s, double budget_bytes_per_s,
+                      double margin_bytes_per_s, double epoch_s, double *rates_out, double *admit_s_out) {
+    return guarded([&] {
+        return epoch_schedule_body(policy, n, layer_bytes, layer_compute_s, num_layers, arrival_s, budget_bytes_per_s,
+                                   margin_bytes_per_s, epoch_s, rates_out, admit_s_out);
+    });
 }

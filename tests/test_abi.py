@@ -212,6 +212,12 @@ def test_block_table_check():
     with pytest.raises(oc.OcError):
         oc.oc_block_table_check([3, 1], 40, 4, 16)
     oc.oc_block_table_check(np.zeros(0, np.int32), 0, 4, 16)
+    # the check's memory follows the table, not the pool: a pool of 2^62
+    # pages is no reason to fail
+    oc.oc_block_table_check([5, 1 << 30, 7], 40, 1 << 62, 16)
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_block_table_check([5, 1 << 30, 5], 40, 1 << 62, 16)
+    assert e.value.status == L.OC_ERANGE and "repeats" in str(e.value)
 
 
 def test_context_rejects_an_absent_device():

@@ -429,6 +429,9 @@ int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_o
                       int64_t max_prefix_tokens, int64_t max_suffix_tokens, void **ctx);
 
 /* Run the pipeline over n_reqs requests for all L layers; synchronous.
+ * A context serves one run at a time; runs on different contexts may
+ * overlap, from different host threads (each context has its own streams,
+ * staging and producer threads).
  * stats (optional) has n_reqs entries.  On OC_ETIMEOUT / OC_EABORT the run is
  * stopped, all enqueued GPU work is drained and the context stays usable.
  * Once the producer completes a payload, the byte count it reports is

@@ -1302,6 +1302,9 @@ static int context_create_body(int device, const oc_kv_pool *kv_pool, const oc_p
         const size_t obj = (size_t)l.num_layers * 2 * l.chunk_tokens * l.num_kv_heads * l.head_dim * 2;
         c->slot_bytes = std::max(c->slot_bytes, obj);
     }
+    // the producer's ring always has its slots, even for requests that bring
+    // no cached prefix (the driver and producer index the ring per item)
+    if (c->opts.mode == OC_MODE_PRODUCER) c->slot_bytes = std::max<size_t>(c->slot_bytes, 256);
     int n_dev = 0;
     if (hipGetDeviceCount(&n_dev) != hipSuccess || device < 0 || device >= n_dev)
         return fail(OC_EINVAL, "no such device");
@@ -1312,7 +1315,7 @@ static int context_create_body(int device, const oc_kv_pool *kv_pool, const oc_p
         return fail(OC_EHIP, "stream creation failed");
     if (hipEventCreateWithFlags(&c->caller_done, hipEventDisableTiming) != hipSuccess)
         return fail(OC_EHIP, "event creation failed");
-    if (c->opts.mode == OC_MODE_PRODUCER && c->slot_bytes > 0) {
+    if (c->opts.mode == OC_MODE_PRODUCER) {
         c->slots.resize((size_t)c->opts.slots);
         for (auto &s : c->slots) {
             if (hipHostMalloc(&s.pinned, c->slot_bytes, hipHostMallocDefault) != hipSuccess ||

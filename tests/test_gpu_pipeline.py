@@ -352,6 +352,26 @@ def test_unknown_fault_rejected():
     assert e.value.status == oc._lib.OC_EINVAL
 
 
+def test_requests_without_a_cached_prefix_through_the_producer():
+    # a context made for requests that bring no cached prefix at all
+    # (max_prefix_tokens 0) still has its staging ring; every delivery and
+    # policy runs, the pool stays untouched and each output is the attention
+    # over the suffix alone
+    import paper_2605_22850_amd as oc
+    print("[pipeline] producer, no cached prefix", flush=True)
+    rs = RequestSet(3, 8, 2, 128, [0, 0], [17, 40], 8, seed=13).upload()
+    for kw in ({}, {"rate_bytes_per_s": 1e6}, {"delivery": "chunkwise"}, {"delivery": "auto", "theta_bytes": 1e9},
+               {"alloc_policy": "equal", "rate_bytes_per_s": 1e6}):
+        for r in rs.reqs:
+            r.out.zero_()
+        _run(rs, oc.OC_MODE_PRODUCER, **kw)
+        assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool()), kw
+        for r in range(2):
+            out = from_dev(rs.reqs[r].out)
+            for l in range(rs.L):
+                assert_attention_close(out[l], rs.expected_out(r, l), f"{kw} request {r} layer {l}")
+
+
 def test_bad_request_rejected_before_running():
     import paper_2605_22850_amd as oc
     print("[pipeline] validation", flush=True)

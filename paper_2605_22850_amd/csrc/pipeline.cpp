@@ -20,9 +20,9 @@
 #include <condition_variable>
 #include <cstring>
 #include <deque>
-#include <queue>
 #include <memory>
 #include <mutex>
+#include <queue>
 #include <string>
 #include <thread>
 #include <vector>
@@ -396,13 +396,14 @@ struct Producer {
 // byte: a request that finishes early does not pass its rate on to the
 // others in flight; later admissions get it.  The dispatcher hands out
 // payload pieces by weighted deficit round robin to the copy threads, which
-// copy each piece once its release time has come.  A request's credit grows with elapsed time at its rate (the
-// weight), not by a fixed amount per round: rounds are uneven in length, and
-// a per-round quantum would hold a slow request below its rate whenever its
-// share of a round is smaller than the round's length times its rate.  A request
-// starts its next layer only when a staging slot is free; its layers are
-// reported to the driver in layer order, and the driver lands whichever
-// layer is reported first, so a slow request does not hold up a fast one.
+// copy each piece once its release time has come.  A request's credit grows
+// with elapsed time at its rate (the weight), not by a fixed amount per
+// round: rounds are uneven in length, and a per-round quantum would hold a
+// slow request below its rate whenever its share of a round is smaller than
+// the round's length times its rate.  A request starts its next layer only
+// when a staging slot is free; its layers are reported to the driver in
+// layer order, and the driver lands whichever layer is reported first, so a
+// slow request does not hold up a fast one.
 struct RateProducer {
     Context *c;
     RunShared *sh;

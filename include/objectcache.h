@@ -420,9 +420,11 @@ typedef struct {
 } oc_request_stats;
 
 /* Create a context on `device` for one pool.  Allocates the streams, events,
- * pinned and HBM staging rings (slots * max_layer_bytes each) and the
- * attention workspace for up to max_prefix_tokens / max_suffix_tokens, and
- * keeps them until oc_context_destroy.  The pool stays caller-owned.  An
+ * the attention workspace for up to max_prefix_tokens / max_suffix_tokens
+ * and, in PRODUCER mode, the pinned and HBM staging rings (`slots` slots
+ * each, a slot holding the largest layer payload, max_prefix_tokens * b
+ * bytes, or one whole chunk object if that is larger and the delivery may be
+ * chunkwise), and keeps them until oc_context_destroy.  The pool stays caller-owned.  An
  * absent device is OC_EINVAL.  Context calls make `device` current while they
  * run and give the caller its current device back. */
 int oc_context_create(int device, const oc_kv_pool *kv_pool, const oc_pipeline_opts *opts,

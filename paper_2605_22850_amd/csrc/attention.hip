@@ -202,7 +202,7 @@ __device__ __forceinline__ void matrix_phase(WaveState<D> &w, const uint16_t *V,
     bf16x8 f[N];
     // the wavefront in its matrix phase issues ahead of its SIMD partner's
     // softmax: the MFMA pipe is the longer of the two (about 3 % per layer)
-    __builtin_amdgcn_s_setprio(1);
+    __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int n = 0; n < LOOKAHEAD && n < N; ++n) f[n] = PV ? pre[n] : load(n);
 #pragma unroll
@@ -217,7 +217,7 @@ __device__ __forceinline__ void matrix_phase(WaveState<D> &w, const uint16_t *V,
         }
         __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_s_setprio(1);
 }
 
 // Softmax phase of a wavefront for one block: the block maximum (one lane
@@ -271,6 +271,10 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KBatch batch) {
     // (scalar loads at a uniform offset; indexing the by-value copy would
     // place it in scratch memory)
     typedef const __attribute__((address_space(4))) KBatch *kbatch_ptr;
+    // every wavefront issues ahead of the ingest wavefronts that may share
+    // its SIMD (they keep the lowest priority); the matrix phase goes one
+    // level higher still
+    __builtin_amdgcn_s_setprio(1);
     const kbatch_ptr bp = (kbatch_ptr)__builtin_amdgcn_kernarg_segment_ptr();
     int req = 0;
     for (int i = 1; i < bp->n; ++i) req += (int)blockIdx.x >= bp->first_wg[i];
@@ -706,6 +710,10 @@ int64_t attention_grid(const AttnPlan &p) { return 8 * (((int64_t)p.nkv * p.n_sp
 
 // a dispatch holds at most 2^32 - 1 work-items along x
 int64_t attention_max_grid() { return OC_MAX_GRID_ITEMS / THREADS; }
+
+size_t attention_lds_bytes(int head_dim) {
+    return head_dim == 64 ? attn_lds_bytes<64>() : head_dim == 128 ? attn_lds_bytes<128>() : 0;
+}
 
 int check_attention_shape(const oc_layout &l, int64_t Tp, int64_t Ts) {
     if (l.head_dim != 64 && l.head_dim != 128) return fail(OC_ESHAPE, "attention supports head_dim 64 or 128");

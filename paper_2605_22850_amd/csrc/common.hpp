@@ -158,6 +158,10 @@ int check_attention_args(const oc_layout &lay, int64_t Tp, int64_t Ts);
 int64_t attention_grid(const AttnPlan &p);
 // at most this many workgroups in one attention launch (all its requests)
 int64_t attention_max_grid();
+// LDS one attention workgroup holds at this head_dim (0: not supported)
+size_t attention_lds_bytes(int head_dim);
+// LDS of one compute unit on gfx950
+constexpr size_t CU_LDS_BYTES = 160 * 1024;
 // one launch for up to MAX_ATTN_BATCH requests of one layer: keys are split
 // so that every workgroup gets about the same number of key blocks
 constexpr int MAX_ATTN_BATCH = 16;

@@ -10,10 +10,11 @@
 //    run): one piece per thread in payload order, so every wavefront reads
 //    1 KiB of the payload contiguously and writes four 256-byte rows, and
 //    many short wavefronts keep the most bytes in flight;
-//  - beside the attention kernel of an earlier layer, where only a couple of
-//    ingest wavefronts per SIMD fit: a thread takes 8 slots x one 16-byte
-//    column of one (page, head) block and moves its K rows, then its V rows
-//    (8 loads in flight, one page lookup per 256 bytes moved).
+//  - beside the attention kernel of an earlier layer, where two ingest
+//    wavefronts per SIMD run at the lowest issue priority: a thread takes
+//    8 slots x one 16-byte column of one (page, head) block and moves its K
+//    rows, then its V rows (8 loads in flight, one page lookup per 256 bytes
+//    moved, a shift decode of the thread's block and column).
 // The gather (pool -> payload or whole chunk objects, the offload direction)
 // numbers pieces the same way, reversed.  The suffix append writes the new
 // tokens' K/V rows behind the prefix through the same block table.
@@ -25,52 +26,80 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 
-// 8 slots x one 16-byte column of one (page, head) block, K then V.
+// 8 slots x one 16-byte column of one (page, head) block, K then V.  With
+// POW2 (d/8, page size, KV heads and a chunk size of at least 8 all powers of
+// two) the decode is shifts and masks and the 8 tokens sit in one chunk.
+// Every group of 8 slots lies wholly inside or wholly past the prefix when
+// the chunk size is a multiple of 8; only other chunk sizes reach the
+// per-token bounds checks.
+template <bool POW2>
 __global__ __launch_bounds__(kThreads, 8) void kv_ingest_rows_kernel(IngestArgs a, int64_t n_rows8) {
     const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (u >= n_rows8) return;
-    const int d = a.d, Ps = a.Ps, G = a.G, nkv = a.n_kv;
-    const int c = (int)(u % a.d8);
-    int64_t rest = u / a.d8;
-    const int s8 = (int)(rest % (Ps / 8));
-    rest /= Ps / 8;
-    const int h = (int)(rest % nkv);
-    const int64_t q = rest / nkv;
-    const int64_t D = (int64_t)nkv * d;
-    const int64_t T0 = q * Ps + s8 * 8;                  // first token of the 8
-    const int64_t left = a.num_tokens - T0;
-    const int valid = left < 8 ? (int)left : 8;          // tokens inside the prefix
-    const int64_t page = a.pages[q];
-    uint16_t *kdst = a.pool_k + ((page * nkv + h) * Ps + s8 * 8) * (int64_t)d + c * 8;
-    const int64_t col = (int64_t)h * d + c * 8;
-    // payload row of token T0 + i, K matrix (the V row is G*D further on)
-    int64_t src[8];
-    if (G % 8 == 0) {
-        // the 8 tokens sit in one chunk, one payload row apart
-        const int64_t j = T0 / G, t0 = T0 - j * G;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) src[i] = j * a.chunk_stride + (t0 + i) * D + col;
+    const int d = a.d, G = a.G, nkv = a.n_kv;
+    int c, s8, h;
+    int64_t q, T0;
+    if (POW2) {
+        const int lg_s8 = a.lg_ps - 3;                   // page_size / 8 groups per page
+        c = (int)(u & (a.d8 - 1));
+        s8 = (int)((u >> a.lg_d8) & ((1 << lg_s8) - 1));
+        h = (int)((u >> (a.lg_d8 + lg_s8)) & (nkv - 1));
+        q = u >> (a.lg_d8 + lg_s8 + a.lg_nkv);
+        T0 = (q << a.lg_ps) + s8 * 8;
     } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int64_t T = T0 + i, j = T / G;
-            src[i] = j * a.chunk_stride + (T - j * G) * D + col;
-        }
+        c = (int)(u % a.d8);
+        int64_t rest = u / a.d8;
+        s8 = (int)(rest % (a.Ps / 8));
+        rest /= a.Ps / 8;
+        h = (int)(rest % nkv);
+        q = rest / nkv;
+        T0 = q * a.Ps + s8 * 8;                          // first token of the 8
     }
+    const int64_t left = a.num_tokens - T0;
+    if (left <= 0) return;                               // slots past the prefix
+    const int64_t D = (int64_t)nkv * d;
+    const int64_t page = a.pages[q];
+    uint16_t *kdst = a.pool_k + ((page * nkv + h) * a.Ps + s8 * 8) * (int64_t)d + c * 8;
+    const int64_t col = (int64_t)h * d + c * 8;
+    const int64_t vstep = (int64_t)G * D;                // K row -> V row of a token
+    // non-temporal: the payload is read once and the pool rows are not read
+    // again until that layer's attention, so keep both out of the L2 that the
+    // running attention uses for its K/V tiles
     u32x4 r[8];
+    if (POW2 || (G % 8 == 0)) {
+        // the 8 tokens sit in one chunk, one payload row apart, all inside
+        // the prefix (it is a whole number of chunks)
+        const int64_t j = POW2 ? T0 >> a.lg_g : T0 / G;
+        const uint16_t *src = a.staging + j * a.chunk_stride + (T0 - j * G) * D + col;
+#pragma unroll
+        for (int kv = 0; kv < 2; ++kv) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + kv * vstep + i * D));
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                __builtin_nontemporal_store(r[i], reinterpret_cast<u32x4 *>(kdst + kv * a.region + i * d));
+        }
+        return;
+    }
+    // chunk sizes that are not a multiple of 8: the 8 tokens may span two
+    // chunks and run past the prefix
+    const int valid = left < 8 ? (int)left : 8;
+    int64_t src[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int64_t T = T0 + i, j = T / G;
+        src[i] = j * a.chunk_stride + (T - j * G) * D + col;
+    }
 #pragma unroll
     for (int kv = 0; kv < 2; ++kv) {
-        const int64_t off = kv * (int64_t)G * D;
-        uint16_t *dst = kdst + kv * a.region;
-        // non-temporal: the payload is read once and the pool rows are not
-        // read again until that layer's attention, so keep both out of the
-        // L2 that the running attention uses for its K/V tiles
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-            if (i < valid) r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.staging + src[i] + off));
+            if (i < valid)
+                r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.staging + src[i] + kv * vstep));
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-            if (i < valid) __builtin_nontemporal_store(r[i], reinterpret_cast<u32x4 *>(dst + i * d));
+            if (i < valid) __builtin_nontemporal_store(r[i], reinterpret_cast<u32x4 *>(kdst + kv * a.region + i * d));
     }
 }
 
@@ -185,18 +214,27 @@ static bool prepare(IngestArgs &a) {
 hipError_t launch_ingest(IngestArgs a, int64_t n_pages_used, hipStream_t s, bool beside_compute) {
     if (n_pages_used == 0) return hipSuccess;
     const bool p2 = prepare(a);
-    const int64_t n_units = n_pages_used * a.n_kv;
     if (beside_compute && a.token0 == 0) {
         const int64_t n = n_pages_used * a.n_kv * (a.Ps / 8) * a.d8;
-        hipLaunchKernelGGL(kv_ingest_rows_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                           s, a, n);
+        const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
+        // Each workgroup reserves half the LDS an attention workgroup leaves
+        // free (the kernel itself uses none), so that at most two ingest
+        // workgroups, two wavefronts per SIMD, share a CU with the attention;
+        // registers alone would admit three.  With the attention's wavefronts
+        // issuing ahead of the ingest's, that is the count that moves the
+        // most bytes without lengthening the attention beside it.
+        const size_t attn = attention_lds_bytes(a.d);
+        const size_t lds = attn > 0 && attn < CU_LDS_BYTES ? (CU_LDS_BYTES - attn) / 2 : 0;
+        if (p2 && a.Ps >= 8 && a.G >= 8)
+            hipLaunchKernelGGL(kv_ingest_rows_kernel<true>, grid, dim3(kThreads), lds, s, a, n);
+        else
+            hipLaunchKernelGGL(kv_ingest_rows_kernel<false>, grid, dim3(kThreads), lds, s, a, n);
     } else {
         const int64_t n = a.num_tokens * 2 * a.n_kv * a.d8;   // 16-byte pieces of the payload
         const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
         if (p2) hipLaunchKernelGGL(kv_ingest_src_kernel<true>, grid, dim3(kThreads), 0, s, a, n);
         else hipLaunchKernelGGL(kv_ingest_src_kernel<false>, grid, dim3(kThreads), 0, s, a, n);
     }
-    (void)n_units;
     return hipGetLastError();
 }
 

@@ -192,3 +192,61 @@ def test_batch8_batched_pipeline_launch_at_full_size():
             err = assert_attention_close(got[li][rows], ref, f"batch8 request {r} layer {l}")
             print(f"  request {r} (T_p {wl.prefix_tokens[r]}) layer {l}: rows {len(rows)} "
                   f"max|err| {err[0]:.2e} rel L2 {err[1]:.2e}", flush=True)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("rate", [0.0, 12.5e9])
+def test_producer_pipeline_at_full_size(rate):
+    """The 8b-64k request through the host producer at full size: every
+    chunk object in host memory, each layer payload assembled from them,
+    landed in HBM (in spans of 32 MiB while it is produced, when capped at
+    12.5 GB/s; whole, uncapped), ingested (the second layer beside the first
+    layer's attention) and attended.  The two pool layers hold the workload's
+    first and last layers; the pool is compared bit for bit with the
+    oracle's scatter and the attention with the float64 oracle on 64 sampled
+    suffix rows and every head.  Capped, the run cannot end before the
+    producer's last byte is due at the cap."""
+    import torch
+    import paper_2605_22850_amd as oc
+    wl = kvgen.workload("8b-64k")
+    L, nq, nkv, d, G, Ps = (wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.chunk_tokens,
+                            wl.page_size)
+    layers = [0, L - 1]
+    n, tp, ts = wl.n_chunks(0), wl.prefix_tokens[0], wl.suffix_tokens[0]
+    print(f"[producer full size] 8b-64k rate {rate / 1e9:g} GB/s: T_p {tp}, T_s {ts}, pool {wl.pool_pages}",
+          flush=True)
+    layout = oc.Layout(2, nq, nkv, d, Ps, G, wl.pool_pages)
+    table = kvgen.block_tables(wl.seed, [wl.pages_needed(0)], wl.pool_pages)[0]
+    pool = torch.full((layout.pool_elems,), int(np.uint16(SENTINEL).view(np.int16)), dtype=torch.int16,
+                      device="cuda")
+    want_pool = np.full(oracle.pool_shape(2, wl.pool_pages, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+    sl = [kvgen.chunk_layer_slices(wl.seed, 0, l, n, wl.slice_elems) for l in layers]
+    for li in range(2):
+        oracle.ingest_layer(sl[li].reshape(-1), n, G, nkv, d, Ps, table, want_pool, li)
+    objects = np.ascontiguousarray(np.concatenate(sl, axis=1))          # object j: its two layer slices
+    q, kn, vn = [np.stack([kvgen.suffix_tensor(wl.seed, kind, 0, l, shape) for l in layers])
+                 for kind, shape in ((kvgen.KIND_Q, (ts, nq, d)), (kvgen.KIND_KNEW, (ts, nkv, d)),
+                                     (kvgen.KIND_VNEW, (ts, nkv, d)))]
+    req = oc.Request(tp, ts, torch.from_numpy(table).cuda(), to_dev(q, "bf16"), to_dev(kn, "bf16"),
+                     to_dev(vn, "bf16"), torch.zeros((2, ts, nq, d), dtype=torch.bfloat16, device="cuda"),
+                     chunk_objects=objects)
+    ctx = oc.oc_context_create(pool, layout, oc.OC_MODE_PRODUCER, tp, ts, rate_bytes_per_s=rate)
+    try:
+        stats = oc.oc_pipeline_run(ctx, [req], 2)
+    finally:
+        oc.oc_context_destroy(ctx)
+    torch.cuda.synchronize()
+    layer_bytes = tp * 2 * nkv * d * 2
+    if rate > 0:
+        due_ms = 2 * layer_bytes / rate * 1e3
+        print(f"  TTFT {stats[0]['ttft_ms']:.2f} ms, last byte due at {due_ms:.2f} ms", flush=True)
+        assert stats[0]["ttft_ms"] >= due_ms, "the producer delivered faster than its cap"
+    assert np.array_equal(from_dev(pool).reshape(want_pool.shape), want_pool), "pool differs from the oracle's"
+    del want_pool
+    rows = sample_rows(ts, seed=7)
+    got = from_dev(req.out)
+    for li, l in enumerate(layers):
+        k, v = oracle.logical_kv([np.ascontiguousarray(s) for s in sl[li]], G, nkv, d, 0)
+        ref = oracle.attention(q[li], k, v, kn[li], vn[li], rows=rows)
+        err = assert_attention_close(got[li][rows], ref, f"producer 8b-64k layer {l}")
+        print(f"  layer {l}: rows {len(rows)} max|err| {err[0]:.2e} rel L2 {err[1]:.2e}", flush=True)

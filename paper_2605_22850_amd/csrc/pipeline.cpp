@@ -120,6 +120,25 @@ static int start_threads(std::vector<std::thread> &pool, int n, F fn) {
     return (int)pool.size();
 }
 
+// Writes zeros over [p, p + bytes) from up to `threads` threads (the rest
+// on the calling thread if the system refuses more), faulting every page in.
+static void prefault(unsigned char *p, size_t bytes, int threads) {
+    const size_t part = (bytes + (size_t)threads - 1) / (size_t)threads;
+    std::vector<std::thread> pool;
+    size_t done = 0;
+    for (int i = 0; i < threads && done < bytes; ++i) {
+        const size_t len = std::min(part, bytes - done);
+        try {
+            pool.emplace_back([p, done, len] { std::memset(p + done, 0, len); });
+        } catch (...) {
+            break;
+        }
+        done += len;
+    }
+    if (done < bytes) std::memset(p + done, 0, bytes - done);
+    for (auto &t : pool) t.join();
+}
+
 // Stall and abort stop delivery at fault_layer; a short write still delivers.
 static inline bool stops_at(const oc_pipeline_opts &o, int32_t layer) {
     return (o.fault == OC_FAULT_STALL || o.fault == OC_FAULT_ABORT) && layer == o.fault_layer;
@@ -1323,6 +1342,16 @@ static int context_create_body(int device, const oc_kv_pool *kv_pool, const oc_p
                 hipMalloc(&s.device, c->slot_bytes) != hipSuccess)
                 return fail(OC_ENOMEM, "staging slot allocation failed");
         }
+        // Touch the ring once now, each pinned page by the host and each slot
+        // by one DMA: a fresh ring's first pass is otherwise several times
+        // slower (the producer's first copies into it, and the first DMAs
+        // from it), which would delay the first run's layers by tens of ms.
+        for (auto &s : c->slots) {
+            prefault(static_cast<unsigned char *>(s.pinned), c->slot_bytes, c->opts.producer_threads);
+            if (hipMemcpyAsync(s.device, s.pinned, c->slot_bytes, hipMemcpyHostToDevice, c->copy) != hipSuccess)
+                return fail(OC_EHIP, "staging slot warm-up copy failed");
+        }
+        if (hipStreamSynchronize(c->copy) != hipSuccess) return fail(OC_EHIP, "staging slot warm-up copy failed");
     }
     AttnPlan p;
     plan_attention(l, max_prefix_tokens, max_suffix_tokens, &p);

@@ -147,6 +147,9 @@ __device__ inline void src_order_piece(const IngestArgs &a, int64_t e, int64_t &
 // Ingest, one 16-byte piece per thread in payload order: every wavefront
 // reads 1 KiB of the payload contiguously and writes 256-byte rows into the
 // (page, head) blocks.  Many short wavefronts keep the most bytes in flight.
+// Every byte is read once and written once, so both sides bypass the L2's
+// normal retention (non-temporal): about 2.5 % faster alone than plain
+// accesses at the 8b-64k layer.
 // For whole chunk objects blockIdx.y is the layer.
 template <bool POW2>
 __global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, int64_t n_pieces) {
@@ -154,21 +157,23 @@ __global__ __launch_bounds__(kThreads) void kv_ingest_src_kernel(IngestArgs a, i
     if (e >= n_pieces) return;
     int64_t stage, pool;
     src_order_piece<POW2>(a, e, stage, pool);
-    const u32x4 v = *reinterpret_cast<const u32x4 *>(a.staging + stage);
-    *reinterpret_cast<u32x4 *>(a.pool_k + pool) = v;
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.staging + stage));
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(a.pool_k + pool));
 }
 
 // Gather (pool -> layer payload or whole chunk objects, the offload
 // direction): the same numbering, so every wavefront writes 1 KiB of the
-// output contiguously and reads 256-byte pool rows.
+// output contiguously and reads 256-byte pool rows; non-temporal on both
+// sides like the ingest (about 7 % faster than plain accesses over the
+// chunk objects of the 64K prefix).
 template <bool POW2>
 __global__ __launch_bounds__(kThreads) void kv_gather_src_kernel(IngestArgs a, uint16_t *out, int64_t n_pieces) {
     const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (e >= n_pieces) return;
     int64_t stage, pool;
     src_order_piece<POW2>(a, e, stage, pool);
-    const u32x4 v = *reinterpret_cast<const u32x4 *>(a.pool_k + pool);
-    *reinterpret_cast<u32x4 *>(out + stage) = v;
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.pool_k + pool));
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(out + stage));
 }
 
 // Suffix append: token i of k_new / v_new ([T_s][n_kv][d]; blockIdx.y picks

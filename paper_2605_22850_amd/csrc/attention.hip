@@ -588,24 +588,43 @@ __device__ __forceinline__ void combine_block(const float *ml_part, const float 
     if (gr >= (int64_t)nkv * rows) return;
     const int g = (int)(gr / rows);
     const int64_t row = gr - (int64_t)g * rows;
-    // the splits' partials are independent loads: unrolled, their latencies
-    // overlap instead of adding up split after split
+    // One pass over the splits, eight at a time: a group's (m, l) pairs and
+    // partial rows are independent loads issued together, so the merge waits
+    // on memory once per group rather than once for the maxima and again
+    // for the sums; the running maximum rescales what earlier groups added.
     const int64_t split_stride = (int64_t)nkv * rows_pad;
     const int64_t prow0 = (int64_t)g * rows_pad + row;
-    float M = -__builtin_inff();
-#pragma unroll 8
-    for (int s = 0; s < n_split; ++s) M = fmaxf(M, ml_part[(prow0 + s * split_stride) * 2]);
-    const float Mu = M == -__builtin_inff() ? 0.f : M;
+    constexpr int GS = 8;
+    float M = -__builtin_inff(), L = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    float L = 0.f;
-#pragma unroll 4
-    for (int s = 0; s < n_split; ++s) {
-        const int64_t prow = prow0 + s * split_stride;
-        const float2 ml = *reinterpret_cast<const float2 *>(ml_part + prow * 2);
-        const f32x4 o = *reinterpret_cast<const f32x4 *>(o_part + prow * D + c4 * 4);
-        const float w = __builtin_amdgcn_exp2f(ml.x - Mu);
-        L += w * ml.y;
-        acc += w * o;
+    for (int s0 = 0; s0 < n_split; s0 += GS) {
+        float2 ml[GS];
+        f32x4 o[GS];
+#pragma unroll
+        for (int i = 0; i < GS; ++i) {
+            if (s0 + i < n_split) {
+                const int64_t prow = prow0 + (int64_t)(s0 + i) * split_stride;
+                ml[i] = *reinterpret_cast<const float2 *>(ml_part + prow * 2);
+                o[i] = *reinterpret_cast<const f32x4 *>(o_part + prow * D + c4 * 4);
+            }
+        }
+        float Mg = M;
+#pragma unroll
+        for (int i = 0; i < GS; ++i)
+            if (s0 + i < n_split) Mg = fmaxf(Mg, ml[i].x);
+        const float Mu = Mg == -__builtin_inff() ? 0.f : Mg;
+        const float r = __builtin_amdgcn_exp2f(M - Mu);     // 0 while nothing has been added
+        L *= r;
+        acc *= r;
+#pragma unroll
+        for (int i = 0; i < GS; ++i) {
+            if (s0 + i < n_split) {
+                const float w = __builtin_amdgcn_exp2f(ml[i].x - Mu);
+                L += w * ml[i].y;
+                acc += w * o[i];
+            }
+        }
+        M = Mg;
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
     const int64_t tok = row / grp;

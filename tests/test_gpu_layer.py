@@ -253,3 +253,40 @@ def test_random_shapes_ingest_and_attention(i):
     torch.cuda.synchronize()
     assert np.array_equal(from_dev(c.d_pool).reshape(c.pool_shape()), c.expected_pool())
     assert_attention_close(from_dev(out), c.expected_attention(), f"random {i}")
+
+
+# (G, Ps, n_chunks, nkv, d): page sizes other than 16 (any multiple of 8 is a
+# valid pool for the data-movement entry points; only the attention needs 16),
+# chunks smaller than, equal to, larger than and straddling a page
+PAGE_SIZE_CASES = [(8, 8, 23, 2, 64), (16, 8, 11, 8, 128), (24, 8, 7, 2, 128), (8, 24, 29, 2, 64),
+                   (16, 24, 13, 8, 128), (48, 24, 5, 4, 64), (16, 32, 17, 8, 128), (8, 32, 31, 1, 64),
+                   (64, 32, 4, 2, 128), (40, 48, 6, 8, 128)]
+
+
+@pytest.mark.parametrize("G,Ps,n,nkv,d", PAGE_SIZE_CASES)
+def test_page_sizes_ingest_gather_append(G, Ps, n, nkv, d):
+    """Ingest (whole pool bit for bit against the oracle's scatter), the
+    gather back into the layer payload, and the suffix append behind the
+    prefix (against the oracle's append), for a pool of Ps-slot pages."""
+    import torch
+    import kvgen
+    import oracle
+    from paper_2605_22850_amd import oc_kv_layer_gather, oc_kv_suffix_append
+    Ts, L, layer = 21, 2, 1
+    Tp = n * G
+    need = -(-(Tp + Ts) // Ps)
+    P = need + 5
+    print(f"[page sizes] G {G} Ps {Ps} chunks {n} nkv {nkv} d {d}", flush=True)
+    table = kvgen.block_tables(Ps * 1000 + G, [need], P)[0]
+    c = LayerCase(2 * nkv, nkv, d, G, Ps, n, Ts, P, L, layer, seed=G * 7 + Ps, table=table).upload()
+    c.run_ingest()
+    torch.cuda.synchronize()
+    want = c.expected_pool()
+    assert np.array_equal(from_dev(c.d_pool).reshape(c.pool_shape()), want), "pool differs after the ingest"
+    back = torch.zeros_like(c.d_staging)
+    oc_kv_layer_gather(c.d_table, Tp, c.d_pool, c.layout, layer, back, n)
+    oc_kv_suffix_append(c.d_k, c.d_v, Ts, c.d_table, Tp, c.d_pool, c.layout, layer)
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(back), c.staging), "gather is not the inverse of the ingest"
+    oracle.append_suffix(c.k_new, c.v_new, Tp, c.table, want, layer, Ps)
+    assert np.array_equal(from_dev(c.d_pool).reshape(c.pool_shape()), want), "pool differs after the append"

@@ -96,6 +96,10 @@ def _numpy_scatter(staging, n_chunks, G, nkv, d, Ps, table, pool, layer):
     (8, 16, 5, 2, 8),        # two chunks per page, last page half full
     (32, 16, 3, 1, 16),      # two pages per chunk
     (16, 16, 1, 8, 128),     # Llama-shaped page
+    (8, 8, 7, 2, 16),        # page of 8 slots
+    (16, 24, 5, 2, 8),       # page size not a power of two, chunks straddle pages
+    (40, 24, 3, 1, 16),      # chunks longer than a page, neither divides the other
+    (8, 32, 9, 4, 8),        # four chunks per page, last page partial
 ])
 def test_ingest_matches_numpy_formulation(G, Ps, n_chunks, nkv, d):
     rng = np.random.default_rng(7)

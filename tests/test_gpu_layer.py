@@ -257,17 +257,21 @@ def test_random_shapes_ingest_and_attention(i):
 
 # (G, Ps, n_chunks, nkv, d): page sizes other than 16 (any multiple of 8 is a
 # valid pool for the data-movement entry points; only the attention needs 16),
-# chunks smaller than, equal to, larger than and straddling a page
+# chunks smaller than, equal to, larger than and straddling a page; and head
+# sizes the attention does not take (any multiple of 8 moves the same way),
+# power-of-two and not, with odd KV-head counts
 PAGE_SIZE_CASES = [(8, 8, 23, 2, 64), (16, 8, 11, 8, 128), (24, 8, 7, 2, 128), (8, 24, 29, 2, 64),
                    (16, 24, 13, 8, 128), (48, 24, 5, 4, 64), (16, 32, 17, 8, 128), (8, 32, 31, 1, 64),
-                   (64, 32, 4, 2, 128), (40, 48, 6, 8, 128)]
+                   (64, 32, 4, 2, 128), (40, 48, 6, 8, 128),
+                   (16, 16, 9, 3, 96), (16, 16, 7, 2, 256), (32, 16, 5, 5, 32), (8, 16, 13, 1, 8)]
 
 
 @pytest.mark.parametrize("G,Ps,n,nkv,d", PAGE_SIZE_CASES)
 def test_page_sizes_ingest_gather_append(G, Ps, n, nkv, d):
     """Ingest (whole pool bit for bit against the oracle's scatter), the
     gather back into the layer payload, and the suffix append behind the
-    prefix (against the oracle's append), for a pool of Ps-slot pages."""
+    prefix (against the oracle's append), for a pool of Ps-slot pages and
+    d-element head rows."""
     import torch
     import kvgen
     import oracle

@@ -153,3 +153,51 @@ def test_chunkwise_delivery_validation():
         assert b"chunkwise" in str(e.value).encode()
     finally:
         oc.oc_context_destroy(ctx)
+
+
+# (G, Ps, n_chunks, nkv, d, L): whole chunk objects into pools whose pages are
+# not 16 slots, or whose head rows the attention does not take
+OBJECT_SHAPE_CASES = [(8, 24, 17, 2, 64, 3), (40, 8, 5, 3, 96, 2), (16, 32, 9, 8, 128, 4), (24, 48, 6, 1, 256, 2)]
+
+
+@pytest.mark.parametrize("G,Ps,n,nkv,d,L", OBJECT_SHAPE_CASES)
+def test_chunk_objects_at_other_page_and_head_sizes(G, Ps, n, nkv, d, L):
+    """Every layer of whole chunk objects in one call, first all of them and
+    then a range starting mid-prefix on a fresh pool: the pool equals the
+    oracle's per-layer scatter bit for bit, and the offload gather of the
+    same range returns the stored objects."""
+    import torch
+    import kvgen
+    import oracle
+    import paper_2605_22850_amd as oc
+    print(f"[chunk objects] G {G} Ps {Ps} chunks {n} nkv {nkv} d {d} L {L}", flush=True)
+    Tp = n * G
+    need = -(-Tp // Ps)
+    P = need + 3
+    slice_elems = 2 * G * nkv * d
+    objs = kvgen.chunk_objects(Ps * 31 + G, 0, L, n, slice_elems)          # [n][L][S/2]
+    table = kvgen.block_tables(Ps * 31 + G, [need], P)[0]
+    layout = oc.Layout(L, 2 * nkv, nkv, d, Ps, G, P)
+    d_table = torch.from_numpy(table.copy()).cuda()
+    for first, count in ((0, n), (n // 3, n - n // 3 - 1)):
+        pool = torch.full((layout.pool_elems,), int(np.uint16(SENTINEL).view(np.int16)), dtype=torch.int16,
+                          device="cuda")
+        want = np.full(oracle.pool_shape(L, P, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+        part = np.ascontiguousarray(objs[first:first + count])
+        for l in range(L):
+            # the oracle scatters the range as the layer payload of chunks first .. first+count-1:
+            # its tokens start at first * G, so it runs over a table shifted by those tokens' pages
+            full = np.full((n, slice_elems), 0, dtype=np.uint16)
+            full[first:first + count] = part[:, l, :]
+            ref = np.full(oracle.pool_shape(L, P, nkv, Ps, d), SENTINEL, dtype=np.uint16)
+            oracle.ingest_layer(full.reshape(-1), n, G, nkv, d, Ps, table, ref, l)
+            # keep only the slots of tokens first*G .. (first+count)*G - 1
+            for T in range(first * G, (first + count) * G):
+                page, slot = table[T // Ps], T % Ps
+                want[l, :, page, :, slot * d:(slot + 1) * d] = ref[l, :, page, :, slot * d:(slot + 1) * d]
+        oc.oc_kv_chunks_ingest(to_dev(part.reshape(-1)), count, first, d_table, Tp, pool, layout)
+        out = torch.empty(count * L * slice_elems, dtype=torch.int16, device="cuda")
+        oc.oc_kv_chunks_gather(d_table, Tp, pool, layout, first, count, out)
+        torch.cuda.synchronize()
+        assert np.array_equal(from_dev(pool).reshape(want.shape), want), f"pool differs (chunks {first}+{count})"
+        assert np.array_equal(from_dev(out).reshape(part.shape), part), f"gather differs (chunks {first}+{count})"

@@ -175,7 +175,10 @@ size_t oc_attention_workspace_bytes(const oc_layout *layout, int64_t prefix_toke
  * [suffix_tokens][n_kv][d]; bfloat16, 16-byte aligned.  Scores and
  * accumulation are fp32; out is rounded to bfloat16 (nearest even).
  * workspace: device, at least oc_attention_workspace_bytes(), 256-byte
- * aligned.  suffix_tokens >= 1.  Asynchronous on `stream`. */
+ * aligned.  suffix_tokens >= 1.  Asynchronous on `stream`.  The kernel's
+ * wavefronts raise their issue priority (s_setprio 1, 2 in the matrix
+ * phases), so kernels at the default priority that share its compute units,
+ * such as the pipeline's ingest, issue after it. */
 int oc_suffix_prefill_layer(const void *q, const void *k_new, const void *v_new,
                             int64_t suffix_tokens, const oc_kv_pool *kv_pool,
                             const oc_block_table *block_table, int32_t layer, void *out,

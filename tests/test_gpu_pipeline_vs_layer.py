@@ -124,3 +124,22 @@ def test_batched_layer_launch(name):
 
 def _f64(bits):
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.timeout(300)
+def test_more_requests_than_one_launch_takes():
+    # 17 requests, one more than a batched launch holds: the pipeline falls
+    # back to one attention launch per request, and every request still
+    # matches the oracle on every row of every layer
+    import paper_2605_22850_amd as oc
+    n = 17
+    pre, suf = [128 + 16 * i for i in range(n)], [5 + i for i in range(n)]
+    print(f"[batched] {n} requests", flush=True)
+    rs = RequestSet(2, 8, 2, 64, pre, suf, 1024, seed=17).upload(with_payload=True)
+    stats = _run(rs, oc.OC_MODE_DEVICE_STAGED)
+    assert np.array_equal(from_dev(rs.d_pool).reshape(rs.pool_shape()), rs.expected_pool()), "ingest"
+    assert len({st["done_ms"][1] for st in stats}) > 1, "17 requests cannot share one launch"
+    for r in range(n):
+        out = from_dev(rs.reqs[r].out)
+        for l in range(2):
+            assert_attention_close(out[l], rs.expected_out(r, l), f"request {r} layer {l}")

@@ -121,8 +121,13 @@ static int start_threads(std::vector<std::thread> &pool, int n, F fn) {
 }
 
 // Writes zeros over [p, p + bytes) from up to `threads` threads (the rest
-// on the calling thread if the system refuses more), faulting every page in.
+// on the calling thread if the system refuses more), faulting every page in;
+// a ring under 64 MiB per slot is written by the calling thread alone.
 static void prefault(unsigned char *p, size_t bytes, int threads) {
+    if (bytes < ((size_t)64 << 20) || threads <= 1) {
+        std::memset(p, 0, bytes);
+        return;
+    }
     const size_t part = (bytes + (size_t)threads - 1) / (size_t)threads;
     std::vector<std::thread> pool;
     size_t done = 0;
